@@ -1,0 +1,198 @@
+"""CPU oracle for the fused Indexer-TopK operation.
+
+TEST INFRASTRUCTURE ONLY. The library never imports, links or calls this
+module; only the test suite, the smoke check and the benchmark's CPU-baseline
+leg do. It shares no code with the GPU path.
+
+What it computes is the plain definition of the operation, with none of the
+method's performance devices (sampling, binning, thresholds, candidate
+buffers): those cannot change an exact top-k, so the oracle leaves them out.
+
+* Index score -- Eq. (1), sec. 2.1 (DSA indexer):
+      I[t, s] = sum_j w[t, j] * ReLU(q[t, j] . k[s])
+  evaluated in float64 from exactly dequantised inputs, then rounded once to
+  float32 (round to nearest even).
+* Inner-product score -- the k-NN case of sec. 3.1 (Eq. 2 with f an inner
+  product, sec. 3.2 "inner-product-based" scorers): the same sum without the
+  ReLU; with one head and unit weights it is q . k.
+* Exact top-k -- Eq. (2), sec. 3.1: for every query the k visible keys with the
+  highest score. The paper requires exactness (sec. 3.1 "exactly identify",
+  sec. 3.2 "preserving exact Top-k correctness") but does not say how ties are
+  broken; this oracle makes the answer unique with one total order:
+      higher score first; -0.0 equals +0.0; NaN ranks below -inf;
+      equal scores -> lower key index first.
+  Rows with fewer than k visible keys return all of them, then padding
+  (index -1, score -inf).
+* Visibility -- the query chunk attends to the preceding context (sec. 1, the
+  DSA prefill description): row t sees keys [0, e_t) with
+  e_t = clamp(causal_offsets[t], 0, Nk), or all Nk keys when no offsets are
+  given.
+* fp8 inputs are OCP E4M3FN bytes (decoded here from the format definition:
+  1 sign bit, 4 exponent bits with bias 7, 3 mantissa bits, no infinities,
+  S.1111.111 is NaN) times a positive float32 per-token scale; the product is
+  exact in float64.
+* bf16 inputs are the upper 16 bits of a float32.
+"""
+from __future__ import annotations
+
+from typing import Optional, Sequence, Tuple
+
+import numpy as np
+
+PAD_INDEX = -1
+PAD_SCORE = np.float32(-np.inf)
+
+
+# ----------------------------------------------------------------------------
+# Decoding of the storage formats
+# ----------------------------------------------------------------------------
+
+def bf16_to_f64(bits: np.ndarray) -> np.ndarray:
+    """bfloat16 bit patterns (uint16) -> float64 (exact)."""
+    b = np.asarray(bits).astype(np.uint32) << np.uint32(16)
+    return b.view(np.float32).astype(np.float64)
+
+
+def e4m3fn_to_f64(bits: np.ndarray) -> np.ndarray:
+    """OCP FP8 E4M3FN bit patterns (uint8) -> float64 (exact)."""
+    b = np.asarray(bits).astype(np.int64)
+    sign = np.where((b >> 7) & 1, -1.0, 1.0)
+    e = (b >> 3) & 0xF
+    m = (b & 0x7).astype(np.float64)
+    normal = (1.0 + m / 8.0) * np.exp2(e.astype(np.float64) - 7.0)
+    subnormal = (m / 8.0) * np.exp2(-6.0)
+    mag = np.where(e == 0, subnormal, normal)
+    mag = np.where((e == 15) & ((b & 0x7) == 7), np.nan, mag)
+    return sign * mag
+
+
+def dequantize(x: np.ndarray, dtype: str, scale: Optional[np.ndarray] = None) -> np.ndarray:
+    """Storage array -> float64 values.
+
+    dtype "f32": x is float32; "bf16": x is uint16 bit patterns; "fp8": x is
+    uint8 E4M3FN bit patterns and ``scale`` (float32, broadcast over the last
+    axis) multiplies every value."""
+    if dtype == "f32":
+        v = np.asarray(x, dtype=np.float32).astype(np.float64)
+    elif dtype == "bf16":
+        v = bf16_to_f64(x)
+    elif dtype == "fp8":
+        v = e4m3fn_to_f64(x)
+    else:
+        raise ValueError(dtype)
+    if scale is not None:
+        v = v * np.asarray(scale, dtype=np.float32).astype(np.float64)[..., None]
+    return v
+
+
+def visible_counts(causal_offsets: Optional[np.ndarray], nq: int, nk: int) -> np.ndarray:
+    """e_t for every row (see the module docstring)."""
+    if causal_offsets is None:
+        return np.full(nq, nk, dtype=np.int64)
+    return np.clip(np.asarray(causal_offsets, dtype=np.int64), 0, nk)
+
+
+# ----------------------------------------------------------------------------
+# Scores -- Eq. (1)
+# ----------------------------------------------------------------------------
+
+def row_scores(q_row: np.ndarray, w_row: Optional[np.ndarray], keys: np.ndarray, mode: str) -> np.ndarray:
+    """Scores of one query against every row of ``keys``.
+
+    q_row [H, d] float64, w_row [H] float64 or None (unit weights), keys [n, d]
+    float64. Returns float32 [n]: the float64 value of Eq. (1) (mode "dsa") or
+    of the weighted inner product (mode "ip"), rounded once to float32."""
+    x = q_row @ keys.T                      # [H, n]: per-head q_{t,j} . k_s
+    if mode == "dsa":
+        x = np.maximum(x, 0.0)              # ReLU of each head's dot product
+    elif mode != "ip":
+        raise ValueError(mode)
+    w = np.ones(q_row.shape[0]) if w_row is None else w_row
+    return (w @ x).astype(np.float32)       # weighted sum over heads, one rounding
+
+
+def index_scores(q: np.ndarray, w: Optional[np.ndarray], keys: np.ndarray, mode: str,
+                 rows: Optional[Sequence[int]] = None, ncols: Optional[int] = None) -> np.ndarray:
+    """Dense float32 score matrix [len(rows), ncols] for dequantised float64
+    inputs q [Nq, H, d], w [Nq, H] (or None), keys [Nk, d]. Every column is
+    scored, visible or not."""
+    rows = range(q.shape[0]) if rows is None else rows
+    ncols = keys.shape[0] if ncols is None else ncols
+    out = np.empty((len(rows), ncols), dtype=np.float32)
+    for i, t in enumerate(rows):
+        out[i] = row_scores(q[t], None if w is None else w[t], keys[:ncols], mode)
+    return out
+
+
+# ----------------------------------------------------------------------------
+# Exact selection -- Eq. (2)
+# ----------------------------------------------------------------------------
+
+def order(scores: np.ndarray) -> np.ndarray:
+    """Indices of ``scores`` (float32, 1-D) sorted by the oracle's total order:
+    score descending, NaN last, -0.0 == +0.0, ties by ascending index."""
+    s = np.asarray(scores, dtype=np.float32).astype(np.float64)
+    nan = np.isnan(s)
+    neg = np.where(nan, 0.0, -s)            # -(-0.0) == 0.0 == -(+0.0) compare equal
+    idx = np.arange(s.size)
+    # lexsort: last key is primary; stable, so equal keys keep index order.
+    return np.lexsort((idx, neg, nan))
+
+
+def select_row(scores: np.ndarray, e: int, k: int) -> Tuple[np.ndarray, np.ndarray]:
+    """Exact top-k of the visible prefix scores[:e] of one row.
+
+    Returns (idx int32 [k], score float32 [k]) sorted by the total order, with
+    min(k, e) real entries followed by padding (-1, -inf)."""
+    vis = np.asarray(scores[:e], dtype=np.float32)
+    o = order(vis)[:k]
+    idx = np.full(k, PAD_INDEX, dtype=np.int32)
+    sc = np.full(k, PAD_SCORE, dtype=np.float32)
+    idx[:o.size] = o
+    sc[:o.size] = vis[o]
+    return idx, sc
+
+
+def topk_select(scores: np.ndarray, nk: int, k: int, causal_offsets: Optional[np.ndarray] = None,
+                rows: Optional[Sequence[int]] = None) -> Tuple[np.ndarray, np.ndarray]:
+    """Scores-in selection: exact top-k of every requested row of a float32
+    score matrix whose first ``nk`` columns are keys."""
+    nq = scores.shape[0]
+    rows = list(range(nq)) if rows is None else list(rows)
+    e = visible_counts(causal_offsets, nq, nk)
+    out_i = np.empty((len(rows), k), dtype=np.int32)
+    out_s = np.empty((len(rows), k), dtype=np.float32)
+    for i, t in enumerate(rows):
+        out_i[i], out_s[i] = select_row(scores[t, :nk], int(e[t]), k)
+    return out_i, out_s
+
+
+def indexer_topk(q: np.ndarray, q_dtype: str, q_scale: Optional[np.ndarray], w: Optional[np.ndarray],
+                 keys: np.ndarray, k_scale: Optional[np.ndarray], k: int, mode: str = "dsa",
+                 causal_offsets: Optional[np.ndarray] = None, rows: Optional[Sequence[int]] = None,
+                 return_scores: bool = False):
+    """Fused operation, defined plainly: Eq. (1) scores for the visible keys of
+    each requested row, then the exact top-k of Eq. (2).
+
+    q [Nq, H, d] and keys [Nk, d] in storage form (float32 / uint16 bf16 bits /
+    uint8 E4M3FN bits, all with the same ``q_dtype``); q_scale [Nq, H] and
+    k_scale [Nk] for fp8; w [Nq, H] float32 or None. Returns (idx, scores)
+    [len(rows), k], plus the full per-row float32 score rows when
+    ``return_scores``."""
+    nq, nk = q.shape[0], keys.shape[0]
+    rows = list(range(nq)) if rows is None else list(rows)
+    e = visible_counts(causal_offsets, nq, nk)
+    kd = dequantize(keys, q_dtype, k_scale)
+    wd = None if w is None else np.asarray(w, dtype=np.float32).astype(np.float64)
+    out_i = np.empty((len(rows), k), dtype=np.int32)
+    out_s = np.empty((len(rows), k), dtype=np.float32)
+    full = []
+    for i, t in enumerate(rows):
+        qd = dequantize(q[t], q_dtype, None if q_scale is None else q_scale[t])
+        s = row_scores(qd, None if wd is None else wd[t], kd[: e[t]], mode)
+        out_i[i], out_s[i] = select_row(s, int(e[t]), k)
+        if return_scores:
+            full.append(s)
+    if return_scores:
+        return out_i, out_s, full
+    return out_i, out_s
