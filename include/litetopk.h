@@ -1,0 +1,194 @@
+/*
+ * litetopk.h -- C ABI of the MI355X (gfx950) fused Indexer-TopK library.
+ *
+ * The library scores every causally visible key for every query with the DSA
+ * indexer score and returns the exact per-row top-k, following the paper's
+ * sample -> filter (bin, gate, online threshold refresh, batched write-back)
+ * -> select workflow (sec. 3.1 "Overview", sec. 3.2), with an exact fallback
+ * for rows whose candidate buffer overflows.
+ *
+ * Conventions shared by every entry point
+ *  - Every array argument is a DEVICE pointer owned by the caller. The library
+ *    never allocates or frees device memory, never synchronises the device or
+ *    the stream, and keeps no state between calls: all scratch lives in the
+ *    caller's workspace. Calls on different streams with different
+ *    workspaces may run concurrently.
+ *  - `stream` is a hipStream_t passed as an opaque pointer (NULL = the null
+ *    stream). All work is enqueued on it in order; the call returns before the
+ *    work finishes.
+ *  - Argument checks happen on the host before anything is enqueued; a
+ *    failing check returns a negative status and enqueues nothing. Device-side
+ *    data problems (NaN or infinite scores) are not errors: they follow the
+ *    total order below.
+ *  - Total order used for selection (Eq. 2 of sec. 3.1 leaves ties open):
+ *    higher score first; -0.0 equals +0.0; NaN ranks below -inf; equal scores
+ *    go to the lower key index. The selected SET is therefore unique.
+ *  - Output rows: row t holds min(k, e_t) selected entries followed by padding
+ *    (index -1, score -inf). e_t = clamp(causal_offsets[t], 0, num_keys), or
+ *    num_keys when causal_offsets is NULL: row t sees keys [0, e_t). Scores are
+ *    the raw float32 index scores I (never bin-space values). Without
+ *    LT_SORTED_OUTPUT the selected entries come in an unspecified but
+ *    deterministic order (the paper's select writes the above-threshold bins
+ *    directly, sec. 3.2 "Top-k Selection"); with it they are sorted by the
+ *    total order.
+ */
+#ifndef LITETOPK_H
+#define LITETOPK_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* ---- status codes ------------------------------------------------------ */
+#define LT_OK 0
+#define LT_EINVAL (-1)        /* bad pointer, size, stride, alignment or option   */
+#define LT_EUNSUPPORTED (-2)  /* (dtype, heads, head_dim) not built, or k > LT_K_MAX */
+#define LT_EWORKSPACE (-3)    /* workspace smaller than the *_workspace_size value */
+#define LT_EHIP (-4)          /* a HIP launch or event call failed                 */
+
+#define LT_K_MAX 8192         /* largest k (the paper's largest, sec. 4.1 retrieval) */
+#define LT_MAX_BINS 256
+
+/* ---- enums --------------------------------------------------------------- */
+typedef enum {
+  LT_F32 = 0,         /* float32                                            */
+  LT_BF16 = 1,        /* bfloat16                                           */
+  LT_FP8_E4M3FN = 2   /* OCP FP8 E4M3FN bytes with per-token float32 scales */
+} lt_dtype;
+
+typedef enum {
+  /* Eq. (1), sec. 2.1: I[t,s] = sum_j w[t,j] * ReLU(q[t,j] . k[s]) */
+  LT_SCORE_DSA = 0,
+  /* inner-product scorer (k-NN, sec. 3.1): I[t,s] = sum_j w[t,j] * (q[t,j] . k[s]) */
+  LT_SCORE_IP = 1
+} lt_score_mode;
+
+/* flags for lt_options.flags */
+#define LT_SORTED_OUTPUT 1u   /* sort every output row by the total order          */
+#define LT_FORCE_FALLBACK 2u  /* send every row through the exact fallback path    */
+
+/* Stage boundaries recorded into lt_options.stage_events when it is non-NULL:
+   event i is recorded on `stream` before stage i, the last one after the last
+   stage, so elapsed(event[i], event[i+1]) is the device time of stage i. */
+#define LT_STAGE_SAMPLE 0     /* score / read the sample keys                  */
+#define LT_STAGE_RANGE 1      /* per-row range, bin width and initial threshold */
+#define LT_STAGE_FILTER 2     /* fused score + gate + write-back scan           */
+#define LT_STAGE_SELECT 3     /* final selection from the candidate buffers     */
+#define LT_STAGE_FALLBACK 4   /* exact fallback for overflowed rows             */
+#define LT_NUM_STAGE_EVENTS 6
+
+/* Tuning knobs. Pass NULL for the defaults; otherwise start from
+   lt_options_default() and change fields. None of them changes a result. */
+typedef struct lt_options {
+  int32_t num_bins;        /* m, equal-width bins over the sample range (sec. 3.2
+                              "Sampling"); 1..LT_MAX_BINS; default 256          */
+  int32_t sample_size;     /* k': sampled keys per launch (sec. 3.2: k' = 3k for
+                              DSA); negative = default: 3k in DSA mode,
+                              max(3k, min(Nk/64, 65536)) in IP mode (the scores-in
+                              entry uses 3k); 0 disables the gate                */
+  int32_t capacity;        /* candidate slots per (row, key split); <= 0 = default
+                              max(12k, 2048) (sec. 4.2: 12k for k = 2048)       */
+  int32_t key_splits;      /* key-range splits per row in the fused scan; 0 = auto */
+  int32_t refresh_tiles;   /* key tiles between threshold refreshes; 0 = default */
+  uint32_t flags;          /* LT_SORTED_OUTPUT | LT_FORCE_FALLBACK               */
+  uint64_t seed;           /* seed of the key sample                             */
+  void** stage_events;     /* NULL, or LT_NUM_STAGE_EVENTS hipEvent_t handles     */
+  int32_t* row_stats;      /* NULL, or a DEVICE int32 [num_queries, 4] receiving per
+                              row: {candidates written (summed over splits),
+                              final threshold bin, fallback reason (0 none,
+                              1 buffer overflow, 2 threshold-bin overflow,
+                              3 forced), candidates in the threshold bin}       */
+} lt_options;
+
+/* Fills *opts with the defaults (k-dependent fields are resolved per call). */
+void lt_options_default(lt_options* opts);
+
+/* ---- fused Indexer-TopK ------------------------------------------------- */
+
+/* Bytes of device workspace lt_indexer_topk needs for this shape. Returns 0
+   for an invalid or unsupported shape. */
+size_t lt_indexer_topk_workspace_size(int32_t num_queries, int32_t num_keys, int32_t num_heads,
+                                      int32_t head_dim, lt_dtype dtype, lt_score_mode mode,
+                                      int32_t k, const lt_options* opts);
+
+/* Exact per-row top-k of the index score (Eq. 1 for LT_SCORE_DSA, the inner
+   product for LT_SCORE_IP) over the visible keys, Eq. (2), computed by the
+   fused sample / filter / select pipeline of sec. 3.2 without materialising
+   the score matrix.
+
+   q         [num_queries, num_heads, head_dim] in `dtype`, row-major (for fp8:
+             E4M3FN bytes). 16-byte aligned.
+   q_scale   [num_queries, num_heads] float32 > 0, fp8 only (NULL otherwise).
+   w         [num_queries, num_heads] float32 head weights w[t,j]; NULL = all 1.
+   keys      [num_keys, head_dim] in `dtype`, row-major. 16-byte aligned.
+   k_scale   [num_keys] float32 > 0, fp8 only (NULL otherwise).
+             For fp8 the scales multiply the decoded values; they must be
+             positive so that they factor out of the ReLU.
+   k         1..LT_K_MAX.
+   causal_offsets  [num_queries] int32 or NULL (see the row convention above).
+   out_idx   [num_queries, k] int32;  out_scores [num_queries, k] float32.
+   workspace at least lt_indexer_topk_workspace_size(...) bytes, 256-byte aligned;
+             its contents on entry do not matter.
+   Supported (dtype, mode, num_heads, head_dim): f32 DSA (4, 64), f32 DSA and IP
+   (1, 64); bf16 DSA (64, 128), bf16 DSA (4, 128), bf16 DSA and IP (1, 128);
+   fp8 DSA (64, 128). Anything else returns LT_EUNSUPPORTED. */
+int lt_indexer_topk(const void* q, const float* q_scale, const float* w, const void* keys,
+                    const float* k_scale, lt_dtype dtype, lt_score_mode mode, int32_t num_queries,
+                    int32_t num_keys, int32_t num_heads, int32_t head_dim, int32_t k,
+                    const int32_t* causal_offsets, int32_t* out_idx, float* out_scores,
+                    void* workspace, size_t workspace_bytes, const lt_options* opts, void* stream);
+
+/* ---- dense scores (the decoupled baseline's score stage, sec. 1) --------- */
+
+/* Writes the float32 index score of every (query, key) pair, visible or not,
+   to scores[t * ld + s] for s < num_keys (ld >= num_keys). Same arguments and
+   supported shapes as lt_indexer_topk; the arithmetic is bit-identical to the
+   fused scan's, so lt_topk_select over this matrix returns exactly what
+   lt_indexer_topk returns. This is the materialising path the paper's
+   method exists to avoid; it serves as the unfused baseline and for tests. */
+int lt_indexer_scores(const void* q, const float* q_scale, const float* w, const void* keys,
+                      const float* k_scale, lt_dtype dtype, lt_score_mode mode,
+                      int32_t num_queries, int32_t num_keys, int32_t num_heads, int32_t head_dim,
+                      float* scores, int64_t ld, void* stream);
+
+/* ---- scores-in selection --------------------------------------------------- */
+
+size_t lt_topk_select_workspace_size(int32_t num_queries, int32_t num_keys, int32_t k,
+                                     const lt_options* opts);
+
+/* Exact per-row top-k (Eq. 2) of a float32 score matrix: scores[t * row_stride
+   + s], s < num_keys (row_stride >= num_keys, 16-byte aligned rows, i.e.
+   row_stride % 4 == 0). Uses the same sample / bin / gate / refresh / select
+   pipeline as the fused entry, streaming the scores from HBM once. Bit-exact:
+   the output entries are input values, chosen under the total order. */
+int lt_topk_select(const float* scores, int64_t row_stride, int32_t num_queries, int32_t num_keys,
+                   int32_t k, const int32_t* causal_offsets, int32_t* out_idx, float* out_scores,
+                   void* workspace, size_t workspace_bytes, const lt_options* opts, void* stream);
+
+/* Exact per-row top-k of a float32 score matrix by plain radix selection over
+   all visible scores, with no sampling or filtering (the decoupled designs'
+   selector, sec. 1 and sec. 3.2 "Top-k Selection"). Needs no workspace.
+   `flags` accepts LT_SORTED_OUTPUT. Same layout rules as lt_topk_select. */
+int lt_topk_radix(const float* scores, int64_t row_stride, int32_t num_queries, int32_t num_keys,
+                  int32_t k, const int32_t* causal_offsets, int32_t* out_idx, float* out_scores,
+                  uint32_t flags, void* stream);
+
+/* ---- timing helpers ------------------------------------------------------- */
+
+/* Thin wrappers over hipEventCreate / hipEventDestroy / hipEventElapsedTime /
+   hipEventRecord / hipEventSynchronize for callers without a HIP binding. */
+int lt_event_create(void** event);
+int lt_event_destroy(void* event);
+int lt_event_record(void* event, void* stream);
+int lt_event_elapsed_ms(void* start, void* stop, float* ms);  /* synchronises on stop */
+
+/* Human-readable text for a status code. */
+const char* lt_strerror(int status);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* LITETOPK_H */

@@ -1,0 +1,330 @@
+// C ABI of the library (include/litetopk.h): argument checks, option
+// resolution, workspace carving and the stream-ordered launch sequence.
+#include <string.h>
+
+#include <algorithm>
+
+#include "internal.hpp"
+#include "select_dev.hpp"
+
+using namespace lt;
+
+namespace {
+
+constexpr int kDefaultBins = 256;
+constexpr int kDefaultRefreshTiles = 4;     // fused scan: key tiles between refreshes
+constexpr int kDefaultRefreshChunks = 4;    // scores-in scan: 256-key chunks between refreshes
+constexpr int kFallbackGridFused = 64;      // rows re-scored concurrently (scratch rows)
+constexpr int kFallbackGridScores = 256;
+constexpr int kTargetBlocks = 256;          // one block per CU before key splitting stops
+constexpr size_t kHistLdsBudget = 96 * 1024;
+constexpr int kSampleBlockScores = 64;      // scores-in sample: runs of 64 consecutive keys
+
+inline size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
+
+struct Resolved {
+  int m, ns, cap, S, L, refresh, E;
+  uint32_t flags;
+  uint64_t seed;
+  void** ev;
+  int32_t* stats;
+};
+
+struct Layout {
+  size_t qctl, queue, params, samp, cnt, hist, cand, scratch, total;
+};
+
+Layout carve(int nq, int nk, const Resolved& r, bool fused) {
+  Layout L{};
+  size_t off = 0;
+  auto take = [&](size_t bytes) {
+    size_t o = off;
+    off = align256(off + bytes);
+    return o;
+  };
+  L.qctl = take(256);
+  L.queue = take((size_t)nq * 4);
+  L.params = take((size_t)nq * sizeof(RowParam));
+  L.samp = fused ? take((size_t)nq * r.ns * 4) : 0;
+  L.cnt = take((size_t)nq * r.S * 4);
+  L.hist = take((size_t)nq * r.S * r.m * 4);
+  L.cand = take((size_t)nq * r.S * r.cap * 8);
+  L.scratch = fused ? take((size_t)kFallbackGridFused * nk * 4) : 0;
+  L.total = off;
+  return L;
+}
+
+int select_entries(int k) {
+  int e = 2 * next_pow2(k);
+  return e < 4096 ? 4096 : e;
+}
+
+// Options common to both filter pipelines.
+void resolve_common(const lt_options* o, int k, Resolved& r) {
+  lt_options d;
+  lt_options_default(&d);
+  if (!o) o = &d;
+  r.m = o->num_bins > 0 ? std::min(o->num_bins, LT_MAX_BINS) : kDefaultBins;
+  r.cap = o->capacity > 0 ? o->capacity : std::max(12 * k, 2048);
+  r.flags = o->flags;
+  r.seed = o->seed;
+  r.ev = o->stage_events;
+  r.stats = o->row_stats;
+  r.E = select_entries(k);
+}
+
+Resolved resolve_fused(const lt_options* o, int nq, int nk, int k, int mode, const ScoreShape& sh) {
+  Resolved r{};
+  resolve_common(o, k, r);
+  lt_options d;
+  lt_options_default(&d);
+  if (!o) o = &d;
+  const size_t mcap = kHistLdsBudget / (4 * (size_t)sh.queries_per_block);
+  if ((size_t)r.m > mcap) r.m = (int)std::max<size_t>(mcap, 1);
+  int ns = o->sample_size;
+  if (ns < 0) {
+    ns = 3 * k;  // sec. 3.2: k' = 3k
+    if (mode == LT_SCORE_IP) ns = std::max(ns, std::min(nk / 64, 65536));
+  }
+  r.ns = sample_count(ns, nk);
+  const int steps = (nk + sh.keys_per_step - 1) / sh.keys_per_step;
+  const int tiles = (nq + sh.queries_per_block - 1) / sh.queries_per_block;
+  int S = 1;
+  if (o->key_splits > 0) {
+    S = std::min(o->key_splits, std::max(steps, 1));
+  } else {
+    // Split the key range only while the GPU is not yet full and every split
+    // still spans many times the sample (a split's threshold tightens only
+    // from its own histogram).
+    const long long span = 16LL * std::max(k, r.ns);
+    while ((long long)tiles * S < kTargetBlocks && (long long)nk / (2 * S) >= span) S *= 2;
+  }
+  r.S = S;
+  const int per = (nk + S - 1) / S;
+  r.L = ((per + sh.keys_per_step - 1) / sh.keys_per_step) * sh.keys_per_step;
+  if (r.L == 0) r.L = sh.keys_per_step;
+  r.refresh = o->refresh_tiles > 0 ? o->refresh_tiles : kDefaultRefreshTiles;
+  return r;
+}
+
+Resolved resolve_scores(const lt_options* o, int nq, int nk, int k) {
+  Resolved r{};
+  resolve_common(o, k, r);
+  lt_options d;
+  lt_options_default(&d);
+  if (!o) o = &d;
+  int ns = o->sample_size < 0 ? 3 * k : o->sample_size;
+  r.ns = sample_count(ns, nk);
+  int S = 1;
+  if (o->key_splits > 0) S = o->key_splits;
+  r.S = std::max(1, std::min(S, (nk + 255) / 256 + 1));
+  const int per = (nk + r.S - 1) / r.S;
+  r.L = std::max(256, ((per + 255) / 256) * 256);
+  r.refresh = o->refresh_tiles > 0 ? o->refresh_tiles : kDefaultRefreshChunks;
+  (void)nq;
+  return r;
+}
+
+inline bool aligned(const void* p, size_t a) { return ((uintptr_t)p % a) == 0; }
+
+inline int hip_status(hipError_t e) { return e == hipSuccess ? LT_OK : LT_EHIP; }
+
+inline void record(const Resolved& r, int i, hipStream_t st) {
+  if (r.ev && r.ev[i]) (void)hipEventRecord((hipEvent_t)r.ev[i], st);
+}
+
+int check_score_args(const void* q, const float* q_scale, const void* keys, const float* k_scale,
+                     lt_dtype dtype, lt_score_mode mode, int nq, int nk, int h, int d) {
+  if (nq < 0 || nk < 0 || h <= 0 || d <= 0) return LT_EINVAL;
+  if (dtype != LT_F32 && dtype != LT_BF16 && dtype != LT_FP8_E4M3FN) return LT_EINVAL;
+  if (mode != LT_SCORE_DSA && mode != LT_SCORE_IP) return LT_EINVAL;
+  if (nq > 0 && (!q || !aligned(q, 16))) return LT_EINVAL;
+  if (nk > 0 && (!keys || !aligned(keys, 16))) return LT_EINVAL;
+  if (dtype == LT_FP8_E4M3FN && ((nq > 0 && !q_scale) || (nk > 0 && !k_scale))) return LT_EINVAL;
+  if (!score_shape(dtype, mode, h, d).supported) return LT_EUNSUPPORTED;
+  return LT_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+void lt_options_default(lt_options* o) {
+  if (!o) return;
+  memset(o, 0, sizeof(*o));
+  o->num_bins = kDefaultBins;
+  o->sample_size = -1;
+  o->capacity = 0;
+  o->key_splits = 0;
+  o->refresh_tiles = 0;
+  o->flags = 0;
+  o->seed = 0x5EED5EEDull;
+  o->stage_events = nullptr;
+  o->row_stats = nullptr;
+}
+
+const char* lt_strerror(int status) {
+  switch (status) {
+    case LT_OK: return "ok";
+    case LT_EINVAL: return "invalid argument";
+    case LT_EUNSUPPORTED: return "unsupported (dtype, heads, head_dim, mode) or k";
+    case LT_EWORKSPACE: return "workspace too small";
+    case LT_EHIP: return "HIP runtime error";
+    default: return "unknown status";
+  }
+}
+
+size_t lt_indexer_topk_workspace_size(int32_t nq, int32_t nk, int32_t h, int32_t d, lt_dtype dtype,
+                                      lt_score_mode mode, int32_t k, const lt_options* opts) {
+  if (nq < 0 || nk < 0 || k < 1 || k > LT_K_MAX) return 0;
+  ScoreShape sh = score_shape(dtype, mode, h, d);
+  if (!sh.supported) return 0;
+  Resolved r = resolve_fused(opts, nq, nk, k, mode, sh);
+  return carve(nq, nk, r, true).total;
+}
+
+int lt_indexer_topk(const void* q, const float* q_scale, const float* w, const void* keys,
+                    const float* k_scale, lt_dtype dtype, lt_score_mode mode, int32_t nq, int32_t nk,
+                    int32_t h, int32_t d, int32_t k, const int32_t* offs, int32_t* out_idx,
+                    float* out_scores, void* workspace, size_t workspace_bytes, const lt_options* opts,
+                    void* stream) {
+  int rc = check_score_args(q, q_scale, keys, k_scale, dtype, mode, nq, nk, h, d);
+  if (rc) return rc;
+  if (k < 1) return LT_EINVAL;
+  if (k > LT_K_MAX) return LT_EUNSUPPORTED;
+  if (nq == 0) return LT_OK;
+  if (!out_idx || !out_scores || !workspace || !aligned(workspace, 256)) return LT_EINVAL;
+  const ScoreShape sh = score_shape(dtype, mode, h, d);
+  const Resolved r = resolve_fused(opts, nq, nk, k, mode, sh);
+  const Layout L = carve(nq, nk, r, true);
+  if (workspace_bytes < L.total) return LT_EWORKSPACE;
+  hipStream_t st = (hipStream_t)stream;
+  uint8_t* ws = static_cast<uint8_t*>(workspace);
+  uint32_t* qctl = reinterpret_cast<uint32_t*>(ws + L.qctl);
+  int32_t* queue = reinterpret_cast<int32_t*>(ws + L.queue);
+  RowParam* params = reinterpret_cast<RowParam*>(ws + L.params);
+  float* samp = reinterpret_cast<float*>(ws + L.samp);
+  uint32_t* cnt = reinterpret_cast<uint32_t*>(ws + L.cnt);
+  uint32_t* hist = reinterpret_cast<uint32_t*>(ws + L.hist);
+  int2* cand = reinterpret_cast<int2*>(ws + L.cand);
+  float* scratch = reinterpret_cast<float*>(ws + L.scratch);
+  ScoreArgs a{q, q_scale, w, keys, k_scale, (int)dtype, (int)mode, nq, nk, h, d, offs};
+
+  hipError_t e;
+  record(r, LT_STAGE_SAMPLE, st);
+  if ((e = launch_init(qctl, st)) != hipSuccess) return hip_status(e);
+  if (r.ns > 0 && (e = launch_sample_scores(a, r.ns, r.seed, samp, st)) != hipSuccess) return hip_status(e);
+  record(r, LT_STAGE_RANGE, st);
+  if ((e = launch_range(false, samp, r.ns, nq, nk, offs, r.ns, 1, r.seed, r.m, k, params, st)) != hipSuccess)
+    return hip_status(e);
+  record(r, LT_STAGE_FILTER, st);
+  if ((e = launch_fused_scan(a, params, r.S, r.L, r.cap, r.m, k, r.refresh, cnt, hist, cand, st)) != hipSuccess)
+    return hip_status(e);
+  record(r, LT_STAGE_SELECT, st);
+  if ((e = launch_select(params, cnt, hist, cand, nq, r.S, r.cap, r.m, k, r.E, r.flags, out_idx, out_scores, qctl,
+                         queue, r.stats, st)) != hipSuccess)
+    return hip_status(e);
+  record(r, LT_STAGE_FALLBACK, st);
+  if ((e = launch_fused_fallback(a, k, r.flags, qctl, queue, scratch, kFallbackGridFused, out_idx, out_scores,
+                                 st)) != hipSuccess)
+    return hip_status(e);
+  record(r, LT_NUM_STAGE_EVENTS - 1, st);
+  return LT_OK;
+}
+
+int lt_indexer_scores(const void* q, const float* q_scale, const float* w, const void* keys,
+                      const float* k_scale, lt_dtype dtype, lt_score_mode mode, int32_t nq, int32_t nk,
+                      int32_t h, int32_t d, float* scores, int64_t ld, void* stream) {
+  int rc = check_score_args(q, q_scale, keys, k_scale, dtype, mode, nq, nk, h, d);
+  if (rc) return rc;
+  if (ld < nk) return LT_EINVAL;
+  if (nq == 0 || nk == 0) return LT_OK;
+  if (!scores) return LT_EINVAL;
+  ScoreArgs a{q, q_scale, w, keys, k_scale, (int)dtype, (int)mode, nq, nk, h, d, nullptr};
+  return hip_status(launch_dense_scores(a, scores, ld, (hipStream_t)stream));
+}
+
+size_t lt_topk_select_workspace_size(int32_t nq, int32_t nk, int32_t k, const lt_options* opts) {
+  if (nq < 0 || nk < 0 || k < 1 || k > LT_K_MAX) return 0;
+  Resolved r = resolve_scores(opts, nq, nk, k);
+  return carve(nq, nk, r, false).total;
+}
+
+static int check_select_args(const float* scores, int64_t stride, int nq, int nk, int k) {
+  if (nq < 0 || nk < 0 || k < 1) return LT_EINVAL;
+  if (k > LT_K_MAX) return LT_EUNSUPPORTED;
+  if (stride < nk || stride % 4 != 0) return LT_EINVAL;
+  if (nq > 0 && nk > 0 && (!scores || !aligned(scores, 16))) return LT_EINVAL;
+  return LT_OK;
+}
+
+int lt_topk_select(const float* scores, int64_t stride, int32_t nq, int32_t nk, int32_t k,
+                   const int32_t* offs, int32_t* out_idx, float* out_scores, void* workspace,
+                   size_t workspace_bytes, const lt_options* opts, void* stream) {
+  int rc = check_select_args(scores, stride, nq, nk, k);
+  if (rc) return rc;
+  if (nq == 0) return LT_OK;
+  if (!out_idx || !out_scores || !workspace || !aligned(workspace, 256)) return LT_EINVAL;
+  const Resolved r = resolve_scores(opts, nq, nk, k);
+  const Layout L = carve(nq, nk, r, false);
+  if (workspace_bytes < L.total) return LT_EWORKSPACE;
+  hipStream_t st = (hipStream_t)stream;
+  uint8_t* ws = static_cast<uint8_t*>(workspace);
+  uint32_t* qctl = reinterpret_cast<uint32_t*>(ws + L.qctl);
+  int32_t* queue = reinterpret_cast<int32_t*>(ws + L.queue);
+  RowParam* params = reinterpret_cast<RowParam*>(ws + L.params);
+  uint32_t* cnt = reinterpret_cast<uint32_t*>(ws + L.cnt);
+  uint32_t* hist = reinterpret_cast<uint32_t*>(ws + L.hist);
+  int2* cand = reinterpret_cast<int2*>(ws + L.cand);
+
+  hipError_t e;
+  record(r, LT_STAGE_SAMPLE, st);
+  if ((e = launch_init(qctl, st)) != hipSuccess) return hip_status(e);
+  record(r, LT_STAGE_RANGE, st);
+  if ((e = launch_range(true, scores, stride, nq, nk, offs, r.ns, kSampleBlockScores, r.seed, r.m, k, params,
+                        st)) != hipSuccess)
+    return hip_status(e);
+  record(r, LT_STAGE_FILTER, st);
+  if ((e = launch_filter(scores, stride, nq, nk, offs, params, r.S, r.L, r.cap, r.m, k, r.refresh, cnt, hist,
+                         cand, st)) != hipSuccess)
+    return hip_status(e);
+  record(r, LT_STAGE_SELECT, st);
+  if ((e = launch_select(params, cnt, hist, cand, nq, r.S, r.cap, r.m, k, r.E, r.flags, out_idx, out_scores, qctl,
+                         queue, r.stats, st)) != hipSuccess)
+    return hip_status(e);
+  record(r, LT_STAGE_FALLBACK, st);
+  if ((e = launch_fallback_scores(scores, stride, nk, offs, k, r.flags, qctl, queue, out_idx, out_scores,
+                                  kFallbackGridScores, st)) != hipSuccess)
+    return hip_status(e);
+  record(r, LT_NUM_STAGE_EVENTS - 1, st);
+  return LT_OK;
+}
+
+int lt_topk_radix(const float* scores, int64_t stride, int32_t nq, int32_t nk, int32_t k,
+                  const int32_t* offs, int32_t* out_idx, float* out_scores, uint32_t flags, void* stream) {
+  int rc = check_select_args(scores, stride, nq, nk, k);
+  if (rc) return rc;
+  if (nq == 0) return LT_OK;
+  if (!out_idx || !out_scores) return LT_EINVAL;
+  return hip_status(launch_radix(scores, stride, nq, nk, offs, k, flags, out_idx, out_scores, (hipStream_t)stream));
+}
+
+int lt_event_create(void** ev) {
+  if (!ev) return LT_EINVAL;
+  hipEvent_t e;
+  if (hipEventCreate(&e) != hipSuccess) return LT_EHIP;
+  *ev = (void*)e;
+  return LT_OK;
+}
+
+int lt_event_destroy(void* ev) { return hip_status(hipEventDestroy((hipEvent_t)ev)); }
+
+int lt_event_record(void* ev, void* stream) { return hip_status(hipEventRecord((hipEvent_t)ev, (hipStream_t)stream)); }
+
+int lt_event_elapsed_ms(void* a, void* b, float* ms) {
+  if (!ms) return LT_EINVAL;
+  if (hipEventSynchronize((hipEvent_t)b) != hipSuccess) return LT_EHIP;
+  return hip_status(hipEventElapsedTime(ms, (hipEvent_t)a, (hipEvent_t)b));
+}
+
+}  // extern "C"

@@ -1,0 +1,66 @@
+// Internal interface between the C ABI (abi.hip) and the kernel translation
+// units. Not installed; the public interface is include/litetopk.h.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "../../include/litetopk.h"
+#include "common.hpp"
+
+namespace lt {
+
+// ---- selection side (select.hip) ----
+hipError_t launch_init(uint32_t* qctl, hipStream_t st);
+hipError_t launch_range(bool from_scores, const float* src, int64_t stride, int nq, int nk,
+                        const int32_t* offs, int ns, int blk, uint64_t seed, int m, int k,
+                        RowParam* params, hipStream_t st);
+hipError_t launch_filter(const float* scores, int64_t stride, int nq, int nk, const int32_t* offs,
+                         const RowParam* params, int S, int L, int cap, int m, int k, int refresh,
+                         uint32_t* cnt, uint32_t* hist, int2* cand, hipStream_t st);
+size_t select_lds_bytes(int E);
+hipError_t launch_select(const RowParam* params, const uint32_t* cnt, const uint32_t* hist,
+                         const int2* cand, int nq, int S, int cap, int m, int k, int E,
+                         uint32_t flags, int32_t* out_i, float* out_s, uint32_t* qctl,
+                         int32_t* queue, int32_t* stats, hipStream_t st);
+hipError_t launch_fallback_scores(const float* scores, int64_t stride, int nk, const int32_t* offs,
+                                  int k, uint32_t flags, const uint32_t* qctl, const int32_t* queue,
+                                  int32_t* out_i, float* out_s, int grid, hipStream_t st);
+hipError_t launch_radix(const float* scores, int64_t stride, int nq, int nk, const int32_t* offs,
+                        int k, uint32_t flags, int32_t* out_i, float* out_s, hipStream_t st);
+
+// ---- score side (score.hip) ----
+struct ScoreArgs {
+  const void* q;
+  const float* q_scale;
+  const float* w;
+  const void* keys;
+  const float* k_scale;
+  int dtype, mode, nq, nk, h, d;
+  const int32_t* offs;
+};
+
+// Static shape of one compiled score configuration.
+struct ScoreShape {
+  int supported;
+  int queries_per_block;  // queries one block owns
+  int keys_per_step;      // keys per LDS tile
+  int threads;            // block size
+  size_t scan_lds;        // LDS bytes of the scan (tiles), excluding histograms
+};
+ScoreShape score_shape(int dtype, int mode, int h, int d);
+
+// Sample scores: samp[t * ns + i] = I(t, sample_key(i)), blk = 1.
+hipError_t launch_sample_scores(const ScoreArgs& a, int ns, uint64_t seed, float* samp, hipStream_t st);
+// Dense scores: out[t * ld + s] = I(t, s) for every key.
+hipError_t launch_dense_scores(const ScoreArgs& a, float* out, int64_t ld, hipStream_t st);
+// Fused score + gate + write-back scan over S key splits of L keys each.
+hipError_t launch_fused_scan(const ScoreArgs& a, const RowParam* params, int S, int L, int cap, int m,
+                             int k, int refresh, uint32_t* cnt, uint32_t* hist, int2* cand,
+                             hipStream_t st);
+// Exact fallback for queued rows: dense re-score into scratch [grid, nk], then radix select.
+hipError_t launch_fused_fallback(const ScoreArgs& a, int k, uint32_t flags, const uint32_t* qctl,
+                                 const int32_t* queue, float* scratch, int grid, int32_t* out_i,
+                                 float* out_s, hipStream_t st);
+
+}  // namespace lt

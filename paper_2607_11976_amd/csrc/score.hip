@@ -1,0 +1,648 @@
+// Score-side kernels (gfx950): the index score of Eq. (1) on MFMA matrix
+// cores with the ReLU / head-weighted epilogue in registers, driven by one
+// LDS-tiled key scan that feeds four consumers:
+//   * the sample scorer (sec. 3.2 "Sampling"),
+//   * the dense scorer (the materialising baseline, sec. 1),
+//   * the fused filter scan (sec. 3.2 "Filtering" + "Threshold Refresh"),
+//   * the exact fallback for overflowed rows.
+// All four share the same arithmetic, so their scores are bit-identical.
+//
+// Layout of the contraction. A block owns QT = WAVES * QW queries and streams
+// the keys through LDS in tiles of KT = 32 * NT keys (double-buffered). Each
+// wave owns QW queries and keeps their QW * H head vectors stationary in VGPRs
+// as the A operand (rows = (query, head), 32 per M tile); the key tile is the B
+// operand (columns = keys). With 32x32 MFMA tiles each lane ends up holding 16
+// heads of one key column per M tile, so the head reduction of Eq. (1) is an
+// in-lane chain of ReLU + FMA, plus (for H >= 8) one exchange between the two
+// 32-lane halves, arranged so that after it every lane holds a full score.
+#include <utility>
+
+#include "internal.hpp"
+#include "select_dev.hpp"
+
+namespace lt {
+
+enum { DT_F32 = LT_F32, DT_BF16 = LT_BF16, DT_FP8 = LT_FP8_E4M3FN };
+
+typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
+typedef float f32x16_t __attribute__((ext_vector_type(16)));
+typedef int i32x8_t __attribute__((ext_vector_type(8)));
+typedef int i32x4_t __attribute__((ext_vector_type(4)));
+
+template <int N, class F>
+__device__ __forceinline__ void static_for(F&& f) {
+  [&]<int... I>(std::integer_sequence<int, I...>) {
+    (f(std::integral_constant<int, I>{}), ...);
+  }(std::make_integer_sequence<int, N>{});
+}
+
+// ---------------------------------------------------------------------------
+// MFMA flavours. Each lane feeds FB bytes = KI/2 consecutive elements of its
+// row (A) or column (B) per instruction: elements [KI/2 * (lane / 32), +KI/2)
+// of the K slice. A and B use the same lane->k assignment, so the instruction
+// sums every product of the slice exactly once.
+// ---------------------------------------------------------------------------
+template <int DT>
+struct Mfma;
+
+template <>
+struct Mfma<DT_F32> {
+  static constexpr int KI = 2, ES = 4, FB = 4;
+  using Frag = float;
+  __device__ static Frag load(const uint8_t* p) { return *reinterpret_cast<const float*>(p); }
+  __device__ static Frag zero() { return 0.0f; }
+  __device__ static f32x16_t mma(Frag a, Frag b, f32x16_t c) {
+    return __builtin_amdgcn_mfma_f32_32x32x2f32(a, b, c, 0, 0, 0);
+  }
+};
+
+template <>
+struct Mfma<DT_BF16> {
+  static constexpr int KI = 16, ES = 2, FB = 16;
+  using Frag = bf16x8_t;
+  __device__ static Frag load(const uint8_t* p) { return *reinterpret_cast<const bf16x8_t*>(p); }
+  __device__ static Frag zero() { return __builtin_bit_cast(bf16x8_t, i32x4_t{0, 0, 0, 0}); }
+  __device__ static f32x16_t mma(Frag a, Frag b, f32x16_t c) {
+    return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
+  }
+};
+
+template <>
+struct Mfma<DT_FP8> {
+  static constexpr int KI = 64, ES = 1, FB = 32;
+  using Frag = i32x8_t;
+  __device__ static Frag load(const uint8_t* p) {
+    i32x4_t lo = *reinterpret_cast<const i32x4_t*>(p);
+    i32x4_t hi = *reinterpret_cast<const i32x4_t*>(p + 16);
+    return i32x8_t{lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
+  }
+  __device__ static Frag zero() { return i32x8_t{0, 0, 0, 0, 0, 0, 0, 0}; }
+  // OCP E4M3 for both operands (format code 0), unit block scales (E8M0 127).
+  __device__ static f32x16_t mma(Frag a, Frag b, f32x16_t c) {
+    return __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(a, b, c, 0, 0, 0, 127, 0, 127);
+  }
+};
+
+// ---------------------------------------------------------------------------
+// Static configuration of one (dtype, H, d) variant.
+// ---------------------------------------------------------------------------
+template <int DT_, int H_, int D_, int QW_, int NT_, int WAVES_, bool RELU_>
+struct Cfg {
+  using M = Mfma<DT_>;
+  static constexpr int DT = DT_, H = H_, D = D_, QW = QW_, NT = NT_, WAVES = WAVES_;
+  static constexpr bool RELU = RELU_;
+  static constexpr int MT = QW * H / 32;               // M tiles per wave
+  static constexpr int KS = D / M::KI;                 // K steps per key
+  static constexpr int KT = 32 * NT;                   // keys per tile
+  static constexpr int QT = WAVES * QW;                // queries per block
+  static constexpr int ROWB = D * M::ES;               // bytes per key row
+  static constexpr int LSTRIDE = ROWB + 16;            // padded LDS row (bank spread)
+  static constexpr int TILE_BYTES = KT * LSTRIDE;
+  static constexpr int CPK = ROWB / 16;                // 16-byte chunks per key
+  static constexpr int CHUNKS = KT * CPK;
+  static constexpr int NTHREADS = WAVES * kWave;
+  static constexpr int CPT = (CHUNKS + NTHREADS - 1) / NTHREADS;
+  // GROUPED: H <= 4, a 4-row accumulator group holds whole queries, no
+  // cross-lane step. Otherwise H % 8 == 0 and the halves are combined.
+  static constexpr bool GROUPED = H <= 4;
+  static constexpr int GPQ = GROUPED ? 4 / H : 1;      // queries per 4-row group
+  static constexpr int NI = GROUPED ? NT * MT * 4 * GPQ : NT * QW / 2;  // scores per lane per tile
+  static_assert((QW * H) % 32 == 0, "a wave must fill whole M tiles");
+  static_assert(D % M::KI == 0, "head dim must be a multiple of the MFMA K");
+  static_assert(ROWB % 16 == 0, "key rows must be a multiple of 16 bytes");
+  static_assert(GROUPED ? (4 % H == 0) : (H % 8 == 0 && (NT * QW) % 2 == 0), "unsupported head layout");
+
+  // Score item `it` of a lane in half h (0: lanes 0-31, 1: lanes 32-63):
+  // which of the wave's queries and which 32-key sub-tile it belongs to.
+  __host__ __device__ static constexpr int item_q(int it, int h) {
+    if constexpr (GROUPED) {
+      const int s = it % GPQ, g = it / GPQ, i = g % 4, mt = (g / 4) % MT;
+      return (32 * mt + 8 * i + 4 * h + s * H) / H;
+    } else {
+      return (2 * it + h) / NT;
+    }
+  }
+  __host__ __device__ static constexpr int item_nt(int it, int h) {
+    if constexpr (GROUPED) return it / (MT * 4 * GPQ);
+    else return (2 * it + h) % NT;
+  }
+};
+
+// Per-wave stationary operands: the A fragments of the wave's queries and the
+// head weight of every accumulator row the lane holds.
+template <class C>
+struct WaveQ {
+  typename C::M::Frag qa[C::MT][C::KS];
+  float wv[C::MT][16];
+};
+
+template <class C>
+__device__ __forceinline__ void load_q(WaveQ<C>& s, const ScoreArgs& a, int qbase) {
+  using M = typename C::M;
+  const int l = lane_id(), h = l >> 5, r32 = l & 31;
+  const uint8_t* q = static_cast<const uint8_t*>(a.q);
+#pragma unroll
+  for (int mt = 0; mt < C::MT; ++mt) {
+    const int r = 32 * mt + r32, ql = r / C::H, j = r % C::H, t = qbase + ql;
+#pragma unroll
+    for (int ks = 0; ks < C::KS; ++ks) {
+      if (t < a.nq) {
+        const int64_t el = ((int64_t)t * C::H + j) * C::D + ks * M::KI + h * (M::KI / 2);
+        s.qa[mt][ks] = M::load(q + el * M::ES);
+      } else {
+        s.qa[mt][ks] = M::zero();
+      }
+    }
+  }
+#pragma unroll
+  for (int mt = 0; mt < C::MT; ++mt) {
+#pragma unroll
+    for (int v = 0; v < 16; ++v) {
+      const int r = 32 * mt + 8 * (v >> 2) + 4 * h + (v & 3), ql = r / C::H, j = r % C::H, t = qbase + ql;
+      float wt = 0.0f;
+      if (t < a.nq) {
+        wt = a.w ? a.w[(int64_t)t * C::H + j] : 1.0f;
+        if constexpr (C::DT == DT_FP8) wt *= a.q_scale[(int64_t)t * C::H + j];
+      }
+      s.wv[mt][v] = wt;
+    }
+  }
+}
+
+// q . k for every (row, key) of the tile: acc[nt][mt] holds the 32x32 block of
+// M tile mt against 32-key sub-tile nt. Accumulator register v of a lane is
+// row 8*(v/4) + 4*(lane/32) + v%4 of the M tile, column lane%32.
+template <class C>
+__device__ __forceinline__ void mma_tile(const WaveQ<C>& s, const uint8_t* tile, f32x16_t (&acc)[C::NT][C::MT]) {
+  using M = typename C::M;
+  const int l = lane_id(), h = l >> 5, r32 = l & 31;
+#pragma unroll
+  for (int nt = 0; nt < C::NT; ++nt)
+#pragma unroll
+    for (int mt = 0; mt < C::MT; ++mt) acc[nt][mt] = f32x16_t{};
+#pragma unroll
+  for (int ks = 0; ks < C::KS; ++ks) {
+#pragma unroll
+    for (int nt = 0; nt < C::NT; ++nt) {
+      const typename M::Frag b = M::load(tile + (nt * 32 + r32) * C::LSTRIDE + ks * M::KI * M::ES + h * M::FB);
+#pragma unroll
+      for (int mt = 0; mt < C::MT; ++mt) acc[nt][mt] = M::mma(s.qa[mt][ks], b, acc[nt][mt]);
+    }
+  }
+}
+
+// Eq. (1) epilogue in registers: ReLU of every head's dot product, weighted
+// sum over heads (inner-product mode skips the ReLU).
+template <class C>
+__device__ __forceinline__ void epilogue(const WaveQ<C>& s, const f32x16_t (&acc)[C::NT][C::MT], float (&out)[C::NI]) {
+  const int h = lane_id() >> 5;
+  if constexpr (C::GROUPED) {
+#pragma unroll
+    for (int nt = 0; nt < C::NT; ++nt)
+#pragma unroll
+      for (int mt = 0; mt < C::MT; ++mt)
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+#pragma unroll
+          for (int sq = 0; sq < C::GPQ; ++sq) {
+            float sum = 0.0f;
+#pragma unroll
+            for (int r = 0; r < C::H; ++r) {
+              const int v = 4 * i + sq * C::H + r;
+              float x = acc[nt][mt][v];
+              if constexpr (C::RELU) x = fmaxf(x, 0.0f);
+              sum = fmaf(s.wv[mt][v], x, sum);
+            }
+            out[((nt * C::MT + mt) * 4 + i) * C::GPQ + sq] = sum;
+          }
+  } else {
+    float part[C::NT][C::QW];
+#pragma unroll
+    for (int nt = 0; nt < C::NT; ++nt)
+#pragma unroll
+      for (int q = 0; q < C::QW; ++q) part[nt][q] = 0.0f;
+#pragma unroll
+    for (int nt = 0; nt < C::NT; ++nt)
+#pragma unroll
+      for (int mt = 0; mt < C::MT; ++mt)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const int q = (32 * mt + 8 * i) / C::H;
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            const int v = 4 * i + r;
+            float x = acc[nt][mt][v];
+            if constexpr (C::RELU) x = fmaxf(x, 0.0f);
+            part[nt][q] = fmaf(s.wv[mt][v], x, part[nt][q]);
+          }
+        }
+    // Lane halves hold disjoint head subsets of the same (query, key). Pair
+    // the (query, sub-tile) entries: half 0 finishes entry 2i, half 1 entry
+    // 2i+1, each sending the partial the other half needs.
+#pragma unroll
+    for (int it = 0; it < C::NI; ++it) {
+      const int e0 = 2 * it, e1 = 2 * it + 1;
+      const float a0 = part[e0 % C::NT][e0 / C::NT];
+      const float a1 = part[e1 % C::NT][e1 / C::NT];
+      const float recv = __shfl_xor(h ? a0 : a1, 32, kWave);
+      out[it] = (h ? a1 : a0) + recv;
+    }
+  }
+}
+
+struct SrcContig {
+  __device__ int key(int i) const { return i; }
+};
+struct SrcSample {
+  int ns, nk;
+  uint64_t seed;
+  __device__ int key(int i) const { return sample_key(i, ns, nk, 1, seed); }
+};
+
+// The block-wide scan of positions [kbeg, kend) of `src` (key index =
+// src.key(position)), double-buffered through LDS. Every wave runs the MFMA
+// tile and the epilogue and hands its scores to `sink`.
+template <class C, class Src, class Sink>
+__device__ __forceinline__ void wg_scan(const ScoreArgs& a, const Src& src, int kbeg, int kend, uint8_t* tiles,
+                                        const WaveQ<C>& wq, Sink& sink) {
+  const int tid = threadIdx.x, l = lane_id(), h = l >> 5, r32 = l & 31;
+  const uint8_t* keys = static_cast<const uint8_t*>(a.keys);
+  const int nsteps = kend > kbeg ? (kend - kbeg + C::KT - 1) / C::KT : 0;
+  if (nsteps == 0) return;
+  i32x4_t regs[C::CPT];
+  auto gload = [&](int k0) {
+#pragma unroll
+    for (int c = 0; c < C::CPT; ++c) {
+      const int ch = tid + c * C::NTHREADS;
+      regs[c] = i32x4_t{0, 0, 0, 0};
+      if (ch < C::CHUNKS) {
+        const int kk = ch / C::CPK, part = ch - kk * C::CPK, i = k0 + kk;
+        if (i < kend)
+          regs[c] = *reinterpret_cast<const i32x4_t*>(keys + (int64_t)src.key(i) * C::ROWB + part * 16);
+      }
+    }
+  };
+  auto sstore = [&](int buf) {
+#pragma unroll
+    for (int c = 0; c < C::CPT; ++c) {
+      const int ch = tid + c * C::NTHREADS;
+      if (ch < C::CHUNKS) {
+        const int kk = ch / C::CPK, part = ch - kk * C::CPK;
+        *reinterpret_cast<i32x4_t*>(tiles + buf * C::TILE_BYTES + kk * C::LSTRIDE + part * 16) = regs[c];
+      }
+    }
+  };
+  gload(kbeg);
+  sstore(0);
+  __syncthreads();
+  for (int st = 0; st < nsteps; ++st) {
+    const int k0 = kbeg + st * C::KT;
+    if (st + 1 < nsteps) gload(k0 + C::KT);
+    f32x16_t acc[C::NT][C::MT];
+    mma_tile<C>(wq, tiles + (st & 1) * C::TILE_BYTES, acc);
+    float sc[C::NI];
+    epilogue<C>(wq, acc, sc);
+    if constexpr (C::DT == DT_FP8) {
+#pragma unroll
+      for (int it = 0; it < C::NI; ++it) {
+        const int nt = h ? C::item_nt(it, 1) : C::item_nt(it, 0);
+        const int pos = k0 + nt * 32 + r32;
+        sc[it] *= pos < kend ? a.k_scale[src.key(pos)] : 0.0f;
+      }
+    }
+    sink.consume(st, k0, kend, sc);
+    if (st + 1 < nsteps) sstore((st + 1) & 1);
+    __syncthreads();
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Sinks
+// ---------------------------------------------------------------------------
+
+// Writes every score to out[t * ld + position].
+template <class C>
+struct DenseSink {
+  float* out;
+  int64_t ld;
+  int qbase, nq;
+  __device__ void consume(int, int k0, int kend, const float (&sc)[C::NI]) {
+    const int l = lane_id(), h = l >> 5, r32 = l & 31;
+#pragma unroll
+    for (int it = 0; it < C::NI; ++it) {
+      const int q = h ? C::item_q(it, 1) : C::item_q(it, 0);
+      const int nt = h ? C::item_nt(it, 1) : C::item_nt(it, 0);
+      const int pos = k0 + nt * 32 + r32, t = qbase + q;
+      if (t < nq && pos < kend) out[(int64_t)t * ld + pos] = sc[it];
+    }
+  }
+};
+
+// Writes only the scores of one query row (the fallback's re-score).
+template <class C>
+struct RowSink {
+  float* out;
+  int qbase, target;
+  __device__ void consume(int, int k0, int kend, const float (&sc)[C::NI]) {
+    const int l = lane_id(), h = l >> 5, r32 = l & 31;
+#pragma unroll
+    for (int it = 0; it < C::NI; ++it) {
+      const int q = h ? C::item_q(it, 1) : C::item_q(it, 0);
+      const int nt = h ? C::item_nt(it, 1) : C::item_nt(it, 0);
+      const int pos = k0 + nt * 32 + r32;
+      if (qbase + q == target && pos < kend) out[pos] = sc[it];
+    }
+  }
+};
+
+// The fused filter (sec. 3.2 "Filtering" and "Threshold Refresh") for the
+// wave's QW rows. Per score: bin-space value x = fma(I, delta, c), gate
+// !(x < thr) with thr the current threshold bin, causal mask. Passing scores
+// are compacted with one ballot per item (mbcnt gives each passing lane its
+// slot; the row's tail is wave-private, so no atomics), written as (key,
+// score) to the row's HBM candidate list, and counted in the row's LDS
+// histogram. Every `refresh` tiles the wave recomputes each row's threshold
+// bin from its histogram; the gate only ever tightens.
+template <class C>
+struct FusedSink {
+  float delta[C::QW], cc[C::QW], thr[C::QW];
+  int tau[C::QW], e[C::QW];
+  uint32_t tail[C::QW];
+  uint32_t* hist;     // LDS, [QW][m] for this wave
+  int2* cand;
+  int qbase, nq, S, split, cap, m, k, refresh;
+
+  __device__ void init(const ScoreArgs& a, const RowParam* params, int kend) {
+#pragma unroll
+    for (int q = 0; q < C::QW; ++q) {
+      const int t = qbase + q;
+      int ev = 0;
+      float dl = 1.0f, c = 0.0f;
+      int t0 = -1;
+      if (t < nq) {
+        ev = a.offs ? a.offs[t] : a.nk;
+        ev = ev < 0 ? 0 : (ev > a.nk ? a.nk : ev);
+        const RowParam p = params[t];
+        dl = p.delta;
+        c = p.c;
+        t0 = p.tau0;
+      }
+      e[q] = ev < kend ? ev : kend;
+      delta[q] = dl;
+      cc[q] = c;
+      tau[q] = t0;
+      thr[q] = gate_thr(t0);
+      tail[q] = 0;
+    }
+  }
+
+  __device__ void consume(int st, int k0, int, const float (&sc)[C::NI]) {
+    const int l = lane_id(), h = l >> 5, r32 = l & 31;
+    static_for<C::NI>([&](auto IT) {
+      constexpr int it = decltype(IT)::value;
+      constexpr int qa = C::item_q(it, 0), qb = C::item_q(it, 1);
+      constexpr int na = C::item_nt(it, 0), nb = C::item_nt(it, 1);
+      const int key = k0 + (h ? nb : na) * 32 + r32;
+      const float x = bin_x(sc[it], h ? delta[qb] : delta[qa], h ? cc[qb] : cc[qa]);
+      const bool pass = key < (h ? e[qb] : e[qa]) && !(x < (h ? thr[qb] : thr[qa]));
+      const uint64_t mask = __ballot(pass);
+      const uint32_t mb = mbcnt64(mask);
+      uint32_t pos;
+      if constexpr (qa == qb) {
+        pos = tail[qa] + mb;
+        tail[qa] += (uint32_t)__popcll(mask);
+      } else {
+        const uint32_t lo = (uint32_t)__popcll(mask & 0xFFFFFFFFull);
+        pos = h ? tail[qb] + mb - lo : tail[qa] + mb;
+        tail[qa] += lo;
+        tail[qb] += (uint32_t)__popcll(mask) - lo;
+      }
+      if (pass) {
+        const int q = h ? qb : qa;
+        if (pos < (uint32_t)cap)
+          cand[((int64_t)(qbase + q) * S + split) * cap + pos] = make_int2(key, __float_as_int(sc[it]));
+        const int b = bin_of(x, m);
+        if (b >= 0) atomicAdd(&hist[q * m + b], 1u);
+      }
+    });
+    if ((st + 1) % refresh == 0) {
+      __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "wavefront");
+#pragma unroll
+      for (int q = 0; q < C::QW; ++q) {
+        const int t2 = wave_threshold(hist + q * m, m, (uint32_t)k, nullptr);
+        if (t2 > tau[q]) {
+          tau[q] = t2;
+          thr[q] = gate_thr(t2);
+        }
+      }
+    }
+  }
+
+  __device__ void finish(uint32_t* cnt, uint32_t* hist_out) {
+    __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "wavefront");
+    const int l = lane_id();
+#pragma unroll
+    for (int q = 0; q < C::QW; ++q) {
+      const int t = qbase + q;
+      if (t >= nq) continue;
+      const int64_t u = (int64_t)t * S + split;
+      for (int b = l; b < m; b += kWave) hist_out[u * m + b] = hist[q * m + b];
+      if (l == 0) cnt[u] = tail[q];
+    }
+  }
+};
+
+// ---------------------------------------------------------------------------
+// Kernels
+// ---------------------------------------------------------------------------
+template <class C>
+__global__ __launch_bounds__(C::NTHREADS) void k_sample(ScoreArgs a, int ns, uint64_t seed, float* samp, int slice) {
+  extern __shared__ __align__(16) uint8_t lds[];
+  const int q0 = blockIdx.x * C::QT, wave = threadIdx.x / kWave, qbase = q0 + wave * C::QW;
+  const int kb = blockIdx.y * slice, ke = min(kb + slice, ns);
+  WaveQ<C> wq;
+  load_q<C>(wq, a, qbase);
+  DenseSink<C> sink{samp, ns, qbase, a.nq};
+  wg_scan<C>(a, SrcSample{ns, a.nk, seed}, kb, ke, lds, wq, sink);
+}
+
+template <class C>
+__global__ __launch_bounds__(C::NTHREADS) void k_dense(ScoreArgs a, float* out, int64_t ld, int slice) {
+  extern __shared__ __align__(16) uint8_t lds[];
+  const int q0 = blockIdx.x * C::QT, wave = threadIdx.x / kWave, qbase = q0 + wave * C::QW;
+  const int kb = blockIdx.y * slice, ke = min(kb + slice, a.nk);
+  WaveQ<C> wq;
+  load_q<C>(wq, a, qbase);
+  DenseSink<C> sink{out, ld, qbase, a.nq};
+  wg_scan<C>(a, SrcContig{}, kb, ke, lds, wq, sink);
+}
+
+template <class C>
+__global__ __launch_bounds__(C::NTHREADS) void k_fused(ScoreArgs a, const RowParam* params, int S, int L, int cap,
+                                                       int m, int k, int refresh, uint32_t* cnt,
+                                                       uint32_t* hist_out, int2* cand) {
+  extern __shared__ __align__(16) uint8_t lds[];
+  uint32_t* hist = reinterpret_cast<uint32_t*>(lds + 2 * C::TILE_BYTES);
+  int* emax = reinterpret_cast<int*>(hist + C::QT * m);
+  const int tile = blockIdx.x / S, split = blockIdx.x - tile * S;
+  const int q0 = tile * C::QT, wave = threadIdx.x / kWave, qbase = q0 + wave * C::QW;
+  for (int i = threadIdx.x; i < C::QT * m; i += C::NTHREADS) hist[i] = 0u;
+  if (threadIdx.x == 0) *emax = 0;
+  __syncthreads();
+  if (threadIdx.x < C::QT && q0 + (int)threadIdx.x < a.nq) {
+    int ev = a.offs ? a.offs[q0 + threadIdx.x] : a.nk;
+    ev = ev < 0 ? 0 : (ev > a.nk ? a.nk : ev);
+    atomicMax(emax, ev);
+  }
+  __syncthreads();
+  const int kb = split * L;
+  const int ke = min(min(kb + L, a.nk), *emax);
+  WaveQ<C> wq;
+  load_q<C>(wq, a, qbase);
+  FusedSink<C> sink;
+  sink.hist = hist + wave * C::QW * m;
+  sink.cand = cand;
+  sink.qbase = qbase;
+  sink.nq = a.nq;
+  sink.S = S;
+  sink.split = split;
+  sink.cap = cap;
+  sink.m = m;
+  sink.k = k;
+  sink.refresh = refresh;
+  sink.init(a, params, ke);
+  wg_scan<C>(a, SrcContig{}, kb, ke, lds, wq, sink);
+  sink.finish(cnt, hist_out);
+}
+
+template <class C>
+__global__ __launch_bounds__(C::NTHREADS) void k_fused_fallback(ScoreArgs a, int k, uint32_t flags,
+                                                                const uint32_t* qctl, const int32_t* queue,
+                                                                float* scratch, int32_t* out_i, float* out_s) {
+  extern __shared__ __align__(16) uint8_t lds[];
+  const uint32_t n = qctl[0];
+  const int wave = threadIdx.x / kWave;
+  for (uint32_t r = blockIdx.x; r < n; r += gridDim.x) {
+    const int row = queue[r];
+    const int q0 = (row / C::QT) * C::QT, qbase = q0 + wave * C::QW;
+    int e = a.offs ? a.offs[row] : a.nk;
+    e = e < 0 ? 0 : (e > a.nk ? a.nk : e);
+    float* srow = scratch + (int64_t)blockIdx.x * a.nk;
+    WaveQ<C> wq;
+    load_q<C>(wq, a, qbase);
+    RowSink<C> sink{srow, qbase, row};
+    wg_scan<C>(a, SrcContig{}, 0, e, lds, wq, sink);
+    __threadfence_block();
+    __syncthreads();
+    radix_select_row<C::NTHREADS>(srow, e, k, out_i + (int64_t)row * k, out_s + (int64_t)row * k,
+                                  flags & LT_SORTED_OUTPUT, lds);
+    __syncthreads();
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Compiled variants and dispatch
+// ---------------------------------------------------------------------------
+//            dtype   H   d  QW NT WAVES RELU
+#define LT_VARIANTS(X)                   \
+  X(DT_F32, 4, 64, 8, 2, 4, true)        \
+  X(DT_F32, 1, 64, 32, 2, 4, true)       \
+  X(DT_F32, 1, 64, 32, 2, 4, false)      \
+  X(DT_BF16, 64, 128, 1, 2, 8, true)     \
+  X(DT_BF16, 4, 128, 8, 2, 4, true)      \
+  X(DT_BF16, 1, 128, 32, 2, 4, true)     \
+  X(DT_BF16, 1, 128, 32, 2, 4, false)    \
+  X(DT_FP8, 64, 128, 1, 2, 8, true)
+
+template <class F>
+static bool with_cfg(int dt, int mode, int h, int d, F&& f) {
+  const bool relu = mode == LT_SCORE_DSA;
+#define LT_CASE(DT, H, D, QW, NT, WV, RELU)                          \
+  if (dt == DT && h == H && d == D && relu == RELU) {                \
+    f.template operator()<Cfg<DT, H, D, QW, NT, WV, RELU>>();        \
+    return true;                                                     \
+  }
+  LT_VARIANTS(LT_CASE)
+#undef LT_CASE
+  return false;
+}
+
+ScoreShape score_shape(int dtype, int mode, int h, int d) {
+  ScoreShape s{0, 0, 0, 0, 0};
+  with_cfg(dtype, mode, h, d, [&]<class C>() {
+    s.supported = 1;
+    s.queries_per_block = C::QT;
+    s.keys_per_step = C::KT;
+    s.threads = C::NTHREADS;
+    s.scan_lds = 2 * C::TILE_BYTES;
+  });
+  return s;
+}
+
+static constexpr int kSlice = 8192;   // positions per block in the sample / dense scorers
+
+hipError_t launch_sample_scores(const ScoreArgs& a, int ns, uint64_t seed, float* samp, hipStream_t st) {
+  hipError_t err = hipErrorInvalidValue;
+  with_cfg(a.dtype, a.mode, a.h, a.d, [&]<class C>() {
+    dim3 grid((a.nq + C::QT - 1) / C::QT, (ns + kSlice - 1) / kSlice);
+    if (grid.x == 0 || grid.y == 0) {
+      err = hipSuccess;
+      return;
+    }
+    hipLaunchKernelGGL(k_sample<C>, grid, dim3(C::NTHREADS), 2 * C::TILE_BYTES, st, a, ns, seed, samp, kSlice);
+    err = hipGetLastError();
+  });
+  return err;
+}
+
+hipError_t launch_dense_scores(const ScoreArgs& a, float* out, int64_t ld, hipStream_t st) {
+  hipError_t err = hipErrorInvalidValue;
+  with_cfg(a.dtype, a.mode, a.h, a.d, [&]<class C>() {
+    dim3 grid((a.nq + C::QT - 1) / C::QT, (a.nk + kSlice - 1) / kSlice);
+    if (grid.x == 0 || grid.y == 0) {
+      err = hipSuccess;
+      return;
+    }
+    hipLaunchKernelGGL(k_dense<C>, grid, dim3(C::NTHREADS), 2 * C::TILE_BYTES, st, a, out, ld, kSlice);
+    err = hipGetLastError();
+  });
+  return err;
+}
+
+hipError_t launch_fused_scan(const ScoreArgs& a, const RowParam* params, int S, int L, int cap, int m, int k,
+                             int refresh, uint32_t* cnt, uint32_t* hist, int2* cand, hipStream_t st) {
+  hipError_t err = hipErrorInvalidValue;
+  with_cfg(a.dtype, a.mode, a.h, a.d, [&]<class C>() {
+    const int tiles = (a.nq + C::QT - 1) / C::QT;
+    if (tiles == 0) {
+      err = hipSuccess;
+      return;
+    }
+    const size_t lds = 2 * C::TILE_BYTES + (size_t)C::QT * m * 4 + 16;
+    if (lds > 65536)
+      (void)hipFuncSetAttribute((const void*)k_fused<C>, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+    hipLaunchKernelGGL(k_fused<C>, dim3(tiles * S), dim3(C::NTHREADS), lds, st, a, params, S, L, cap, m, k,
+                       refresh, cnt, hist, cand);
+    err = hipGetLastError();
+  });
+  return err;
+}
+
+hipError_t launch_fused_fallback(const ScoreArgs& a, int k, uint32_t flags, const uint32_t* qctl,
+                                 const int32_t* queue, float* scratch, int grid, int32_t* out_i, float* out_s,
+                                 hipStream_t st) {
+  hipError_t err = hipErrorInvalidValue;
+  with_cfg(a.dtype, a.mode, a.h, a.d, [&]<class C>() {
+    size_t lds = 2 * C::TILE_BYTES;
+    const size_t rl = radix_lds_bytes(k);
+    if (rl > lds) lds = rl;
+    if (lds > 65536)
+      (void)hipFuncSetAttribute((const void*)k_fused_fallback<C>, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+    hipLaunchKernelGGL(k_fused_fallback<C>, dim3(grid), dim3(C::NTHREADS), lds, st, a, k, flags, qctl, queue,
+                       scratch, out_i, out_s);
+    err = hipGetLastError();
+  });
+  return err;
+}
+
+}  // namespace lt

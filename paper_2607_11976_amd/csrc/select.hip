@@ -1,0 +1,400 @@
+// Selection-side kernels: per-row range from the sample, the scores-in
+// filter scan, the final select, the exact fallback and plain radix select.
+#include "internal.hpp"
+#include "select_dev.hpp"
+
+namespace lt {
+
+// ---------------------------------------------------------------------------
+// Zero the fallback queue counter (a kernel, not a memset, so the launch
+// sequence can be captured in a graph).
+// ---------------------------------------------------------------------------
+__global__ void k_init(uint32_t* qctl) {
+  if (threadIdx.x < 4) qctl[threadIdx.x] = 0u;
+}
+
+// ---------------------------------------------------------------------------
+// Range and initial threshold (sec. 3.2 "Sampling"). One wave per row.
+// s_min / s_max over the row's visible, finite sample scores; delta = m /
+// (s_max - s_min); tau0 = bin of the k-th largest visible sample score, found
+// with the sample's histogram. The sample histogram is NOT carried into the
+// scan: every sampled key is scanned again, and counting it twice could
+// raise the threshold above the true k-th score.
+// FROM_SCORES: the sample is read from a score matrix (scores-in entry);
+// otherwise from the [nq, ns] matrix of sample scores the sample kernel wrote.
+// ---------------------------------------------------------------------------
+template <bool FROM_SCORES>
+__global__ __launch_bounds__(256) void k_range(const float* src, int64_t stride, int nq, int nk,
+                                               const int32_t* offs, int ns, int blk, uint64_t seed,
+                                               int m, int k, RowParam* params) {
+  __shared__ uint32_t hist_all[4][kMaxBins];
+  const int wave = threadIdx.x / kWave, l = lane_id();
+  const int row = blockIdx.x * 4 + wave;
+  if (row >= nq) return;
+  uint32_t* hist = hist_all[wave];
+  int e = offs ? offs[row] : nk;
+  e = e < 0 ? 0 : (e > nk ? nk : e);
+  const float* rp = src + (int64_t)row * stride;
+
+  float mn = __builtin_inff(), mx = -__builtin_inff();
+  uint32_t nvis = 0;
+  for (int i = l; i < ns; i += kWave) {
+    int key = sample_key(i, ns, nk, blk, seed);
+    if (key >= e) continue;
+    float s = FROM_SCORES ? rp[key] : rp[i];
+    ++nvis;
+    if (__builtin_isfinite(s)) {
+      mn = fminf(mn, s);
+      mx = fmaxf(mx, s);
+    }
+  }
+  mn = wave_min(mn);
+  mx = wave_max(mx);
+  nvis = wave_sum(nvis);
+  float delta = 1.0f, c = 0.0f;
+  if (mx > mn) delta = (float)m / (mx - mn);
+  if (!(delta > 0.0f) || !__builtin_isfinite(delta)) delta = 1.0f;
+  if (__builtin_isfinite(mn)) c = -mn * delta;
+  if (!__builtin_isfinite(c)) c = 0.0f;
+
+  for (int b = l; b < kMaxBins; b += kWave) hist[b] = 0u;
+  __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "wavefront");
+  for (int i = l; i < ns; i += kWave) {
+    int key = sample_key(i, ns, nk, blk, seed);
+    if (key >= e) continue;
+    float s = FROM_SCORES ? rp[key] : rp[i];
+    int b = bin_of(bin_x(s, delta, c), m);
+    if (b >= 0) atomicAdd(&hist[b], 1u);
+  }
+  __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "wavefront");
+  int tau0 = wave_threshold(hist, m, (uint32_t)k, nullptr);
+  if (l == 0) params[row] = RowParam{delta, c, tau0, (int)nvis};
+}
+
+// ---------------------------------------------------------------------------
+// Scores-in filter scan (sec. 3.2 "Filtering" + "Threshold Refresh"). One
+// wave owns one (row, key split): it streams its scores once, gates them with
+// the row's current threshold bin, appends the passing ones (ballot + mbcnt
+// compaction, one write per passing key, key order preserved) to its own
+// candidate list, counts them in its own LDS histogram, and refreshes the
+// threshold from that histogram every `refresh` chunks of 256 keys. A list
+// that reaches `cap` stops storing but keeps counting, so the final select can
+// detect the overflow.
+// ---------------------------------------------------------------------------
+constexpr int kFilterWaves = 4;
+
+__global__ __launch_bounds__(kFilterWaves * kWave) void k_filter(
+    const float* scores, int64_t stride, int nq, int nk, const int32_t* offs, const RowParam* params,
+    int S, int L, int cap, int m, int k, int refresh, uint32_t* cnt, uint32_t* hist_out, int2* cand) {
+  __shared__ uint32_t hist_all[kFilterWaves][kMaxBins];
+  const int wave = threadIdx.x / kWave, l = lane_id();
+  const int unit = blockIdx.x * kFilterWaves + wave;
+  if (unit >= nq * S) return;
+  const int row = unit / S, split = unit - row * S;
+  uint32_t* hist = hist_all[wave];
+  int e = offs ? offs[row] : nk;
+  e = e < 0 ? 0 : (e > nk ? nk : e);
+  const int lo = split * L;
+  const int hi = min(lo + L, e);
+  const RowParam p = params[row];
+  int tau = p.tau0;
+  float thr = gate_thr(tau);
+  for (int b = l; b < kMaxBins; b += kWave) hist[b] = 0u;
+  __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "wavefront");
+
+  const float* rp = scores + (int64_t)row * stride;
+  int2* out = cand + (int64_t)unit * cap;
+  uint32_t tail = 0;
+  int it = 0;
+  for (int base = lo; base < hi; base += 4 * kWave, ++it) {
+    const int i0 = base + 4 * l;
+    float v[4];
+    if (i0 + 3 < hi) {
+      float4 t = *reinterpret_cast<const float4*>(rp + i0);
+      v[0] = t.x; v[1] = t.y; v[2] = t.z; v[3] = t.w;
+    } else {
+#pragma unroll
+      for (int j = 0; j < 4; ++j) v[j] = (i0 + j < hi) ? rp[i0 + j] : 0.0f;
+    }
+    float x[4];
+    bool ps[4];
+    uint32_t below = 0, total = 0;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      x[j] = bin_x(v[j], p.delta, p.c);
+      ps[j] = (i0 + j < hi) && !(x[j] < thr);
+      uint64_t mask = __ballot(ps[j]);
+      below += mbcnt64(mask);
+      total += (uint32_t)__popcll(mask);
+    }
+    uint32_t pos = tail + below;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      if (ps[j]) {
+        if (pos < (uint32_t)cap) out[pos] = make_int2(i0 + j, __float_as_int(v[j]));
+        int b = bin_of(x[j], m);
+        if (b >= 0) atomicAdd(&hist[b], 1u);
+        ++pos;
+      }
+    }
+    tail += total;
+    if ((it + 1) % refresh == 0) {
+      __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "wavefront");
+      int t2 = wave_threshold(hist, m, (uint32_t)k, nullptr);
+      if (t2 > tau) {
+        tau = t2;
+        thr = gate_thr(tau);
+      }
+    }
+  }
+  __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "wavefront");
+  for (int b = l; b < m; b += kWave) hist_out[(int64_t)unit * m + b] = hist[b];
+  if (l == 0) cnt[unit] = tail;
+}
+
+// ---------------------------------------------------------------------------
+// Final select (sec. 3.2 "Top-k Selection"). One block per row.
+//  1. Sum the row's per-split histograms; the final threshold bin tau is the
+//     largest bin whose suffix count reaches k (bins >= tau are complete:
+//     every key in them passed the gate, which never exceeded tau).
+//  2. Candidates in bins above tau (fewer than k) go straight to the output,
+//     in key order.
+//  3. Candidates in bin tau are collected in LDS and only they are sorted;
+//     the best k - (count above) complete the row.
+// Rows whose buffer overflowed, whose threshold bin does not fit in LDS, or
+// that are forced, are queued for the exact fallback instead.
+// ---------------------------------------------------------------------------
+constexpr int kSelThreads = 256;
+
+__global__ __launch_bounds__(kSelThreads) void k_select(
+    const RowParam* params, const uint32_t* cnt, const uint32_t* hist, const int2* cand, int nq,
+    int S, int cap, int m, int k, int E, uint32_t flags, int32_t* out_i, float* out_s,
+    uint32_t* qctl, int32_t* queue, int32_t* stats) {
+  extern __shared__ __align__(16) uint8_t lds[];
+  uint32_t* hsum = reinterpret_cast<uint32_t*>(lds);          // [256]
+  uint32_t* tmp = hsum + kMaxBins;                             // [16]
+  uint64_t* ent = reinterpret_cast<uint64_t*>(lds + kMaxBins * 4 + 64);  // [E]
+  const int row = blockIdx.x, tid = threadIdx.x;
+  const bool sorted = flags & LT_SORTED_OUTPUT;
+  int32_t* oi = out_i + (int64_t)row * k;
+  float* os = out_s + (int64_t)row * k;
+
+  // ---- overflow / forced ----
+  uint32_t total_c = 0;
+  int reason = (flags & LT_FORCE_FALLBACK) ? 3 : 0;
+  for (int s = 0; s < S; ++s) {
+    uint32_t c = cnt[(int64_t)row * S + s];
+    total_c += c;
+    if (c > (uint32_t)cap && reason == 0) reason = 1;
+  }
+  auto enqueue = [&](int why, int tau, uint32_t nt) {
+    if (tid == 0) {
+      uint32_t slot = atomicAdd(&qctl[0], 1u);
+      queue[slot] = row;
+      if (stats) {
+        int32_t* st = stats + (int64_t)row * 4;
+        st[0] = (int32_t)total_c;
+        st[1] = tau;
+        st[2] = why;
+        st[3] = (int32_t)nt;
+      }
+    }
+  };
+  if (reason) {
+    enqueue(reason, -2, 0);
+    return;
+  }
+
+  // ---- 1. final threshold bin ----
+  for (int b = tid; b < kMaxBins; b += kSelThreads) {
+    uint32_t h = 0;
+    if (b < m)
+      for (int s = 0; s < S; ++s) h += hist[((int64_t)row * S + s) * m + b];
+    hsum[b] = h;
+  }
+  __syncthreads();
+  if (tid < kWave) {
+    uint32_t above = 0;
+    int tau = wave_threshold(hsum, m, (uint32_t)k, &above);
+    if (tid == 0) {
+      tmp[8] = (uint32_t)tau;
+      tmp[9] = above;
+    }
+  }
+  __syncthreads();
+  const int tau = (int)tmp[8];
+  const uint32_t c_above = tmp[9];
+  __syncthreads();
+  const RowParam p = params[row];
+
+  // ---- 2./3. one ordered pass over the candidates ----
+  uint32_t run_above = 0, run_tie = 0;
+  bool tie_ovf = false;
+  for (int s = 0; s < S; ++s) {
+    const uint32_t n_s = min(cnt[(int64_t)row * S + s], (uint32_t)cap);
+    const int2* cb = cand + ((int64_t)row * S + s) * cap;
+    for (uint32_t base = 0; base < n_s; base += kSelThreads) {
+      const uint32_t i = base + tid;
+      int2 ce = make_int2(0, 0);
+      bool ab = false, ti = false;
+      if (i < n_s) {
+        ce = cb[i];
+        int b = bin_of(bin_x(__int_as_float(ce.y), p.delta, p.c), m);
+        ab = b > tau;
+        ti = b == tau;
+      }
+      uint32_t tot;
+      uint32_t ex = block_scan_excl<kSelThreads>(((uint32_t)ab << 16) | (uint32_t)ti, tmp, &tot);
+      const uint32_t gpos = (uint32_t)s * (uint32_t)cap + i;  // increases with key index
+      if (sorted) {
+        if (ab || ti) {
+          uint32_t q = run_above + run_tie + (ex >> 16) + (ex & 0xFFFFu);
+          if (q < (uint32_t)E) ent[q] = comp_key(__int_as_float(ce.y), gpos);
+        }
+      } else {
+        if (ab) {
+          uint32_t q = run_above + (ex >> 16);
+          if (q < (uint32_t)k) {
+            oi[q] = ce.x;
+            os[q] = __int_as_float(ce.y);
+          }
+        }
+        if (ti) {
+          uint32_t q = run_tie + (ex & 0xFFFFu);
+          if (q < (uint32_t)E) ent[q] = comp_key(__int_as_float(ce.y), gpos);
+        }
+      }
+      run_above += tot >> 16;
+      run_tie += tot & 0xFFFFu;
+    }
+  }
+  const uint32_t nent = sorted ? run_above + run_tie : run_tie;
+  tie_ovf = nent > (uint32_t)E;
+  if (tie_ovf || run_above != c_above) {
+    enqueue(tie_ovf ? 2 : 4, tau, run_tie);
+    return;
+  }
+  const uint32_t need = (uint32_t)k - c_above;
+  const int P = next_pow2((int)nent < 1 ? 1 : (int)nent);
+  for (int i = tid; i < P; i += kSelThreads)
+    if ((uint32_t)i >= nent) ent[i] = 0ull;
+  __syncthreads();
+  bitonic_sort_desc<kSelThreads>(ent, P);
+  const uint32_t first = sorted ? 0u : c_above;
+  const uint32_t take = sorted ? min(nent, (uint32_t)k) : min(need, nent);
+  for (uint32_t i = tid; i < take; i += kSelThreads) {
+    uint32_t gp = comp_pos(ent[i]);
+    uint32_t s = gp / (uint32_t)cap, j = gp - s * (uint32_t)cap;
+    int2 ce = cand[((int64_t)row * S + s) * cap + j];
+    oi[first + i] = ce.x;
+    os[first + i] = __int_as_float(ce.y);
+  }
+  for (uint32_t i = first + take + tid; i < (uint32_t)k; i += kSelThreads) {
+    oi[i] = -1;
+    os[i] = -__builtin_inff();
+  }
+  if (stats && tid == 0) {
+    int32_t* st = stats + (int64_t)row * 4;
+    st[0] = (int32_t)total_c;
+    st[1] = tau;
+    st[2] = 0;
+    st[3] = (int32_t)run_tie;
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Exact fallback for the scores-in entry: the queued rows go through plain
+// radix selection over all their visible scores. Persistent: block b handles
+// queue entries b, b + grid, ...; the queue length is read on the device.
+// ---------------------------------------------------------------------------
+__global__ __launch_bounds__(kSelThreads) void k_fallback_scores(
+    const float* scores, int64_t stride, int nk, const int32_t* offs, int k, uint32_t flags,
+    const uint32_t* qctl, const int32_t* queue, int32_t* out_i, float* out_s) {
+  extern __shared__ __align__(16) uint8_t lds[];
+  const uint32_t n = qctl[0];
+  for (uint32_t r = blockIdx.x; r < n; r += gridDim.x) {
+    const int row = queue[r];
+    int e = offs ? offs[row] : nk;
+    e = e < 0 ? 0 : (e > nk ? nk : e);
+    radix_select_row<kSelThreads>(scores + (int64_t)row * stride, e, k, out_i + (int64_t)row * k,
+                                  out_s + (int64_t)row * k, flags & LT_SORTED_OUTPUT, lds);
+    __syncthreads();
+  }
+}
+
+// Plain radix selection of every row (no sampling, no filtering).
+__global__ __launch_bounds__(kSelThreads) void k_radix(const float* scores, int64_t stride, int nk,
+                                                       const int32_t* offs, int k, uint32_t flags,
+                                                       int32_t* out_i, float* out_s) {
+  extern __shared__ __align__(16) uint8_t lds[];
+  const int row = blockIdx.x;
+  int e = offs ? offs[row] : nk;
+  e = e < 0 ? 0 : (e > nk ? nk : e);
+  radix_select_row<kSelThreads>(scores + (int64_t)row * stride, e, k, out_i + (int64_t)row * k,
+                                out_s + (int64_t)row * k, flags & LT_SORTED_OUTPUT, lds);
+}
+
+// ---------------------------------------------------------------------------
+// Host launchers
+// ---------------------------------------------------------------------------
+hipError_t launch_init(uint32_t* qctl, hipStream_t st) {
+  hipLaunchKernelGGL(k_init, dim3(1), dim3(64), 0, st, qctl);
+  return hipGetLastError();
+}
+
+hipError_t launch_range(bool from_scores, const float* src, int64_t stride, int nq, int nk,
+                        const int32_t* offs, int ns, int blk, uint64_t seed, int m, int k,
+                        RowParam* params, hipStream_t st) {
+  dim3 grid((nq + 3) / 4);
+  if (from_scores)
+    hipLaunchKernelGGL(k_range<true>, grid, dim3(256), 0, st, src, stride, nq, nk, offs, ns, blk, seed, m, k, params);
+  else
+    hipLaunchKernelGGL(k_range<false>, grid, dim3(256), 0, st, src, stride, nq, nk, offs, ns, blk, seed, m, k, params);
+  return hipGetLastError();
+}
+
+hipError_t launch_filter(const float* scores, int64_t stride, int nq, int nk, const int32_t* offs,
+                         const RowParam* params, int S, int L, int cap, int m, int k, int refresh,
+                         uint32_t* cnt, uint32_t* hist, int2* cand, hipStream_t st) {
+  const int units = nq * S;
+  dim3 grid((units + kFilterWaves - 1) / kFilterWaves);
+  hipLaunchKernelGGL(k_filter, grid, dim3(kFilterWaves * kWave), 0, st, scores, stride, nq, nk, offs,
+                     params, S, L, cap, m, k, refresh, cnt, hist, cand);
+  return hipGetLastError();
+}
+
+size_t select_lds_bytes(int E) { return kMaxBins * 4 + 64 + (size_t)E * 8; }
+
+hipError_t launch_select(const RowParam* params, const uint32_t* cnt, const uint32_t* hist,
+                         const int2* cand, int nq, int S, int cap, int m, int k, int E,
+                         uint32_t flags, int32_t* out_i, float* out_s, uint32_t* qctl,
+                         int32_t* queue, int32_t* stats, hipStream_t st) {
+  size_t lds = select_lds_bytes(E);
+  if (lds > 65536) (void)hipFuncSetAttribute((const void*)k_select, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+  hipLaunchKernelGGL(k_select, dim3(nq), dim3(kSelThreads), lds, st, params, cnt, hist, cand, nq, S,
+                     cap, m, k, E, flags, out_i, out_s, qctl, queue, stats);
+  return hipGetLastError();
+}
+
+hipError_t launch_fallback_scores(const float* scores, int64_t stride, int nk, const int32_t* offs,
+                                  int k, uint32_t flags, const uint32_t* qctl, const int32_t* queue,
+                                  int32_t* out_i, float* out_s, int grid, hipStream_t st) {
+  if (radix_lds_bytes(k) > 65536)
+    (void)hipFuncSetAttribute((const void*)k_fallback_scores, hipFuncAttributeMaxDynamicSharedMemorySize,
+                              (int)radix_lds_bytes(k));
+  hipLaunchKernelGGL(k_fallback_scores, dim3(grid), dim3(kSelThreads), radix_lds_bytes(k), st, scores,
+                     stride, nk, offs, k, flags, qctl, queue, out_i, out_s);
+  return hipGetLastError();
+}
+
+hipError_t launch_radix(const float* scores, int64_t stride, int nq, int nk, const int32_t* offs,
+                        int k, uint32_t flags, int32_t* out_i, float* out_s, hipStream_t st) {
+  if (radix_lds_bytes(k) > 65536)
+    (void)hipFuncSetAttribute((const void*)k_radix, hipFuncAttributeMaxDynamicSharedMemorySize,
+                              (int)radix_lds_bytes(k));
+  hipLaunchKernelGGL(k_radix, dim3(nq), dim3(kSelThreads), radix_lds_bytes(k), st, scores, stride, nk,
+                     offs, k, flags, out_i, out_s);
+  return hipGetLastError();
+}
+
+}  // namespace lt

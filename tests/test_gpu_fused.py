@@ -1,0 +1,136 @@
+"""GPU parity of the fused Indexer-TopK (lt_indexer_topk) against the oracle.
+
+* real-valued inputs of every workload law, at sizes the oracle finishes in
+  seconds (several query and key tiles, ragged tails): tolerance + swap rule;
+* exact-arithmetic inputs: bit-exact sets and scores;
+* internal consistency: the fused result equals lt_topk_select over the dense
+  score matrix, bit for bit (same score arithmetic);
+* forced fallback, tiny capacity, one bin, no sample: unchanged results;
+* edge shapes: k = 1, rows shorter than k, empty rows, no mask.
+"""
+import numpy as np
+import pytest
+import torch
+
+from paper_2607_11976_amd import litetopk as lt
+from paper_2607_11976_amd import workloads
+from helpers import oracle_topk, to_dev
+from parity import RTOL, check_row_exact, check_row_tol, visible
+
+pytestmark = pytest.mark.gpu
+
+
+def _fused(x, k, mode="dsa", **opt):
+    d = to_dev(x)
+    nq = d["q"].shape[0]
+    stats = torch.full((nq, 4), -7, dtype=torch.int32, device="cuda")
+    opts = lt.make_options(row_stats=stats, **opt)
+    gi, gs = lt.indexer_topk(d["q"], d["w"], d["keys"], k, d["offsets"], d["q_scale"], d["k_scale"], mode=mode,
+                             options=opts)
+    torch.cuda.synchronize()
+    return gi.cpu().numpy(), gs.cpu().numpy(), stats.cpu().numpy()
+
+
+def _check_tol(x, dtype, k, mode, gi, gs, rows=None):
+    ri, rs, full = oracle_topk(x, dtype, k, mode, rows=rows)
+    nq, nk = x["q"].shape[0], x["keys"].shape[0]
+    e = visible(None if x["offsets"] is None else x["offsets"].numpy(), nq, nk)
+    rows = range(nq) if rows is None else rows
+    for i, t in enumerate(rows):
+        check_row_tol(gi[t], gs[t], ri[i], rs[i], full[i], int(e[t]), k, RTOL[dtype])
+
+
+LAWS = [
+    # name, base config, nq, nk, k
+    ("tiny_fp32_full", "tiny_fp32", None, None, None),
+    ("dsa_bf16", "dsa_bf16_128k", 21, 20011, 2048),
+    ("dsa_bf16_smallk", "dsa_bf16_128k", 19, 7000, 64),
+    ("dsa_fp8", "dsa_fp8_1m", 17, 30001, 2048),
+    ("adversarial_bf16", "adversarial_bf16_256k", 16, 40000, 2048),
+    ("retrieval_bf16", "retrieval_bf16_4m", 70, 50000, 100),
+]
+
+
+@pytest.mark.parametrize("law", LAWS, ids=[l[0] for l in LAWS])
+def test_fused_parity_real_inputs(lib, law):
+    name, base, nq, nk, k = law
+    cfg = workloads.CONFIGS[base]
+    cfg = workloads.scaled(cfg, nq=nq, nk=nk) if nq else cfg
+    k = cfg.k if k is None else k
+    x = workloads.generate(cfg, seed=workloads.CONFIG_SEEDS[base])
+    gi, gs, stats = _fused(x, k, cfg.mode)
+    _check_tol(x, cfg.dtype, k, cfg.mode, gi, gs)
+    assert not np.any(stats[:, 2] == 4)
+
+
+@pytest.mark.parametrize("dtype,h,d", [("f32", 4, 64), ("bf16", 64, 128), ("bf16", 4, 128), ("bf16", 1, 128),
+                                       ("fp8", 64, 128)])
+@pytest.mark.parametrize("sorted_out", [True, False])
+def test_fused_exact_inputs_bit_exact(lib, dtype, h, d, sorted_out):
+    nq, nk, k = 23, 3001, 200
+    x = workloads.exact_inputs(nq, nk, h, d, dtype, seed=11)
+    gi, gs, _ = _fused(x, k, "dsa", sorted_output=sorted_out)
+    ri, rs, _ = oracle_topk(x, dtype, k, "dsa")
+    e = visible(x["offsets"].numpy(), nq, nk)
+    for t in range(nq):
+        check_row_exact(gi[t], gs[t], ri[t], rs[t], int(e[t]), k, sorted_out)
+
+
+@pytest.mark.parametrize("base", ["dsa_bf16_128k", "dsa_fp8_1m", "tiny_fp32", "adversarial_bf16_256k"])
+def test_fused_equals_select_over_dense_scores(lib, base):
+    cfg = workloads.CONFIGS[base]
+    cfg = workloads.scaled(cfg, nq=min(cfg.nq, 24), nk=min(cfg.nk, 25000))
+    k = min(cfg.k, 1024)
+    x = workloads.generate(cfg, seed=5)
+    d = to_dev(x)
+    dense = lt.indexer_scores(d["q"], d["w"], d["keys"], d["q_scale"], d["k_scale"], mode=cfg.mode)
+    si, ss = lt.topk_select(dense, k, causal_offsets=d["offsets"], options=lt.make_options(sorted_output=True))
+    fi, fs, _ = _fused(x, k, cfg.mode, sorted_output=True)
+    np.testing.assert_array_equal(fi, si.cpu().numpy())
+    np.testing.assert_array_equal(fs.view(np.uint32), ss.cpu().numpy().view(np.uint32))
+
+
+@pytest.mark.parametrize("opt", [
+    dict(force_fallback=True),
+    dict(capacity=64),
+    dict(num_bins=1),
+    dict(sample_size=0),
+    dict(key_splits=4),
+    dict(refresh_tiles=1, num_bins=16),
+], ids=lambda o: ",".join(f"{a}={b}" for a, b in o.items()))
+def test_fused_forced_paths_are_exact(lib, opt):
+    cfg = workloads.scaled(workloads.CONFIGS["dsa_bf16_128k"], nq=10, nk=9000)
+    k = 256
+    x = workloads.generate(cfg, seed=8)
+    ref = _fused(x, k, "dsa", sorted_output=True)
+    got = _fused(x, k, "dsa", sorted_output=True, **opt)
+    np.testing.assert_array_equal(got[0], ref[0])
+    np.testing.assert_array_equal(got[1].view(np.uint32), ref[1].view(np.uint32))
+    _check_tol(x, "bf16", k, "dsa", got[0], got[1])
+    if opt.get("force_fallback"):
+        assert np.all(got[2][:, 2] == 3)
+    if opt.get("capacity") == 64:
+        assert np.all(got[2][:, 2] == 1)
+
+
+def test_fused_edge_shapes(lib):
+    cfg = workloads.scaled(workloads.CONFIGS["dsa_bf16_128k"], nq=13, nk=700)
+    x = workloads.generate(cfg, seed=4)
+    offs = np.array([0, 1, 2, 5, 63, 64, 65, 300, 699, 700, 800, -4, 511], dtype=np.int32)
+    x["offsets"] = torch.from_numpy(offs)
+    for k in (1, 3, 64, 512, 1000):
+        gi, gs, _ = _fused(x, k, "dsa")
+        _check_tol(x, "bf16", k, "dsa", gi, gs)
+    x["offsets"] = None
+    gi, gs, _ = _fused(x, 50, "dsa")
+    _check_tol(x, "bf16", 50, "dsa", gi, gs)
+
+
+def test_fused_deterministic(lib):
+    cfg = workloads.scaled(workloads.CONFIGS["dsa_bf16_128k"], nq=16, nk=20000)
+    x = workloads.generate(cfg, seed=6)
+    a = _fused(x, 512, "dsa")
+    b = _fused(x, 512, "dsa")
+    np.testing.assert_array_equal(a[0], b[0])
+    np.testing.assert_array_equal(a[1].view(np.uint32), b[1].view(np.uint32))
+    np.testing.assert_array_equal(a[2], b[2])
