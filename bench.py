@@ -1,0 +1,252 @@
+"""Benchmark of the fused Indexer-TopK on one MI355X.
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--no-1m] [--no-cpu]
+
+A step is one lt_indexer_topk call over the whole 4096-query x 131072-key DSA
+workload (64 indexer heads of dim 128, bf16, k = 2048, causal chunk at the end
+of the context): sample, range, fused score+filter scan, final select and
+fallback, inputs resident in HBM. Prints ONE JSON line with
+
+  value          visible query-key pairs scored and selected per second;
+  roofline       the fused scan kernel (the dominant one) against the bf16
+                 MFMA peak, its duration taken from HIP events recorded
+                 around it on the library's stream over the timed steps;
+  cpu_baseline   the CPU oracle timed on an evenly spaced sample of rows;
+  unfused        the materialising baseline (dense scores + radix select);
+  ctx_1m         the same measurement for the 2048 x 1M fp8 workload.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+import torch
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+from paper_2607_11976_amd import litetopk as lt  # noqa: E402
+from paper_2607_11976_amd import workloads  # noqa: E402
+
+METRIC = "query-key pairs scored+selected/s at 128K/1M ctx; % MFMA & HBM roofline"
+PEAK_TFLOPS = {"bf16": 2500.0, "fp8": 5000.0, "f32": 157.3}
+HBM_PEAK_GBS = 8000.0
+# FETCH_SIZE / WRITE_SIZE of the fused scan kernel (KiB per dispatch, from
+# rocprofv3 --pmc runs of this benchmark) and the counter/actual-byte factor
+# of a plain device copy measured the same way. None until measured.
+TRAFFIC_KIB = {"dsa_bf16_128k": None}
+COPY_FACTOR = None
+
+
+def visible_pairs(cfg) -> int:
+    if not cfg.causal:
+        return cfg.nq * cfg.nk
+    return int(workloads.causal_offsets(cfg.nq, cfg.nk).astype(np.int64).sum())
+
+
+def timed_steps(fn, steps, warmup):
+    for _ in range(warmup):
+        fn()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(steps):
+        fn()
+    torch.cuda.synchronize()
+    return (time.perf_counter() - t0) * 1e3 / steps
+
+
+def measure(name: str, steps: int, warmup: int, unfused: bool):
+    cfg = workloads.CONFIGS[name]
+    x = workloads.generate(cfg, seed=workloads.CONFIG_SEEDS[name])
+    dev = torch.device("cuda")
+    q, w, keys = x["q"].to(dev), x["w"].to(dev), x["keys"].to(dev)
+    qs = None if x["q_scale"] is None else x["q_scale"].to(dev)
+    ks = None if x["k_scale"] is None else x["k_scale"].to(dev)
+    offs = x["offsets"].to(dev)
+    del x
+    nq, nk, k = cfg.nq, cfg.nk, cfg.k
+    pairs = visible_pairs(cfg)
+    dt = lt._dtype_code(q)
+    out = (torch.empty((nq, k), dtype=torch.int32, device=dev), torch.empty((nq, k), dtype=torch.float32, device=dev))
+    # one set of stage events per timed step, read after the timed region
+    evs = [lt.StageEvents() for _ in range(steps)]
+    optss = [lt.make_options(stage_events=e) for e in evs]
+    ws = lt.indexer_topk_workspace(nq, nk, cfg.h, cfg.d, dt, cfg.mode, k, optss[0], dev)
+
+    def step(i):
+        lt.indexer_topk(q, w, keys, k, offs, qs, ks, mode=cfg.mode, options=optss[i], out=out, workspace=ws)
+
+    for _ in range(warmup):
+        step(0)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(steps):
+        step(i)
+    torch.cuda.synchronize()
+    ms = (time.perf_counter() - t0) * 1e3 / steps
+    stages = {s: 0.0 for s in lt.STAGES}
+    for e in evs:
+        for s, v in e.stage_ms().items():
+            stages[s] += v / steps
+        e.close()
+
+    # survivors and fallback rows (untimed call with row statistics)
+    stats = torch.zeros((nq, 4), dtype=torch.int32, device=dev)
+    lt.indexer_topk(q, w, keys, k, offs, qs, ks, mode=cfg.mode, options=lt.make_options(row_stats=stats),
+                    out=out, workspace=ws)
+    st = stats.cpu().numpy()
+    res = dict(ms=ms, pairs=pairs, stages=stages, survivors_mean=float(st[:, 0].mean()),
+               survivors_max=int(st[:, 0].max()), fallback_rows=int((st[:, 2] != 0).sum()),
+               tie_bin_mean=float(st[:, 3].mean()))
+
+    if unfused:
+        dense = torch.empty((nq, nk), dtype=torch.float32, device=dev)
+        oi = torch.empty((nq, k), dtype=torch.int32, device=dev)
+        os_ = torch.empty((nq, k), dtype=torch.float32, device=dev)
+
+        def base():
+            lt.indexer_scores(q, w, keys, qs, ks, mode=cfg.mode, out=dense)
+            lt.topk_radix(dense, k, causal_offsets=offs, out=(oi, os_))
+
+        res["unfused_ms"] = timed_steps(base, max(2, steps // 2), 1)
+        ms_sc = timed_steps(lambda: lt.indexer_scores(q, w, keys, qs, ks, mode=cfg.mode, out=dense), 3, 1)
+        res["unfused_score_ms"] = ms_sc
+        same = torch.equal(torch.sort(oi, dim=1)[0], torch.sort(out[0], dim=1)[0])
+        res["unfused_same_sets"] = bool(same)
+        del dense
+    del ws, q, keys, w
+    torch.cuda.empty_cache()
+    return cfg, res
+
+
+def roofline(cfg, res):
+    flops = 2.0 * cfg.h * cfg.d * res["pairs"]
+    filt_ms = res["stages"]["filter"]
+    achieved = flops / (filt_ms * 1e-3) / 1e12
+    peak = PEAK_TFLOPS[cfg.dtype]
+    traffic = None
+    kib = TRAFFIC_KIB.get(cfg.name)
+    if kib is not None and COPY_FACTOR is not None:
+        traffic = (kib[0] + kib[1]) * 1024.0 / COPY_FACTOR
+    return {"bound": "mfma", "achieved": round(achieved, 2), "peak": peak, "unit": "TFLOP/s",
+            "frac": round(achieved / peak, 4), "traffic": traffic, "kernel": "k_fused (score+filter scan)",
+            "kernel_ms": round(filt_ms, 4), "algorithmic_flops": flops}
+
+
+def cpu_oracle_rate(name: str, budget_s: float):
+    from oracle import litetopk_oracle as orc
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([p.get("num_threads", 1) for p in threadpool_info()] + [1])
+    except Exception:  # pragma: no cover
+        threads = len(os.sched_getaffinity(0))
+    cfg = workloads.CONFIGS[name]
+    x = workloads.generate(cfg, seed=workloads.CONFIG_SEEDS[name])
+
+    def npy(t):
+        if t is None:
+            return None
+        if t.dtype == torch.bfloat16:
+            return t.view(torch.int16).numpy().view(np.uint16)
+        return t.numpy()
+
+    qn, kn, wn = npy(x["q"]), npy(x["keys"]), npy(x["w"])
+    qs, ks = npy(x["q_scale"]), npy(x["k_scale"])
+    offs = x["offsets"].numpy() if x["offsets"] is not None else None
+    e = np.clip(offs.astype(np.int64), 0, cfg.nk) if offs is not None else np.full(cfg.nq, cfg.nk)
+
+    def run(rows):
+        t0 = time.perf_counter()
+        orc.indexer_topk(qn, cfg.dtype, qs, wn, kn, ks, cfg.k, cfg.mode, offs, rows=rows)
+        return time.perf_counter() - t0
+
+    probe = [0, cfg.nq - 1]
+    t = run(probe)
+    per_row = max(t / len(probe), 1e-3)
+    n = int(min(cfg.nq, max(4, budget_s / per_row)))
+    rows = np.unique(np.linspace(0, cfg.nq - 1, n).round().astype(int)).tolist()
+    t = run(rows)
+    pr = float(e[rows].sum())
+    return {"value": pr / t, "unit": "pairs/s", "cores": int(threads), "kind": "oracle",
+            "sample": "%d evenly spaced rows of %s (first and last included), %.0f pairs in %.1f s; numpy float64"
+                      % (len(rows), name, pr, t), "seconds": round(t, 2)}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--no-1m", action="store_true", help="skip the 1M-context fp8 measurement")
+    ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
+    ap.add_argument("--no-unfused", action="store_true", help="skip the unfused baseline")
+    ap.add_argument("--cpu-budget", type=float, default=15.0)
+    args = ap.parse_args()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py measures one GPU only: this build has no multi-GPU path (the fused Indexer-TopK "
+              "shards by query rows with no communication); run with --gpus 1", file=sys.stderr)
+        sys.exit(2)
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        sys.exit(2)
+    lt.load()
+    rank0 = int(os.environ.get("RANK", "0")) == 0
+
+    cfg, res = measure("dsa_bf16_128k", args.steps, args.warmup, not args.no_unfused)
+    print("[bench] dsa_bf16_128k: %.3f ms/step, stages %s" % (res["ms"], {k: round(v, 3) for k, v in
+                                                                         res["stages"].items()}),
+          file=sys.stderr, flush=True)
+    line = {
+        "metric": METRIC,
+        "value": res["pairs"] / (res["ms"] * 1e-3),
+        "unit": "pairs/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(res["ms"], 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": "dsa_bf16_128k", "num_queries": cfg.nq, "num_keys": cfg.nk, "heads": cfg.h,
+                   "head_dim": cfg.d, "k": cfg.k, "causal": cfg.causal, "visible_pairs": res["pairs"],
+                   "parallelism": "single GPU"},
+        "roofline": roofline(cfg, res),
+        "stages_ms": {k: round(v, 4) for k, v in res["stages"].items()},
+        "survivors_per_row": {"mean": round(res["survivors_mean"], 1), "max": res["survivors_max"],
+                              "threshold_bin_mean": round(res["tie_bin_mean"], 1)},
+        "fallback_rows": res["fallback_rows"],
+        "bytes_written_per_query": {
+            "fused": round(res["survivors_mean"] * 8 + cfg.k * 8, 1),
+            "unfused": cfg.nk * 4 + cfg.k * 8},
+    }
+    if "unfused_ms" in res:
+        line["unfused"] = {"ms_per_step": round(res["unfused_ms"], 4),
+                           "score_ms": round(res["unfused_score_ms"], 4),
+                           "pairs_per_s": res["pairs"] / (res["unfused_ms"] * 1e-3),
+                           "same_sets": res["unfused_same_sets"]}
+    if not args.no_1m:
+        cfg2, res2 = measure("dsa_fp8_1m", max(3, args.steps // 4), 2, not args.no_unfused)
+        print("[bench] dsa_fp8_1m: %.3f ms/step" % res2["ms"], file=sys.stderr, flush=True)
+        m = {"workload": "dsa_fp8_1m", "dtype": "fp8", "ms_per_step": round(res2["ms"], 4),
+             "value": res2["pairs"] / (res2["ms"] * 1e-3), "unit": "pairs/s", "visible_pairs": res2["pairs"],
+             "roofline": roofline(cfg2, res2), "stages_ms": {k: round(v, 4) for k, v in res2["stages"].items()},
+             "survivors_per_row_mean": round(res2["survivors_mean"], 1), "fallback_rows": res2["fallback_rows"]}
+        if "unfused_ms" in res2:
+            m["unfused_ms_per_step"] = round(res2["unfused_ms"], 4)
+            m["unfused_same_sets"] = res2["unfused_same_sets"]
+        line["ctx_1m"] = m
+    if rank0 and not args.no_cpu:
+        line["cpu_baseline"] = cpu_oracle_rate("dsa_bf16_128k", args.cpu_budget)
+    if rank0:
+        print(json.dumps(line), flush=True)
+
+
+if __name__ == "__main__":
+    main()
