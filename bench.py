@@ -186,6 +186,10 @@ def main():
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
     ap.add_argument("--no-unfused", action="store_true", help="skip the unfused baseline")
     ap.add_argument("--cpu-budget", type=float, default=15.0)
+    ap.add_argument("--profile-only", default=None, metavar="WORKLOAD",
+                    help="run only `steps` fused calls of one workload (for rocprofv3 counter passes)")
+    ap.add_argument("--copy-calib", type=int, default=0, metavar="MIB",
+                    help="run only device copies of MIB MiB (calibrates FETCH_SIZE / WRITE_SIZE)")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU only: this build has no multi-GPU path (the fused Indexer-TopK "
@@ -196,6 +200,26 @@ def main():
         sys.exit(2)
     lt.load()
     rank0 = int(os.environ.get("RANK", "0")) == 0
+    if args.copy_calib:
+        n = args.copy_calib * (1 << 20) // 4
+        src = torch.ones(n, dtype=torch.float32, device="cuda")
+        dst = torch.empty_like(src)
+        for _ in range(max(1, args.steps)):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        print(json.dumps({"copy_bytes": n * 4, "copies": max(1, args.steps)}))
+        return
+    if args.profile_only:
+        cfg = workloads.CONFIGS[args.profile_only]
+        x = workloads.generate(cfg, seed=workloads.CONFIG_SEEDS[args.profile_only])
+        d = {kk: (None if v is None else v.to("cuda")) for kk, v in x.items()
+             if kk in ("q", "w", "keys", "q_scale", "k_scale", "offsets")}
+        for _ in range(max(1, args.steps)):
+            lt.indexer_topk(d["q"], d["w"], d["keys"], cfg.k, d["offsets"], d["q_scale"], d["k_scale"],
+                            mode=cfg.mode)
+        torch.cuda.synchronize()
+        print(json.dumps({"profiled": args.profile_only, "calls": max(1, args.steps)}))
+        return
 
     cfg, res = measure("dsa_bf16_128k", args.steps, args.warmup, not args.no_unfused)
     print("[bench] dsa_bf16_128k: %.3f ms/step, stages %s" % (res["ms"], {k: round(v, 3) for k, v in

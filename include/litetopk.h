@@ -91,8 +91,7 @@ typedef struct lt_options {
                               entry uses 3k); 0 disables the gate                */
   int32_t capacity;        /* candidate slots per (row, key split); <= 0 = default
                               max(12k, 2048) (sec. 4.2: 12k for k = 2048)       */
-  int32_t key_splits;      /* key-range splits per row in the fused scan; 0 = auto */
-  int32_t refresh_tiles;   /* key tiles between threshold refreshes; 0 = default */
+  int32_t key_splits;      /* key-range splits per row; 0 = auto (fused), 1 (scores-in) */
   uint32_t flags;          /* LT_SORTED_OUTPUT | LT_FORCE_FALLBACK               */
   uint64_t seed;           /* seed of the key sample                             */
   void** stage_events;     /* NULL, or LT_NUM_STAGE_EVENTS hipEvent_t handles     */

@@ -12,8 +12,6 @@ using namespace lt;
 namespace {
 
 constexpr int kDefaultBins = 256;
-constexpr int kDefaultRefreshTiles = 4;     // fused scan: key tiles between refreshes
-constexpr int kDefaultRefreshChunks = 4;    // scores-in scan: 256-key chunks between refreshes
 constexpr int kFallbackGridFused = 64;      // rows re-scored concurrently (scratch rows)
 constexpr int kFallbackGridScores = 256;
 constexpr int kTargetBlocks = 256;          // one block per CU before key splitting stops
@@ -23,7 +21,7 @@ constexpr int kSampleBlockScores = 64;      // scores-in sample: runs of 64 cons
 inline size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 
 struct Resolved {
-  int m, ns, cap, S, L, refresh, E;
+  int m, ns, cap, S, L, E;
   uint32_t flags;
   uint64_t seed;
   void** ev;
@@ -103,7 +101,6 @@ Resolved resolve_fused(const lt_options* o, int nq, int nk, int k, int mode, con
   const int per = (nk + S - 1) / S;
   r.L = ((per + sh.keys_per_step - 1) / sh.keys_per_step) * sh.keys_per_step;
   if (r.L == 0) r.L = sh.keys_per_step;
-  r.refresh = o->refresh_tiles > 0 ? o->refresh_tiles : kDefaultRefreshTiles;
   return r;
 }
 
@@ -120,7 +117,6 @@ Resolved resolve_scores(const lt_options* o, int nq, int nk, int k) {
   r.S = std::max(1, std::min(S, (nk + 255) / 256 + 1));
   const int per = (nk + r.S - 1) / r.S;
   r.L = std::max(256, ((per + 255) / 256) * 256);
-  r.refresh = o->refresh_tiles > 0 ? o->refresh_tiles : kDefaultRefreshChunks;
   (void)nq;
   return r;
 }
@@ -156,7 +152,6 @@ void lt_options_default(lt_options* o) {
   o->sample_size = -1;
   o->capacity = 0;
   o->key_splits = 0;
-  o->refresh_tiles = 0;
   o->flags = 0;
   o->seed = 0x5EED5EEDull;
   o->stage_events = nullptr;
@@ -218,7 +213,7 @@ int lt_indexer_topk(const void* q, const float* q_scale, const float* w, const v
   if ((e = launch_range(false, samp, r.ns, nq, nk, offs, r.ns, 1, r.seed, r.m, k, params, st)) != hipSuccess)
     return hip_status(e);
   record(r, LT_STAGE_FILTER, st);
-  if ((e = launch_fused_scan(a, params, r.S, r.L, r.cap, r.m, k, r.refresh, cnt, hist, cand, st)) != hipSuccess)
+  if ((e = launch_fused_scan(a, params, r.S, r.L, r.cap, r.m, k, cnt, hist, cand, st)) != hipSuccess)
     return hip_status(e);
   record(r, LT_STAGE_SELECT, st);
   if ((e = launch_select(params, cnt, hist, cand, nq, r.S, r.cap, r.m, k, r.E, r.flags, out_idx, out_scores, qctl,
@@ -285,8 +280,7 @@ int lt_topk_select(const float* scores, int64_t stride, int32_t nq, int32_t nk, 
                         st)) != hipSuccess)
     return hip_status(e);
   record(r, LT_STAGE_FILTER, st);
-  if ((e = launch_filter(scores, stride, nq, nk, offs, params, r.S, r.L, r.cap, r.m, k, r.refresh, cnt, hist,
-                         cand, st)) != hipSuccess)
+  if ((e = launch_filter(scores, stride, nq, nk, offs, params, r.S, r.L, r.cap, r.m, k, cnt, hist, cand, st)) != hipSuccess)
     return hip_status(e);
   record(r, LT_STAGE_SELECT, st);
   if ((e = launch_select(params, cnt, hist, cand, nq, r.S, r.cap, r.m, k, r.E, r.flags, out_idx, out_scores, qctl,

@@ -16,8 +16,8 @@ hipError_t launch_range(bool from_scores, const float* src, int64_t stride, int 
                         const int32_t* offs, int ns, int blk, uint64_t seed, int m, int k,
                         RowParam* params, hipStream_t st);
 hipError_t launch_filter(const float* scores, int64_t stride, int nq, int nk, const int32_t* offs,
-                         const RowParam* params, int S, int L, int cap, int m, int k, int refresh,
-                         uint32_t* cnt, uint32_t* hist, int2* cand, hipStream_t st);
+                         const RowParam* params, int S, int L, int cap, int m, int k, uint32_t* cnt,
+                         uint32_t* hist, int2* cand, hipStream_t st);
 size_t select_lds_bytes(int E);
 hipError_t launch_select(const RowParam* params, const uint32_t* cnt, const uint32_t* hist,
                          const int2* cand, int nq, int S, int cap, int m, int k, int E,
@@ -56,8 +56,7 @@ hipError_t launch_sample_scores(const ScoreArgs& a, int ns, uint64_t seed, float
 hipError_t launch_dense_scores(const ScoreArgs& a, float* out, int64_t ld, hipStream_t st);
 // Fused score + gate + write-back scan over S key splits of L keys each.
 hipError_t launch_fused_scan(const ScoreArgs& a, const RowParam* params, int S, int L, int cap, int m,
-                             int k, int refresh, uint32_t* cnt, uint32_t* hist, int2* cand,
-                             hipStream_t st);
+                             int k, uint32_t* cnt, uint32_t* hist, int2* cand, hipStream_t st);
 // Exact fallback for queued rows: dense re-score into scratch [grid, nk], then radix select.
 hipError_t launch_fused_fallback(const ScoreArgs& a, int k, uint32_t flags, const uint32_t* qctl,
                                  const int32_t* queue, float* scratch, int grid, int32_t* out_i,

@@ -107,7 +107,9 @@ struct Cfg {
   static constexpr bool GROUPED = H <= 4;
   static constexpr int GPQ = GROUPED ? 4 / H : 1;      // queries per 4-row group
   static constexpr int NI = GROUPED ? NT * MT * 4 * GPQ : NT * QW / 2;  // scores per lane per tile
+  static constexpr int NIH = GROUPED ? MT * 4 * GPQ : QW;              // per-lane results of one sub-tile
   static_assert((QW * H) % 32 == 0, "a wave must fill whole M tiles");
+  static_assert(NT == 2, "the scan pipelines the two 32-key halves of a tile");
   static_assert(D % M::KI == 0, "head dim must be a multiple of the MFMA K");
   static_assert(ROWB % 16 == 0, "key rows must be a multiple of 16 bytes");
   static_assert(GROUPED ? (4 % H == 0) : (H % 8 == 0 && (NT * QW) % 2 == 0), "unsupported head layout");
@@ -169,83 +171,94 @@ __device__ __forceinline__ void load_q(WaveQ<C>& s, const ScoreArgs& a, int qbas
   }
 }
 
-// q . k for every (row, key) of the tile: acc[nt][mt] holds the 32x32 block of
-// M tile mt against 32-key sub-tile nt. Accumulator register v of a lane is
-// row 8*(v/4) + 4*(lane/32) + v%4 of the M tile, column lane%32.
+// One half step: q . k for every row of the wave against one 32-key sub-tile.
+// acc[mt] is the 32x32 block of M tile mt; accumulator register v of a lane
+// is row 8*(v/4) + 4*(lane/32) + v%4 of the M tile, column lane%32.
 template <class C>
-__device__ __forceinline__ void mma_tile(const WaveQ<C>& s, const uint8_t* tile, f32x16_t (&acc)[C::NT][C::MT]) {
+__device__ __forceinline__ void load_b(const uint8_t* tile, int nt, typename C::M::Frag (&b)[C::KS]) {
   using M = typename C::M;
   const int l = lane_id(), h = l >> 5, r32 = l & 31;
+  const uint8_t* base = tile + (nt * 32 + r32) * C::LSTRIDE + h * M::FB;
 #pragma unroll
-  for (int nt = 0; nt < C::NT; ++nt)
+  for (int ks = 0; ks < C::KS; ++ks) b[ks] = M::load(base + ks * M::KI * M::ES);
+}
+
+template <class C>
+__device__ __forceinline__ void mma_half(const WaveQ<C>& s, const typename C::M::Frag (&b)[C::KS],
+                                         f32x16_t (&acc)[C::MT]) {
+  using M = typename C::M;
 #pragma unroll
-    for (int mt = 0; mt < C::MT; ++mt) acc[nt][mt] = f32x16_t{};
+  for (int mt = 0; mt < C::MT; ++mt) acc[mt] = f32x16_t{};
 #pragma unroll
-  for (int ks = 0; ks < C::KS; ++ks) {
+  for (int ks = 0; ks < C::KS; ++ks)
 #pragma unroll
-    for (int nt = 0; nt < C::NT; ++nt) {
-      const typename M::Frag b = M::load(tile + (nt * 32 + r32) * C::LSTRIDE + ks * M::KI * M::ES + h * M::FB);
+    for (int mt = 0; mt < C::MT; ++mt) acc[mt] = M::mma(s.qa[mt][ks], b[ks], acc[mt]);
+}
+
+// ReLU of Eq. (1) as IEEE-754-2019 maximum (one v_maximum3_f32; NaN
+// propagates); inner-product mode skips it.
+template <class C>
+__device__ __forceinline__ float relu(float x) {
+  if constexpr (C::RELU) return __builtin_elementwise_maximum(x, 0.0f);
+  else return x;
+}
+
+// Eq. (1) epilogue of one sub-tile in registers: ReLU of every head's dot
+// product and the weighted sum over the heads this lane holds.
+//   GROUPED: out[j], j = (mt*4 + i)*GPQ + sq, are complete scores.
+//   else:    out[q] is the lane's partial sum for query q (half of the heads).
+template <class C>
+__device__ __forceinline__ void reduce_half(const WaveQ<C>& s, const f32x16_t (&acc)[C::MT], float (&out)[C::NIH]) {
+  if constexpr (C::GROUPED) {
 #pragma unroll
-      for (int mt = 0; mt < C::MT; ++mt) acc[nt][mt] = M::mma(s.qa[mt][ks], b, acc[nt][mt]);
-    }
+    for (int mt = 0; mt < C::MT; ++mt)
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int sq = 0; sq < C::GPQ; ++sq) {
+          float sum = 0.0f;
+#pragma unroll
+          for (int r = 0; r < C::H; ++r) {
+            const int v = 4 * i + sq * C::H + r;
+            sum = fmaf(s.wv[mt][v], relu<C>(acc[mt][v]), sum);
+          }
+          out[(mt * 4 + i) * C::GPQ + sq] = sum;
+        }
+  } else {
+#pragma unroll
+    for (int q = 0; q < C::QW; ++q) out[q] = 0.0f;
+#pragma unroll
+    for (int mt = 0; mt < C::MT; ++mt)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int q = (32 * mt + 8 * i) / C::H;
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const int v = 4 * i + r;
+          out[q] = fmaf(s.wv[mt][v], relu<C>(acc[mt][v]), out[q]);
+        }
+      }
   }
 }
 
-// Eq. (1) epilogue in registers: ReLU of every head's dot product, weighted
-// sum over heads (inner-product mode skips the ReLU).
+// Both sub-tiles' results -> the lane's NI complete scores. For H >= 8 the
+// lane halves hold disjoint head subsets of the same (query, key): half 0
+// finishes sub-tile 0 of query q, half 1 sub-tile 1, each sending the partial
+// the other half needs.
 template <class C>
-__device__ __forceinline__ void epilogue(const WaveQ<C>& s, const f32x16_t (&acc)[C::NT][C::MT], float (&out)[C::NI]) {
+__device__ __forceinline__ void combine(const float (&h0)[C::NIH], const float (&h1)[C::NIH], float (&sc)[C::NI]) {
   const int h = lane_id() >> 5;
   if constexpr (C::GROUPED) {
 #pragma unroll
-    for (int nt = 0; nt < C::NT; ++nt)
-#pragma unroll
-      for (int mt = 0; mt < C::MT; ++mt)
-#pragma unroll
-        for (int i = 0; i < 4; ++i)
-#pragma unroll
-          for (int sq = 0; sq < C::GPQ; ++sq) {
-            float sum = 0.0f;
-#pragma unroll
-            for (int r = 0; r < C::H; ++r) {
-              const int v = 4 * i + sq * C::H + r;
-              float x = acc[nt][mt][v];
-              if constexpr (C::RELU) x = fmaxf(x, 0.0f);
-              sum = fmaf(s.wv[mt][v], x, sum);
-            }
-            out[((nt * C::MT + mt) * 4 + i) * C::GPQ + sq] = sum;
-          }
+    for (int j = 0; j < C::NIH; ++j) {
+      sc[j] = h0[j];
+      sc[C::NIH + j] = h1[j];
+    }
   } else {
-    float part[C::NT][C::QW];
-#pragma unroll
-    for (int nt = 0; nt < C::NT; ++nt)
-#pragma unroll
-      for (int q = 0; q < C::QW; ++q) part[nt][q] = 0.0f;
-#pragma unroll
-    for (int nt = 0; nt < C::NT; ++nt)
-#pragma unroll
-      for (int mt = 0; mt < C::MT; ++mt)
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          const int q = (32 * mt + 8 * i) / C::H;
-#pragma unroll
-          for (int r = 0; r < 4; ++r) {
-            const int v = 4 * i + r;
-            float x = acc[nt][mt][v];
-            if constexpr (C::RELU) x = fmaxf(x, 0.0f);
-            part[nt][q] = fmaf(s.wv[mt][v], x, part[nt][q]);
-          }
-        }
-    // Lane halves hold disjoint head subsets of the same (query, key). Pair
-    // the (query, sub-tile) entries: half 0 finishes entry 2i, half 1 entry
-    // 2i+1, each sending the partial the other half needs.
 #pragma unroll
     for (int it = 0; it < C::NI; ++it) {
-      const int e0 = 2 * it, e1 = 2 * it + 1;
-      const float a0 = part[e0 % C::NT][e0 / C::NT];
-      const float a1 = part[e1 % C::NT][e1 / C::NT];
-      const float recv = __shfl_xor(h ? a0 : a1, 32, kWave);
-      out[it] = (h ? a1 : a0) + recv;
+      const float recv = __shfl_xor(h ? h0[it] : h1[it], 32, kWave);
+      sc[it] = (h ? h1[it] : h0[it]) + recv;
     }
   }
 }
@@ -260,25 +273,31 @@ struct SrcSample {
 };
 
 // The block-wide scan of positions [kbeg, kend) of `src` (key index =
-// src.key(position)), double-buffered through LDS. Every wave runs the MFMA
-// tile and the epilogue and hands its scores to `sink`.
+// src.key(position)). Keys flow HBM -> VGPR -> LDS through a ring of three
+// tiles (global loads two tiles ahead, one barrier per tile). Each tile is
+// processed in two half steps that overlap the matrix cores with the vector
+// ALUs: while the MFMAs of one 32-key sub-tile run, the epilogue of the other
+// sub-tile (and the sink's gate / write-back for the previous tile) executes.
+// B fragments are read from LDS one half step ahead.
 template <class C, class Src, class Sink>
 __device__ __forceinline__ void wg_scan(const ScoreArgs& a, const Src& src, int kbeg, int kend, uint8_t* tiles,
                                         const WaveQ<C>& wq, Sink& sink) {
+  using Frag = typename C::M::Frag;
   const int tid = threadIdx.x, l = lane_id(), h = l >> 5, r32 = l & 31;
   const uint8_t* keys = static_cast<const uint8_t*>(a.keys);
   const int nsteps = kend > kbeg ? (kend - kbeg + C::KT - 1) / C::KT : 0;
   if (nsteps == 0) return;
   i32x4_t regs[C::CPT];
+  // Rows past kend are clamped to the last valid row: their scores are never
+  // used (every consumer masks positions >= kend), so no branch is needed.
   auto gload = [&](int k0) {
 #pragma unroll
     for (int c = 0; c < C::CPT; ++c) {
       const int ch = tid + c * C::NTHREADS;
-      regs[c] = i32x4_t{0, 0, 0, 0};
-      if (ch < C::CHUNKS) {
-        const int kk = ch / C::CPK, part = ch - kk * C::CPK, i = k0 + kk;
-        if (i < kend)
-          regs[c] = *reinterpret_cast<const i32x4_t*>(keys + (int64_t)src.key(i) * C::ROWB + part * 16);
+      if (C::CHUNKS % C::NTHREADS == 0 || ch < C::CHUNKS) {
+        const int kk = ch / C::CPK, part = ch - kk * C::CPK;
+        const int i = min(k0 + kk, kend - 1);
+        regs[c] = *reinterpret_cast<const i32x4_t*>(keys + (int64_t)src.key(i) * C::ROWB + part * 16);
       }
     }
   };
@@ -292,32 +311,64 @@ __device__ __forceinline__ void wg_scan(const ScoreArgs& a, const Src& src, int 
       }
     }
   };
-  gload(kbeg);
-  sstore(0);
-  __syncthreads();
-  for (int st = 0; st < nsteps; ++st) {
-    const int k0 = kbeg + st * C::KT;
-    if (st + 1 < nsteps) gload(k0 + C::KT);
-    f32x16_t acc[C::NT][C::MT];
-    mma_tile<C>(wq, tiles + (st & 1) * C::TILE_BYTES, acc);
-    float sc[C::NI];
-    epilogue<C>(wq, acc, sc);
+  // both sub-tiles' results of tile st -> complete scores (fp8: key scales)
+  auto scores = [&](int st, const float (&h0)[C::NIH], const float (&h1)[C::NIH], float (&sc)[C::NI]) {
+    combine<C>(h0, h1, sc);
     if constexpr (C::DT == DT_FP8) {
+      const int k0 = kbeg + st * C::KT;
 #pragma unroll
       for (int it = 0; it < C::NI; ++it) {
         const int nt = h ? C::item_nt(it, 1) : C::item_nt(it, 0);
-        const int pos = k0 + nt * 32 + r32;
-        sc[it] *= pos < kend ? a.k_scale[src.key(pos)] : 0.0f;
+        int pos = k0 + nt * 32 + r32;
+        pos = pos < kbeg ? kbeg : (pos < kend ? pos : kend - 1);
+        sc[it] *= a.k_scale[src.key(pos)];
       }
     }
-    sink.consume(st, k0, kend, sc);
-    if (st + 1 < nsteps) sstore((st + 1) & 1);
+  };
+
+  gload(kbeg);
+  sstore(0);
+  gload(kbeg + C::KT);
+  sstore(1);
+  __syncthreads();
+  Frag b0[C::KS], b1[C::KS];
+  f32x16_t acc0[C::MT], acc1[C::MT];
+#pragma unroll
+  for (int mt = 0; mt < C::MT; ++mt) acc1[mt] = f32x16_t{};
+  float h0[C::NIH], h1[C::NIH];
+#pragma unroll
+  for (int j = 0; j < C::NIH; ++j) h0[j] = 0.0f;
+  load_b<C>(tiles, 0, b0);
+  int cur = 0;  // ring slot of tile st
+  for (int st = 0; st < nsteps; ++st) {
+    const uint8_t* tl = tiles + cur * C::TILE_BYTES;
+    const int nxt = cur == 2 ? 0 : cur + 1, fill = nxt == 2 ? 0 : nxt + 1;
+    gload(kbeg + (st + 2) * C::KT);
+    // half step A: MFMA sub-tile 0 of tile st || epilogue of sub-tile 1 of st-1
+    load_b<C>(tl, 1, b1);
+    mma_half<C>(wq, b0, acc0);
+    reduce_half<C>(wq, acc1, h1);
+    float sc[C::NI];
+    scores(st - 1, h0, h1, sc);
+    // half step B: MFMA sub-tile 1 of tile st || epilogue of sub-tile 0 of st
+    load_b<C>(tiles + nxt * C::TILE_BYTES, 0, b0);
+    mma_half<C>(wq, b1, acc1);
+    reduce_half<C>(wq, acc0, h0);
+    // gate + write-back of tile st-1 while the last MFMAs drain
+    sink.consume(st - 1, kbeg + (st - 1) * C::KT, kend, sc, st > 0);
+    sstore(fill);
     __syncthreads();
+    cur = nxt;
   }
+  reduce_half<C>(wq, acc1, h1);
+  float sc[C::NI];
+  scores(nsteps - 1, h0, h1, sc);
+  sink.consume(nsteps - 1, kbeg + (nsteps - 1) * C::KT, kend, sc, true);
 }
 
 // ---------------------------------------------------------------------------
-// Sinks
+// Sinks. consume(st, k0, kend, scores, live) receives the scores of tile st
+// (positions k0 + ...); live is false for the pipeline's priming call.
 // ---------------------------------------------------------------------------
 
 // Writes every score to out[t * ld + position].
@@ -326,14 +377,14 @@ struct DenseSink {
   float* out;
   int64_t ld;
   int qbase, nq;
-  __device__ void consume(int, int k0, int kend, const float (&sc)[C::NI]) {
+  __device__ void consume(int, int k0, int kend, const float (&sc)[C::NI], bool live) {
     const int l = lane_id(), h = l >> 5, r32 = l & 31;
 #pragma unroll
     for (int it = 0; it < C::NI; ++it) {
       const int q = h ? C::item_q(it, 1) : C::item_q(it, 0);
       const int nt = h ? C::item_nt(it, 1) : C::item_nt(it, 0);
       const int pos = k0 + nt * 32 + r32, t = qbase + q;
-      if (t < nq && pos < kend) out[(int64_t)t * ld + pos] = sc[it];
+      if (live && t < nq && pos < kend) out[(int64_t)t * ld + pos] = sc[it];
     }
   }
 };
@@ -343,14 +394,14 @@ template <class C>
 struct RowSink {
   float* out;
   int qbase, target;
-  __device__ void consume(int, int k0, int kend, const float (&sc)[C::NI]) {
+  __device__ void consume(int, int k0, int kend, const float (&sc)[C::NI], bool live) {
     const int l = lane_id(), h = l >> 5, r32 = l & 31;
 #pragma unroll
     for (int it = 0; it < C::NI; ++it) {
       const int q = h ? C::item_q(it, 1) : C::item_q(it, 0);
       const int nt = h ? C::item_nt(it, 1) : C::item_nt(it, 0);
       const int pos = k0 + nt * 32 + r32;
-      if (qbase + q == target && pos < kend) out[pos] = sc[it];
+      if (live && qbase + q == target && pos < kend) out[pos] = sc[it];
     }
   }
 };
@@ -361,16 +412,28 @@ struct RowSink {
 // are compacted with one ballot per item (mbcnt gives each passing lane its
 // slot; the row's tail is wave-private, so no atomics), written as (key,
 // score) to the row's HBM candidate list, and counted in the row's LDS
-// histogram. Every `refresh` tiles the wave recomputes each row's threshold
-// bin from its histogram; the gate only ever tightens.
+// histogram.
+// Threshold refresh: the wave keeps, per row, `above` = the number of counted
+// candidates in bins strictly above the current threshold bin tau. Whenever
+// above >= k, bin tau + 1 still has a suffix count >= k, so tau advances and
+// above drops by the count of the bin it moves to. This keeps tau equal to
+// the histogram walk's result (the largest bin whose suffix count reaches k)
+// after every tile, at the cost of one ballot per item and a short loop only
+// when the threshold actually moves.
 template <class C>
 struct FusedSink {
-  float delta[C::QW], cc[C::QW], thr[C::QW];
+  float delta[C::QW], cc[C::QW], thr[C::QW], thr_up[C::QW];
   int tau[C::QW], e[C::QW];
-  uint32_t tail[C::QW];
+  uint32_t tail[C::QW], above[C::QW];
   uint32_t* hist;     // LDS, [QW][m] for this wave
   int2* cand;
-  int qbase, nq, S, split, cap, m, k, refresh;
+  int qbase, nq, S, split, cap, m, k;
+
+  __device__ void set_tau(int q, int t) {
+    tau[q] = t;
+    thr[q] = gate_thr(t);
+    thr_up[q] = t < m - 1 ? (float)(t + 1) : __builtin_nanf("");
+  }
 
   __device__ void init(const ScoreArgs& a, const RowParam* params, int kend) {
 #pragma unroll
@@ -390,50 +453,70 @@ struct FusedSink {
       e[q] = ev < kend ? ev : kend;
       delta[q] = dl;
       cc[q] = c;
-      tau[q] = t0;
-      thr[q] = gate_thr(t0);
+      set_tau(q, t0);
       tail[q] = 0;
+      above[q] = 0;
     }
   }
 
-  __device__ void consume(int st, int k0, int, const float (&sc)[C::NI]) {
+  __device__ void consume(int, int k0, int, const float (&sc)[C::NI], bool live) {
     const int l = lane_id(), h = l >> 5, r32 = l & 31;
+    float x[C::NI];
+    bool ps[C::NI];
+    uint64_t any = 0;
     static_for<C::NI>([&](auto IT) {
       constexpr int it = decltype(IT)::value;
       constexpr int qa = C::item_q(it, 0), qb = C::item_q(it, 1);
       constexpr int na = C::item_nt(it, 0), nb = C::item_nt(it, 1);
       const int key = k0 + (h ? nb : na) * 32 + r32;
-      const float x = bin_x(sc[it], h ? delta[qb] : delta[qa], h ? cc[qb] : cc[qa]);
-      const bool pass = key < (h ? e[qb] : e[qa]) && !(x < (h ? thr[qb] : thr[qa]));
+      x[it] = bin_x(sc[it], h ? delta[qb] : delta[qa], h ? cc[qb] : cc[qa]);
+      ps[it] = live && key < (h ? e[qb] : e[qa]) && !(x[it] < (h ? thr[qb] : thr[qa]));
+      any |= __ballot(ps[it]);
+    });
+    if (any == 0) return;  // wave-uniform: nothing passed this tile
+    static_for<C::NI>([&](auto IT) {
+      constexpr int it = decltype(IT)::value;
+      constexpr int qa = C::item_q(it, 0), qb = C::item_q(it, 1);
+      constexpr int na = C::item_nt(it, 0), nb = C::item_nt(it, 1);
+      const bool pass = ps[it];
       const uint64_t mask = __ballot(pass);
+      const uint64_t up = __ballot(pass && x[it] >= (h ? thr_up[qb] : thr_up[qa]));
       const uint32_t mb = mbcnt64(mask);
       uint32_t pos;
       if constexpr (qa == qb) {
         pos = tail[qa] + mb;
         tail[qa] += (uint32_t)__popcll(mask);
+        above[qa] += (uint32_t)__popcll(up);
       } else {
         const uint32_t lo = (uint32_t)__popcll(mask & 0xFFFFFFFFull);
         pos = h ? tail[qb] + mb - lo : tail[qa] + mb;
         tail[qa] += lo;
         tail[qb] += (uint32_t)__popcll(mask) - lo;
+        const uint32_t ulo = (uint32_t)__popcll(up & 0xFFFFFFFFull);
+        above[qa] += ulo;
+        above[qb] += (uint32_t)__popcll(up) - ulo;
       }
       if (pass) {
+        const int key = k0 + (h ? nb : na) * 32 + r32;
         const int q = h ? qb : qa;
         if (pos < (uint32_t)cap)
           cand[((int64_t)(qbase + q) * S + split) * cap + pos] = make_int2(key, __float_as_int(sc[it]));
-        const int b = bin_of(x, m);
+        const int b = bin_of(x[it], m);
         if (b >= 0) atomicAdd(&hist[q * m + b], 1u);
       }
     });
-    if ((st + 1) % refresh == 0) {
-      __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "wavefront");
 #pragma unroll
-      for (int q = 0; q < C::QW; ++q) {
-        const int t2 = wave_threshold(hist + q * m, m, (uint32_t)k, nullptr);
-        if (t2 > tau[q]) {
-          tau[q] = t2;
-          thr[q] = gate_thr(t2);
+    for (int q = 0; q < C::QW; ++q) {
+      if (above[q] >= (uint32_t)k) {
+        __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "wavefront");
+        int t = tau[q];
+        uint32_t ab = above[q];
+        while (ab >= (uint32_t)k && t < m - 1) {
+          ++t;
+          ab -= hist[q * m + t];
         }
+        above[q] = ab;
+        set_tau(q, t);
       }
     }
   }
@@ -479,10 +562,10 @@ __global__ __launch_bounds__(C::NTHREADS) void k_dense(ScoreArgs a, float* out, 
 
 template <class C>
 __global__ __launch_bounds__(C::NTHREADS) void k_fused(ScoreArgs a, const RowParam* params, int S, int L, int cap,
-                                                       int m, int k, int refresh, uint32_t* cnt,
+                                                       int m, int k, uint32_t* cnt,
                                                        uint32_t* hist_out, int2* cand) {
   extern __shared__ __align__(16) uint8_t lds[];
-  uint32_t* hist = reinterpret_cast<uint32_t*>(lds + 2 * C::TILE_BYTES);
+  uint32_t* hist = reinterpret_cast<uint32_t*>(lds + 3 * C::TILE_BYTES);
   int* emax = reinterpret_cast<int*>(hist + C::QT * m);
   const int tile = blockIdx.x / S, split = blockIdx.x - tile * S;
   const int q0 = tile * C::QT, wave = threadIdx.x / kWave, qbase = q0 + wave * C::QW;
@@ -509,7 +592,6 @@ __global__ __launch_bounds__(C::NTHREADS) void k_fused(ScoreArgs a, const RowPar
   sink.cap = cap;
   sink.m = m;
   sink.k = k;
-  sink.refresh = refresh;
   sink.init(a, params, ke);
   wg_scan<C>(a, SrcContig{}, kb, ke, lds, wq, sink);
   sink.finish(cnt, hist_out);
@@ -574,7 +656,7 @@ ScoreShape score_shape(int dtype, int mode, int h, int d) {
     s.queries_per_block = C::QT;
     s.keys_per_step = C::KT;
     s.threads = C::NTHREADS;
-    s.scan_lds = 2 * C::TILE_BYTES;
+    s.scan_lds = 3 * C::TILE_BYTES;
   });
   return s;
 }
@@ -589,7 +671,7 @@ hipError_t launch_sample_scores(const ScoreArgs& a, int ns, uint64_t seed, float
       err = hipSuccess;
       return;
     }
-    hipLaunchKernelGGL(k_sample<C>, grid, dim3(C::NTHREADS), 2 * C::TILE_BYTES, st, a, ns, seed, samp, kSlice);
+    hipLaunchKernelGGL(k_sample<C>, grid, dim3(C::NTHREADS), 3 * C::TILE_BYTES, st, a, ns, seed, samp, kSlice);
     err = hipGetLastError();
   });
   return err;
@@ -603,14 +685,14 @@ hipError_t launch_dense_scores(const ScoreArgs& a, float* out, int64_t ld, hipSt
       err = hipSuccess;
       return;
     }
-    hipLaunchKernelGGL(k_dense<C>, grid, dim3(C::NTHREADS), 2 * C::TILE_BYTES, st, a, out, ld, kSlice);
+    hipLaunchKernelGGL(k_dense<C>, grid, dim3(C::NTHREADS), 3 * C::TILE_BYTES, st, a, out, ld, kSlice);
     err = hipGetLastError();
   });
   return err;
 }
 
 hipError_t launch_fused_scan(const ScoreArgs& a, const RowParam* params, int S, int L, int cap, int m, int k,
-                             int refresh, uint32_t* cnt, uint32_t* hist, int2* cand, hipStream_t st) {
+                             uint32_t* cnt, uint32_t* hist, int2* cand, hipStream_t st) {
   hipError_t err = hipErrorInvalidValue;
   with_cfg(a.dtype, a.mode, a.h, a.d, [&]<class C>() {
     const int tiles = (a.nq + C::QT - 1) / C::QT;
@@ -618,11 +700,11 @@ hipError_t launch_fused_scan(const ScoreArgs& a, const RowParam* params, int S, 
       err = hipSuccess;
       return;
     }
-    const size_t lds = 2 * C::TILE_BYTES + (size_t)C::QT * m * 4 + 16;
+    const size_t lds = 3 * C::TILE_BYTES + (size_t)C::QT * m * 4 + 16;
     if (lds > 65536)
       (void)hipFuncSetAttribute((const void*)k_fused<C>, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
     hipLaunchKernelGGL(k_fused<C>, dim3(tiles * S), dim3(C::NTHREADS), lds, st, a, params, S, L, cap, m, k,
-                       refresh, cnt, hist, cand);
+                       cnt, hist, cand);
     err = hipGetLastError();
   });
   return err;
@@ -633,7 +715,7 @@ hipError_t launch_fused_fallback(const ScoreArgs& a, int k, uint32_t flags, cons
                                  hipStream_t st) {
   hipError_t err = hipErrorInvalidValue;
   with_cfg(a.dtype, a.mode, a.h, a.d, [&]<class C>() {
-    size_t lds = 2 * C::TILE_BYTES;
+    size_t lds = 3 * C::TILE_BYTES;
     const size_t rl = radix_lds_bytes(k);
     if (rl > lds) lds = rl;
     if (lds > 65536)

@@ -76,16 +76,17 @@ __global__ __launch_bounds__(256) void k_range(const float* src, int64_t stride,
 // wave owns one (row, key split): it streams its scores once, gates them with
 // the row's current threshold bin, appends the passing ones (ballot + mbcnt
 // compaction, one write per passing key, key order preserved) to its own
-// candidate list, counts them in its own LDS histogram, and refreshes the
-// threshold from that histogram every `refresh` chunks of 256 keys. A list
-// that reaches `cap` stops storing but keeps counting, so the final select can
-// detect the overflow.
+// candidate list and counts them in its own LDS histogram. The threshold is
+// kept current after every chunk of 256 keys with the running count of
+// candidates above it (see FusedSink in score.hip). A list that reaches `cap`
+// stops storing but keeps counting, so the final select can detect the
+// overflow.
 // ---------------------------------------------------------------------------
 constexpr int kFilterWaves = 4;
 
 __global__ __launch_bounds__(kFilterWaves * kWave) void k_filter(
     const float* scores, int64_t stride, int nq, int nk, const int32_t* offs, const RowParam* params,
-    int S, int L, int cap, int m, int k, int refresh, uint32_t* cnt, uint32_t* hist_out, int2* cand) {
+    int S, int L, int cap, int m, int k, uint32_t* cnt, uint32_t* hist_out, int2* cand) {
   __shared__ uint32_t hist_all[kFilterWaves][kMaxBins];
   const int wave = threadIdx.x / kWave, l = lane_id();
   const int unit = blockIdx.x * kFilterWaves + wave;
@@ -99,14 +100,15 @@ __global__ __launch_bounds__(kFilterWaves * kWave) void k_filter(
   const RowParam p = params[row];
   int tau = p.tau0;
   float thr = gate_thr(tau);
+  float thr_up = tau < m - 1 ? (float)(tau + 1) : __builtin_nanf("");
+  uint32_t above = 0;
   for (int b = l; b < kMaxBins; b += kWave) hist[b] = 0u;
   __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "wavefront");
 
   const float* rp = scores + (int64_t)row * stride;
   int2* out = cand + (int64_t)unit * cap;
   uint32_t tail = 0;
-  int it = 0;
-  for (int base = lo; base < hi; base += 4 * kWave, ++it) {
+  for (int base = lo; base < hi; base += 4 * kWave) {
     const int i0 = base + 4 * l;
     float v[4];
     if (i0 + 3 < hi) {
@@ -118,7 +120,7 @@ __global__ __launch_bounds__(kFilterWaves * kWave) void k_filter(
     }
     float x[4];
     bool ps[4];
-    uint32_t below = 0, total = 0;
+    uint32_t below = 0, total = 0, up = 0;
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
       x[j] = bin_x(v[j], p.delta, p.c);
@@ -126,7 +128,9 @@ __global__ __launch_bounds__(kFilterWaves * kWave) void k_filter(
       uint64_t mask = __ballot(ps[j]);
       below += mbcnt64(mask);
       total += (uint32_t)__popcll(mask);
+      up += (uint32_t)__popcll(__ballot(ps[j] && x[j] >= thr_up));
     }
+    if (total == 0) continue;  // wave-uniform
     uint32_t pos = tail + below;
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
@@ -138,13 +142,15 @@ __global__ __launch_bounds__(kFilterWaves * kWave) void k_filter(
       }
     }
     tail += total;
-    if ((it + 1) % refresh == 0) {
+    above += up;
+    if (above >= (uint32_t)k) {
       __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "wavefront");
-      int t2 = wave_threshold(hist, m, (uint32_t)k, nullptr);
-      if (t2 > tau) {
-        tau = t2;
-        thr = gate_thr(tau);
+      while (above >= (uint32_t)k && tau < m - 1) {
+        ++tau;
+        above -= hist[tau];
       }
+      thr = gate_thr(tau);
+      thr_up = tau < m - 1 ? (float)(tau + 1) : __builtin_nanf("");
     }
   }
   __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "wavefront");
@@ -354,12 +360,12 @@ hipError_t launch_range(bool from_scores, const float* src, int64_t stride, int 
 }
 
 hipError_t launch_filter(const float* scores, int64_t stride, int nq, int nk, const int32_t* offs,
-                         const RowParam* params, int S, int L, int cap, int m, int k, int refresh,
-                         uint32_t* cnt, uint32_t* hist, int2* cand, hipStream_t st) {
+                         const RowParam* params, int S, int L, int cap, int m, int k, uint32_t* cnt,
+                         uint32_t* hist, int2* cand, hipStream_t st) {
   const int units = nq * S;
   dim3 grid((units + kFilterWaves - 1) / kFilterWaves);
   hipLaunchKernelGGL(k_filter, grid, dim3(kFilterWaves * kWave), 0, st, scores, stride, nq, nk, offs,
-                     params, S, L, cap, m, k, refresh, cnt, hist, cand);
+                     params, S, L, cap, m, k, cnt, hist, cand);
   return hipGetLastError();
 }
 

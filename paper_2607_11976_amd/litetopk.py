@@ -44,7 +44,6 @@ class LtOptions(ctypes.Structure):
         ("sample_size", ctypes.c_int32),
         ("capacity", ctypes.c_int32),
         ("key_splits", ctypes.c_int32),
-        ("refresh_tiles", ctypes.c_int32),
         ("flags", ctypes.c_uint32),
         ("seed", ctypes.c_uint64),
         ("stage_events", ctypes.c_void_p),
@@ -187,7 +186,7 @@ def _on_gpu(*ts):
             _need(t.is_contiguous(), "tensors must be contiguous")
 
 
-def make_options(num_bins=None, sample_size=None, capacity=None, key_splits=None, refresh_tiles=None,
+def make_options(num_bins=None, sample_size=None, capacity=None, key_splits=None,
                  sorted_output=False, force_fallback=False, seed=None, stage_events=None,
                  row_stats: Optional[torch.Tensor] = None) -> LtOptions:
     o = lt_options_default()
@@ -199,8 +198,6 @@ def make_options(num_bins=None, sample_size=None, capacity=None, key_splits=None
         o.capacity = capacity
     if key_splits is not None:
         o.key_splits = key_splits
-    if refresh_tiles is not None:
-        o.refresh_tiles = refresh_tiles
     o.flags = (LT_SORTED_OUTPUT if sorted_output else 0) | (LT_FORCE_FALLBACK if force_fallback else 0)
     if seed is not None:
         o.seed = seed

@@ -96,7 +96,7 @@ def test_fused_equals_select_over_dense_scores(lib, base):
     dict(num_bins=1),
     dict(sample_size=0),
     dict(key_splits=4),
-    dict(refresh_tiles=1, num_bins=16),
+    dict(num_bins=16, capacity=3000),
 ], ids=lambda o: ",".join(f"{a}={b}" for a, b in o.items()))
 def test_fused_forced_paths_are_exact(lib, opt):
     cfg = workloads.scaled(workloads.CONFIGS["dsa_bf16_128k"], nq=10, nk=9000)

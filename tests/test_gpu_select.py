@@ -85,7 +85,7 @@ def test_select_parity(lib, entry, sorted_out, case):
     dict(sample_size=0),
     dict(num_bins=3, capacity=50),
     dict(key_splits=3),
-    dict(refresh_tiles=1),
+    dict(num_bins=7),
 ], ids=lambda d: ",".join(f"{k}={v}" for k, v in d.items()))
 def test_select_forced_paths_are_still_exact(lib, opt):
     nq, nk, k = 12, 9000, 300
