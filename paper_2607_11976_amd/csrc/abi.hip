@@ -16,6 +16,7 @@ constexpr int kFallbackGridFused = 64;      // rows re-scored concurrently (scra
 constexpr int kFallbackGridScores = 256;
 constexpr int kTargetBlocks = 256;          // one block per CU before key splitting stops
 constexpr size_t kHistLdsBudget = 96 * 1024;
+constexpr size_t kLdsPerBlock = 160 * 1024;   // gfx950 LDS per workgroup
 constexpr int kSampleBlockScores = 64;      // scores-in sample: runs of 64 consecutive keys
 
 inline size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
@@ -77,7 +78,9 @@ Resolved resolve_fused(const lt_options* o, int nq, int nk, int k, int mode, con
   lt_options d;
   lt_options_default(&d);
   if (!o) o = &d;
-  const size_t mcap = kHistLdsBudget / (4 * (size_t)sh.queries_per_block);
+  // per-row LDS histograms share the block's LDS with the key-tile ring
+  const size_t room = kLdsPerBlock - sh.scan_lds - 64;
+  const size_t mcap = std::min(kHistLdsBudget, room) / (4 * (size_t)sh.queries_per_block);
   if ((size_t)r.m > mcap) r.m = (int)std::max<size_t>(mcap, 1);
   int ns = o->sample_size;
   if (ns < 0) {

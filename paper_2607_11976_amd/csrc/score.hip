@@ -71,11 +71,12 @@ template <>
 struct Mfma<DT_FP8> {
   static constexpr int KI = 64, ES = 1, FB = 32;
   using Frag = i32x8_t;
-  __device__ static Frag load(const uint8_t* p) {
-    i32x4_t lo = *reinterpret_cast<const i32x4_t*>(p);
-    i32x4_t hi = *reinterpret_cast<const i32x4_t*>(p + 16);
+  __device__ static Frag load2(const uint8_t* p0, const uint8_t* p1) {
+    i32x4_t lo = *reinterpret_cast<const i32x4_t*>(p0);
+    i32x4_t hi = *reinterpret_cast<const i32x4_t*>(p1);
     return i32x8_t{lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
   }
+  __device__ static Frag load(const uint8_t* p) { return load2(p, p + 16); }
   __device__ static Frag zero() { return i32x8_t{0, 0, 0, 0, 0, 0, 0, 0}; }
   // OCP E4M3 for both operands (format code 0), unit block scales (E8M0 127).
   __device__ static f32x16_t mma(Frag a, Frag b, f32x16_t c) {
@@ -96,20 +97,25 @@ struct Cfg {
   static constexpr int KT = 32 * NT;                   // keys per tile
   static constexpr int QT = WAVES * QW;                // queries per block
   static constexpr int ROWB = D * M::ES;               // bytes per key row
-  static constexpr int LSTRIDE = ROWB + 16;            // padded LDS row (bank spread)
-  static constexpr int TILE_BYTES = KT * LSTRIDE;
+  static constexpr int TILE_BYTES = KT * ROWB;         // LDS tile: rows of 16-B chunks, XOR-swizzled
+  static constexpr int RING = 4;                       // LDS tiles in flight
   static constexpr int CPK = ROWB / 16;                // 16-byte chunks per key
   static constexpr int CHUNKS = KT * CPK;
   static constexpr int NTHREADS = WAVES * kWave;
-  static constexpr int CPT = (CHUNKS + NTHREADS - 1) / NTHREADS;
+  static constexpr int CPT = CHUNKS / NTHREADS;      // staged chunks per thread per tile
   // GROUPED: H <= 4, a 4-row accumulator group holds whole queries, no
   // cross-lane step. Otherwise H % 8 == 0 and the halves are combined.
   static constexpr bool GROUPED = H <= 4;
   static constexpr int GPQ = GROUPED ? 4 / H : 1;      // queries per 4-row group
   static constexpr int NI = GROUPED ? NT * MT * 4 * GPQ : NT * QW / 2;  // scores per lane per tile
   static constexpr int NIH = GROUPED ? MT * 4 * GPQ : QW;              // per-lane results of one sub-tile
+  // epilogue VALU ops of one sub-tile (ReLU + FMA per accumulator element)
+  // spread over the MFMAs of the other sub-tile
+  static constexpr int VALU_PER_MFMA = (2 * 16 * MT + KS * MT - 1) / (KS * MT);
   static_assert((QW * H) % 32 == 0, "a wave must fill whole M tiles");
   static_assert(NT == 2, "the scan pipelines the two 32-key halves of a tile");
+  static_assert(CHUNKS % NTHREADS == 0 && CPT < 16, "tile staging assumes whole instructions per thread");
+  static_assert((CPK & (CPK - 1)) == 0, "chunks per key row must be a power of two");
   static_assert(D % M::KI == 0, "head dim must be a multiple of the MFMA K");
   static_assert(ROWB % 16 == 0, "key rows must be a multiple of 16 bytes");
   static_assert(GROUPED ? (4 % H == 0) : (H % 8 == 0 && (NT * QW) % 2 == 0), "unsupported head layout");
@@ -174,13 +180,29 @@ __device__ __forceinline__ void load_q(WaveQ<C>& s, const ScoreArgs& a, int qbas
 // One half step: q . k for every row of the wave against one 32-key sub-tile.
 // acc[mt] is the 32x32 block of M tile mt; accumulator register v of a lane
 // is row 8*(v/4) + 4*(lane/32) + v%4 of the M tile, column lane%32.
+// LDS tile layout: key row n occupies ROWB contiguous bytes; its 16-byte
+// chunk c is stored at chunk slot c ^ (n mod CPK). The swizzle spreads the
+// 32 lanes that read the same chunk of 32 consecutive keys over distinct
+// banks without padding, so tiles can be filled by direct HBM -> LDS loads.
+template <class C>
+__device__ __forceinline__ int lds_offset(int n, int byte) {
+  return n * C::ROWB + ((((byte >> 4) ^ n) & (C::CPK - 1)) << 4) + (byte & 15);
+}
+
 template <class C>
 __device__ __forceinline__ void load_b(const uint8_t* tile, int nt, typename C::M::Frag (&b)[C::KS]) {
   using M = typename C::M;
   const int l = lane_id(), h = l >> 5, r32 = l & 31;
-  const uint8_t* base = tile + (nt * 32 + r32) * C::LSTRIDE + h * M::FB;
+  const int n = nt * 32 + r32;
 #pragma unroll
-  for (int ks = 0; ks < C::KS; ++ks) b[ks] = M::load(base + ks * M::KI * M::ES);
+  for (int ks = 0; ks < C::KS; ++ks) {
+    const int byte = ks * M::KI * M::ES + h * M::FB;
+    if constexpr (M::FB <= 16) {
+      b[ks] = M::load(tile + lds_offset<C>(n, byte));
+    } else {
+      b[ks] = M::load2(tile + lds_offset<C>(n, byte), tile + lds_offset<C>(n, byte + 16));
+    }
+  }
 }
 
 template <class C>
@@ -257,9 +279,31 @@ __device__ __forceinline__ void combine(const float (&h0)[C::NIH], const float (
   } else {
 #pragma unroll
     for (int it = 0; it < C::NI; ++it) {
-      const float recv = __shfl_xor(h ? h0[it] : h1[it], 32, kWave);
-      sc[it] = (h ? h1[it] : h0[it]) + recv;
+      // v_permlane32_swap(x, y) exchanges x's upper 32 lanes with y's lower
+      // 32 lanes: lanes 0-31 receive h0 of lane + 32 in y, lanes 32-63
+      // receive h1 of lane - 32 in x.
+      const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(h0[it]), __float_as_uint(h1[it]), false, false);
+      sc[it] = h ? h1[it] + __uint_as_float(r[0]) : h0[it] + __uint_as_float(r[1]);
     }
+  }
+}
+
+// Instruction pattern of one half step: per K slice, MFMA / 4 VALU / MFMA /
+// 4 VALU / one LDS read of the next sub-tile's B fragment (issued as soon as
+// the slice's fragment register is free), so the matrix pipe always has an
+// MFMA queued and the epilogue of the other sub-tile runs in its shadow.
+template <class C>
+__device__ __forceinline__ void schedule_half() {
+  constexpr int kMfma = 0x008, kValu = 0x002, kDsRead = 0x100;
+  constexpr int kReadsPerSlice = C::M::FB / 16 > 0 ? C::M::FB / 16 : 1;
+#pragma unroll
+  for (int ks = 0; ks < C::KS; ++ks) {
+#pragma unroll
+    for (int mt = 0; mt < C::MT; ++mt) {
+      __builtin_amdgcn_sched_group_barrier(kMfma, 1, 0);
+      __builtin_amdgcn_sched_group_barrier(kValu, C::VALU_PER_MFMA, 0);
+    }
+    __builtin_amdgcn_sched_group_barrier(kDsRead, kReadsPerSlice, 0);
   }
 }
 
@@ -287,29 +331,33 @@ __device__ __forceinline__ void wg_scan(const ScoreArgs& a, const Src& src, int 
   const uint8_t* keys = static_cast<const uint8_t*>(a.keys);
   const int nsteps = kend > kbeg ? (kend - kbeg + C::KT - 1) / C::KT : 0;
   if (nsteps == 0) return;
-  i32x4_t regs[C::CPT];
-  // Rows past kend are clamped to the last valid row: their scores are never
-  // used (every consumer masks positions >= kend), so no branch is needed.
-  auto gload = [&](int k0) {
+  // Key tiles go straight from HBM to LDS (global_load_lds_dwordx4): each
+  // instruction of a wave fills 64 consecutive 16-byte chunk slots. Rows past
+  // kend are clamped to the last valid row: their scores are never used
+  // (every consumer masks positions >= kend).
+  const int wave = tid / kWave;
+  auto stage = [&](int slot, int k0) {
 #pragma unroll
     for (int c = 0; c < C::CPT; ++c) {
-      const int ch = tid + c * C::NTHREADS;
-      if (C::CHUNKS % C::NTHREADS == 0 || ch < C::CHUNKS) {
-        const int kk = ch / C::CPK, part = ch - kk * C::CPK;
-        const int i = min(k0 + kk, kend - 1);
-        regs[c] = *reinterpret_cast<const i32x4_t*>(keys + (int64_t)src.key(i) * C::ROWB + part * 16);
-      }
+      const int u0 = (c * C::WAVES + wave) * kWave;  // first chunk slot of this instruction
+      const int u = u0 + l, n = u / C::CPK, part = (u ^ n) & (C::CPK - 1);
+      const int i = min(k0 + n, kend - 1);
+      const uint8_t* g = keys + (int64_t)src.key(i) * C::ROWB + part * 16;
+      uint8_t* d = tiles + slot * C::TILE_BYTES + u0 * 16;
+      __builtin_amdgcn_global_load_lds((const void __attribute__((address_space(1)))*)g,
+                                       (void __attribute__((address_space(3)))*)d, 16, 0, 0);
     }
   };
-  auto sstore = [&](int buf) {
-#pragma unroll
-    for (int c = 0; c < C::CPT; ++c) {
-      const int ch = tid + c * C::NTHREADS;
-      if (ch < C::CHUNKS) {
-        const int kk = ch / C::CPK, part = ch - kk * C::CPK;
-        *reinterpret_cast<i32x4_t*>(tiles + buf * C::TILE_BYTES + kk * C::LSTRIDE + part * 16) = regs[c];
-      }
-    }
+  // Wait until at most `n` of this wave's vector-memory operations are in
+  // flight (loads complete in issue order), then a plain barrier: the tile
+  // whose loads are done is visible to every wave. No release fence -- it
+  // would wait for every outstanding load, including the prefetches.
+  auto sync_tiles = [&](int n) {
+    asm volatile("" ::: "memory");
+    if (n == 0) __builtin_amdgcn_s_waitcnt(0x0F70);
+    else __builtin_amdgcn_s_waitcnt(0x0F70 | C::CPT);
+    __builtin_amdgcn_s_barrier();
+    asm volatile("" ::: "memory");
   };
   // both sub-tiles' results of tile st -> complete scores (fp8: key scales)
   auto scores = [&](int st, const float (&h0)[C::NIH], const float (&h1)[C::NIH], float (&sc)[C::NI]) {
@@ -326,11 +374,10 @@ __device__ __forceinline__ void wg_scan(const ScoreArgs& a, const Src& src, int 
     }
   };
 
-  gload(kbeg);
-  sstore(0);
-  gload(kbeg + C::KT);
-  sstore(1);
-  __syncthreads();
+  stage(0, kbeg);
+  stage(1, kbeg + C::KT);
+  stage(2, kbeg + 2 * C::KT);
+  sync_tiles(1);  // tiles 0 and 1 landed (tile 2 may still be in flight)
   Frag b0[C::KS], b1[C::KS];
   f32x16_t acc0[C::MT], acc1[C::MT];
 #pragma unroll
@@ -339,31 +386,38 @@ __device__ __forceinline__ void wg_scan(const ScoreArgs& a, const Src& src, int 
 #pragma unroll
   for (int j = 0; j < C::NIH; ++j) h0[j] = 0.0f;
   load_b<C>(tiles, 0, b0);
-  int cur = 0;  // ring slot of tile st
   for (int st = 0; st < nsteps; ++st) {
-    const uint8_t* tl = tiles + cur * C::TILE_BYTES;
-    const int nxt = cur == 2 ? 0 : cur + 1, fill = nxt == 2 ? 0 : nxt + 1;
-    gload(kbeg + (st + 2) * C::KT);
-    // half step A: MFMA sub-tile 0 of tile st || epilogue of sub-tile 1 of st-1
-    load_b<C>(tl, 1, b1);
+    const uint8_t* tl = tiles + (st & (C::RING - 1)) * C::TILE_BYTES;
+    const uint8_t* tn = tiles + ((st + 1) & (C::RING - 1)) * C::TILE_BYTES;
+    // slot of tile st-1 is free: every wave passed the barrier after reading it
+    stage((st + 3) & (C::RING - 1), kbeg + (st + 3) * C::KT);
+    // half step A: MFMA sub-tile 0 of tile st || epilogue of sub-tile 1 of st-1,
+    // B fragments of sub-tile 1 read as the slots free up
     mma_half<C>(wq, b0, acc0);
+    load_b<C>(tl, 1, b1);
     reduce_half<C>(wq, acc1, h1);
     float sc[C::NI];
     scores(st - 1, h0, h1, sc);
-    // half step B: MFMA sub-tile 1 of tile st || epilogue of sub-tile 0 of st
-    load_b<C>(tiles + nxt * C::TILE_BYTES, 0, b0);
+    schedule_half<C>();
+    // half step B: MFMA sub-tile 1 of tile st || epilogue of sub-tile 0 of st,
+    // B fragments of the next tile's sub-tile 0 read as the slots free up
     mma_half<C>(wq, b1, acc1);
+    load_b<C>(tn, 0, b0);
     reduce_half<C>(wq, acc0, h0);
+    schedule_half<C>();
+    // h0 is only read in the next step; without this use the compiler sinks
+    // its epilogue below the gate's branches, out of the MFMA shadow
+#pragma unroll
+    for (int j = 0; j < C::NIH; ++j) asm volatile("" ::"v"(h0[j]));
     // gate + write-back of tile st-1 while the last MFMAs drain
     sink.consume(st - 1, kbeg + (st - 1) * C::KT, kend, sc, st > 0);
-    sstore(fill);
-    __syncthreads();
-    cur = nxt;
+    sync_tiles(1);  // tile st+2 landed; tile st+3 may still be in flight
   }
   reduce_half<C>(wq, acc1, h1);
   float sc[C::NI];
   scores(nsteps - 1, h0, h1, sc);
   sink.consume(nsteps - 1, kbeg + (nsteps - 1) * C::KT, kend, sc, true);
+  sync_tiles(0);  // no prefetch may still be writing LDS when the caller reuses it
 }
 
 // ---------------------------------------------------------------------------
@@ -565,7 +619,7 @@ __global__ __launch_bounds__(C::NTHREADS) void k_fused(ScoreArgs a, const RowPar
                                                        int m, int k, uint32_t* cnt,
                                                        uint32_t* hist_out, int2* cand) {
   extern __shared__ __align__(16) uint8_t lds[];
-  uint32_t* hist = reinterpret_cast<uint32_t*>(lds + 3 * C::TILE_BYTES);
+  uint32_t* hist = reinterpret_cast<uint32_t*>(lds + C::RING * C::TILE_BYTES);
   int* emax = reinterpret_cast<int*>(hist + C::QT * m);
   const int tile = blockIdx.x / S, split = blockIdx.x - tile * S;
   const int q0 = tile * C::QT, wave = threadIdx.x / kWave, qbase = q0 + wave * C::QW;
@@ -656,7 +710,7 @@ ScoreShape score_shape(int dtype, int mode, int h, int d) {
     s.queries_per_block = C::QT;
     s.keys_per_step = C::KT;
     s.threads = C::NTHREADS;
-    s.scan_lds = 3 * C::TILE_BYTES;
+    s.scan_lds = C::RING * C::TILE_BYTES;
   });
   return s;
 }
@@ -671,7 +725,7 @@ hipError_t launch_sample_scores(const ScoreArgs& a, int ns, uint64_t seed, float
       err = hipSuccess;
       return;
     }
-    hipLaunchKernelGGL(k_sample<C>, grid, dim3(C::NTHREADS), 3 * C::TILE_BYTES, st, a, ns, seed, samp, kSlice);
+    hipLaunchKernelGGL(k_sample<C>, grid, dim3(C::NTHREADS), C::RING * C::TILE_BYTES, st, a, ns, seed, samp, kSlice);
     err = hipGetLastError();
   });
   return err;
@@ -685,7 +739,7 @@ hipError_t launch_dense_scores(const ScoreArgs& a, float* out, int64_t ld, hipSt
       err = hipSuccess;
       return;
     }
-    hipLaunchKernelGGL(k_dense<C>, grid, dim3(C::NTHREADS), 3 * C::TILE_BYTES, st, a, out, ld, kSlice);
+    hipLaunchKernelGGL(k_dense<C>, grid, dim3(C::NTHREADS), C::RING * C::TILE_BYTES, st, a, out, ld, kSlice);
     err = hipGetLastError();
   });
   return err;
@@ -700,7 +754,7 @@ hipError_t launch_fused_scan(const ScoreArgs& a, const RowParam* params, int S, 
       err = hipSuccess;
       return;
     }
-    const size_t lds = 3 * C::TILE_BYTES + (size_t)C::QT * m * 4 + 16;
+    const size_t lds = C::RING * C::TILE_BYTES + (size_t)C::QT * m * 4 + 16;
     if (lds > 65536)
       (void)hipFuncSetAttribute((const void*)k_fused<C>, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
     hipLaunchKernelGGL(k_fused<C>, dim3(tiles * S), dim3(C::NTHREADS), lds, st, a, params, S, L, cap, m, k,
@@ -715,7 +769,7 @@ hipError_t launch_fused_fallback(const ScoreArgs& a, int k, uint32_t flags, cons
                                  hipStream_t st) {
   hipError_t err = hipErrorInvalidValue;
   with_cfg(a.dtype, a.mode, a.h, a.d, [&]<class C>() {
-    size_t lds = 3 * C::TILE_BYTES;
+    size_t lds = C::RING * C::TILE_BYTES;
     const size_t rl = radix_lds_bytes(k);
     if (rl > lds) lds = rl;
     if (lds > 65536)
