@@ -1,0 +1,105 @@
+"""Parity at the full workload sizes, in the launch configuration the
+benchmark times (default options):
+
+* every row: the fused result equals plain radix selection (lt_topk_radix,
+  no sampling or filtering) over the dense score matrix (lt_indexer_scores,
+  the same score arithmetic), bit for bit after sorting both by the total
+  order; every row holds exactly min(k, e_t) distinct visible indices; no row
+  needed the fallback for an internal inconsistency;
+* an evenly spaced sample of rows (first and last included): the fused result
+  against the CPU oracle, within the fp32/bf16 (1e-3) or fp8 (2e-2) tolerance
+  and the swap rule.
+"""
+import numpy as np
+import pytest
+import torch
+
+from paper_2607_11976_amd import litetopk as lt
+from paper_2607_11976_amd import workloads
+from helpers import oracle_topk, to_dev
+from parity import RTOL, check_row_tol, visible
+
+pytestmark = [pytest.mark.gpu, pytest.mark.slow]
+
+FULL = ["tiny_fp32", "dsa_bf16_128k", "dsa_fp8_1m", "adversarial_bf16_256k"]
+
+
+def _sorted_pairs(idx, sc):
+    """Sort every row by the total order (score desc, NaN last, -0 == +0,
+    index asc; padding last), on the host."""
+    idx, sc = idx.cpu().numpy(), sc.cpu().numpy()
+    nq, k = idx.shape
+    row = np.repeat(np.arange(nq), k)
+    i = idx.ravel().astype(np.int64)
+    s = sc.ravel().astype(np.float64)
+    nan = np.isnan(s) | (i < 0)
+    key = np.where(nan, 0.0, -s) + 0.0
+    o = np.lexsort((np.where(i < 0, 1 << 40, i), key, nan, row))
+    return idx.ravel()[o].reshape(nq, k), sc.ravel()[o].reshape(nq, k)
+
+
+@pytest.mark.parametrize("name", FULL)
+def test_full_size_parity(lib, name):
+    cfg = workloads.CONFIGS[name]
+    x = workloads.generate(cfg, seed=workloads.CONFIG_SEEDS[name])
+    d = to_dev(x)
+    nq, nk, k = cfg.nq, cfg.nk, cfg.k
+    stats = torch.zeros((nq, 4), dtype=torch.int32, device="cuda")
+    fi, fs = lt.indexer_topk(d["q"], d["w"], d["keys"], k, d["offsets"], d["q_scale"], d["k_scale"],
+                             mode=cfg.mode, options=lt.make_options(row_stats=stats))
+    dense = lt.indexer_scores(d["q"], d["w"], d["keys"], d["q_scale"], d["k_scale"], mode=cfg.mode)
+    ri, rs = lt.topk_radix(dense, k, causal_offsets=d["offsets"], sorted_output=True)
+    del dense
+    torch.cuda.synchronize()
+    gi, gs = _sorted_pairs(fi, fs)
+    np.testing.assert_array_equal(gi, ri.cpu().numpy(), err_msg="fused sets differ from radix over dense scores")
+    np.testing.assert_array_equal(gs.view(np.uint32), rs.cpu().numpy().view(np.uint32),
+                                  err_msg="fused scores differ from dense scores")
+    e = visible(None if x["offsets"] is None else x["offsets"].numpy(), nq, nk)
+    valid = gi >= 0
+    np.testing.assert_array_equal(valid.sum(1), np.minimum(e, k), err_msg="wrong number of entries")
+    assert np.all((gi < e[:, None]) | ~valid), "index outside the visible range"
+    for t in range(nq):
+        v = gi[t][valid[t]]
+        assert np.unique(v).size == v.size, "duplicate index in row %d" % t
+    st = stats.cpu().numpy()
+    assert not np.any(st[:, 2] == 4)
+    # sampled rows against the CPU oracle
+    rows = sorted(set(np.linspace(0, nq - 1, 8).round().astype(int).tolist()))
+    oi, os_, full = oracle_topk(x, cfg.dtype, k, cfg.mode, rows=rows)
+    fi_h, fs_h = fi.cpu().numpy(), fs.cpu().numpy()
+    ev = visible(None if x["offsets"] is None else x["offsets"].numpy(), nq, nk)
+    for j, t in enumerate(rows):
+        check_row_tol(fi_h[t], fs_h[t], oi[j], os_[j], full[j], int(ev[t]), k, RTOL[cfg.dtype])
+
+
+def test_full_size_retrieval(lib):
+    """10000 queries x 4M items, inner product, k = 100. The dense check runs
+    on three 512-row blocks (first, middle, last query tiles): the full dense
+    matrix would take 160 GB."""
+    name = "retrieval_bf16_4m"
+    cfg = workloads.CONFIGS[name]
+    x = workloads.generate(cfg, seed=workloads.CONFIG_SEEDS[name])
+    d = to_dev(x)
+    nq, nk, k = cfg.nq, cfg.nk, cfg.k
+    stats = torch.zeros((nq, 4), dtype=torch.int32, device="cuda")
+    fi, fs = lt.indexer_topk(d["q"], None, d["keys"], k, None, mode="ip", options=lt.make_options(row_stats=stats))
+    torch.cuda.synchronize()
+    gi, gs = _sorted_pairs(fi, fs)
+    assert np.all(gi >= 0) and np.all(gi < nk)
+    for t in range(nq):
+        assert np.unique(gi[t]).size == k, "duplicate index in row %d" % t
+    assert not np.any(stats.cpu().numpy()[:, 2] == 4)
+    for r0 in (0, nq // 2 - 256, nq - 512):
+        qb = d["q"][r0:r0 + 512].contiguous()
+        dense = lt.indexer_scores(qb, None, d["keys"], mode="ip")
+        ri, rs = lt.topk_radix(dense, k, sorted_output=True)
+        del dense
+        torch.cuda.synchronize()
+        np.testing.assert_array_equal(gi[r0:r0 + 512], ri.cpu().numpy())
+        np.testing.assert_array_equal(gs[r0:r0 + 512].view(np.uint32), rs.cpu().numpy().view(np.uint32))
+    rows = sorted(set(np.linspace(0, nq - 1, 8).round().astype(int).tolist()))
+    oi, os_, full = oracle_topk(x, cfg.dtype, k, cfg.mode, rows=rows)
+    fi_h, fs_h = fi.cpu().numpy(), fs.cpu().numpy()
+    for j, t in enumerate(rows):
+        check_row_tol(fi_h[t], fs_h[t], oi[j], os_[j], full[j], nk, k, RTOL[cfg.dtype])
