@@ -13,7 +13,11 @@ fallback, inputs resident in HBM. Prints ONE JSON line with
                  around it on the library's stream over the timed steps;
   cpu_baseline   the CPU oracle timed on an evenly spaced sample of rows;
   unfused        the materialising baseline (dense scores + radix select);
-  ctx_1m         the same measurement for the 2048 x 1M fp8 workload.
+  ctx_1m         the same measurement for the 2048 x 1M fp8 workload;
+  chunked_prefill  the same 4096 queries processed in chunks (sec. 4.2's
+                 chunked-prefill protocol), with a random sample per chunk and
+                 with the sample taken from the previous chunk's top-k
+                 (sec. 3.2 "Sampling"), total time over all chunks.
 """
 from __future__ import annotations
 
@@ -124,6 +128,59 @@ def measure(name: str, steps: int, warmup: int, unfused: bool):
     return cfg, res
 
 
+def chunked_prefill(name: str, chunk: int, reps: int):
+    """All queries of `name` in chunks of `chunk` rows over the same keys;
+    'random' samples every chunk at random, 'previous' takes each chunk's
+    sample from the previous chunk's output (lt_sample_from_topk, included in
+    the time). Returns total milliseconds over the chunks (mean of reps) and
+    mean survivors per row."""
+    cfg = workloads.CONFIGS[name]
+    x = workloads.generate(cfg, seed=workloads.CONFIG_SEEDS[name])
+    dev = torch.device("cuda")
+    d = {kk: (None if v is None else v.to(dev)) for kk, v in x.items()
+         if kk in ("q", "w", "keys", "q_scale", "k_scale", "offsets")}
+    del x
+    nq, nk, k = cfg.nq, cfg.nk, cfg.k
+    ns = 3 * k
+    starts = list(range(0, nq, chunk))
+    parts = [{kk: (None if d[kk] is None else d[kk][c0:c0 + chunk].contiguous())
+              for kk in ("q", "w", "q_scale", "offsets")} for c0 in starts]
+    outs = [(torch.empty((p["q"].shape[0], k), dtype=torch.int32, device=dev),
+             torch.empty((p["q"].shape[0], k), dtype=torch.float32, device=dev)) for p in parts]
+    hints = [torch.empty(ns, dtype=torch.int32, device=dev) for _ in parts]
+    hws = torch.empty(lt.lt_sample_from_topk_workspace_size(nk), dtype=torch.uint8, device=dev)
+    dt = lt._dtype_code(d["q"])
+    opt_r = lt.make_options()
+    ws = lt.indexer_topk_workspace(chunk, nk, cfg.h, cfg.d, dt, cfg.mode, k, opt_r, dev)
+    opt_h = [lt.make_options(sample_keys=h) for h in hints]
+    ws_h = lt.indexer_topk_workspace(chunk, nk, cfg.h, cfg.d, dt, cfg.mode, k, opt_h[0], dev)
+
+    def run(previous, stats=None):
+        for j, p in enumerate(parts):
+            o = opt_r if (not previous or j == 0) else opt_h[j - 1]
+            if stats is not None:
+                o = lt.make_options(row_stats=stats[j], sample_keys=hints[j - 1] if (previous and j) else None)
+            lt.indexer_topk(p["q"], p["w"], d["keys"], k, p["offsets"], p["q_scale"], d["k_scale"], mode=cfg.mode,
+                            options=o, out=outs[j], workspace=ws_h if (previous and j) else ws)
+            if previous and j + 1 < len(parts):
+                lt.sample_from_topk(outs[j][0], nk, ns, out=hints[j], workspace=hws)
+
+    res = {"workload": name, "chunk": chunk, "chunks": len(parts), "sample_size": ns}
+    for mode in ("random", "previous"):
+        res[mode + "_ms"] = round(timed_steps(lambda: run(mode == "previous"), reps, 1), 4)
+        st = [torch.zeros((p["q"].shape[0], 4), dtype=torch.int32, device=dev) for p in parts]
+        run(mode == "previous", st)
+        sv = torch.cat(st).cpu().numpy()
+        res[mode + "_survivors_per_row"] = round(float(sv[:, 0].mean()), 1)
+        res[mode + "_fallback_rows"] = int((sv[:, 2] != 0).sum())
+    # the previous-chunk sampler alone
+    res["sample_from_topk_ms"] = round(timed_steps(
+        lambda: lt.sample_from_topk(outs[0][0], nk, ns, out=hints[0], workspace=hws), 5, 1), 4)
+    del d, parts, outs, ws, ws_h
+    torch.cuda.empty_cache()
+    return res
+
+
 def roofline(cfg, res):
     flops = 2.0 * cfg.h * cfg.d * res["pairs"]
     filt_ms = res["stages"]["filter"]
@@ -185,6 +242,7 @@ def main():
     ap.add_argument("--no-1m", action="store_true", help="skip the 1M-context fp8 measurement")
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
     ap.add_argument("--no-unfused", action="store_true", help="skip the unfused baseline")
+    ap.add_argument("--no-chunked", action="store_true", help="skip the chunked-prefill measurement")
     ap.add_argument("--cpu-budget", type=float, default=15.0)
     ap.add_argument("--profile-only", default=None, metavar="WORKLOAD",
                     help="run only `steps` fused calls of one workload (for rocprofv3 counter passes)")
@@ -266,6 +324,9 @@ def main():
             m["unfused_ms_per_step"] = round(res2["unfused_ms"], 4)
             m["unfused_same_sets"] = res2["unfused_same_sets"]
         line["ctx_1m"] = m
+    if not args.no_chunked:
+        line["chunked_prefill"] = [chunked_prefill("dsa_bf16_128k", c, 3) for c in (256, 1024)]
+        print("[bench] chunked prefill done", file=sys.stderr, flush=True)
     if rank0 and not args.no_cpu:
         line["cpu_baseline"] = cpu_oracle_rate("dsa_bf16_128k", args.cpu_budget)
     if rank0:

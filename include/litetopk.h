@@ -51,6 +51,7 @@ extern "C" {
 
 #define LT_K_MAX 8192         /* largest k (the paper's largest, sec. 4.1 retrieval) */
 #define LT_MAX_BINS 256
+#define LT_SAMPLE_LIST_MAX 32768  /* longest caller-supplied sample list */
 
 /* ---- enums --------------------------------------------------------------- */
 typedef enum {
@@ -88,7 +89,9 @@ typedef struct lt_options {
   int32_t sample_size;     /* k': sampled keys per launch (sec. 3.2: k' = 3k for
                               DSA); negative = default: 3k in DSA mode,
                               max(3k, min(Nk/64, 65536)) in IP mode (the scores-in
-                              entry uses 3k); 0 disables the gate                */
+                              entry uses 3k); 0 disables the gate. With
+                              sample_keys set: the length of that list,
+                              1..LT_SAMPLE_LIST_MAX                            */
   int32_t capacity;        /* candidate slots per (row, key split); <= 0 = default
                               max(12k, 2048) (sec. 4.2: 12k for k = 2048)       */
   int32_t key_splits;      /* key-range splits per row; 0 = auto (fused), 1 (scores-in) */
@@ -100,6 +103,16 @@ typedef struct lt_options {
                               final threshold bin, fallback reason (0 none,
                               1 buffer overflow, 2 threshold-bin overflow,
                               3 forced), candidates in the threshold bin}       */
+  const int32_t* sample_keys; /* NULL = a random stratified sample drawn with
+                              `seed`; else a DEVICE int32 [sample_size] list of
+                              key indices to score as the sample instead. Sec. 3.2
+                              "Sampling" reuses the keys that occur most often in
+                              the previous chunk's top-k (lt_sample_from_topk).
+                              Any list gives exact results: entries outside
+                              [0, num_keys) and repeated entries are dropped, and
+                              row t uses only the entries below e_t. The list is
+                              read on the stream; it must stay valid until the
+                              call's work has run.                              */
 } lt_options;
 
 /* Fills *opts with the defaults (k-dependent fields are resolved per call). */
@@ -174,6 +187,30 @@ int lt_topk_select(const float* scores, int64_t row_stride, int32_t num_queries,
 int lt_topk_radix(const float* scores, int64_t row_stride, int32_t num_queries, int32_t num_keys,
                   int32_t k, const int32_t* causal_offsets, int32_t* out_idx, float* out_scores,
                   uint32_t flags, void* stream);
+
+/* ---- sample from the previous chunk (sec. 3.2 "Sampling") ---------------- */
+
+/* Bytes of device workspace lt_sample_from_topk needs for num_keys keys
+   (0 for num_keys < 0). */
+size_t lt_sample_from_topk_workspace_size(int32_t num_keys);
+
+/* The sample the paper takes for a prefill chunk: the keys that occur most
+   often in the previous chunk's top-k results. count(s) is the number of
+   entries prev_idx[t * ld + j] == s over t < prev_rows, j < prev_k; entries
+   outside [0, num_keys) (such as the -1 padding) are ignored. The selected
+   keys are the sample_size keys of largest count (equal counts: lower key
+   index first), restricted to keys with count >= 1. They are written to
+   sample_keys[0, n) in ascending key order, followed by -1 up to
+   sample_size. The result is meant as lt_options.sample_keys for the next
+   chunk of queries over the same keys (any list is safe there).
+   prev_idx    DEVICE int32, rows of `ld` >= prev_k entries (prev_rows may be 0).
+   sample_keys DEVICE int32 [sample_size]; 1 <= sample_size <= LT_SAMPLE_LIST_MAX.
+   workspace   at least lt_sample_from_topk_workspace_size(num_keys) bytes,
+               256-byte aligned; contents on entry do not matter.
+   Limits: prev_rows * prev_k < 2^31. */
+int lt_sample_from_topk(const int32_t* prev_idx, int64_t ld, int32_t prev_rows, int32_t prev_k,
+                        int32_t num_keys, int32_t sample_size, int32_t* sample_keys, void* workspace,
+                        size_t workspace_bytes, void* stream);
 
 /* ---- timing helpers ------------------------------------------------------- */
 

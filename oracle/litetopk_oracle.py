@@ -32,6 +32,12 @@ buffers): those cannot change an exact top-k, so the oracle leaves them out.
   S.1111.111 is NaN) times a positive float32 per-token scale; the product is
   exact in float64.
 * bf16 inputs are the upper 16 bits of a float32.
+* Previous-chunk sample -- sec. 3.2 "Sampling": for a prefill chunk the
+  sample is the k' keys that occur most often in the previous chunk's top-k
+  results. The paper does not say how equal counts are ordered or what
+  happens when fewer than k' distinct keys occur; the oracle takes equal
+  counts in ascending key order and returns only keys that occur at least
+  once (then padding -1), listed in ascending key order.
 """
 from __future__ import annotations
 
@@ -196,3 +202,21 @@ def indexer_topk(q: np.ndarray, q_dtype: str, q_scale: Optional[np.ndarray], w: 
     if return_scores:
         return out_i, out_s, full
     return out_i, out_s
+
+
+def sample_from_topk(prev_idx: np.ndarray, num_keys: int, sample_size: int) -> np.ndarray:
+    """Previous-chunk sample, sec. 3.2 "Sampling": count how often every key
+    in [0, num_keys) occurs in the previous chunk's top-k lists (entries
+    outside that range, such as the -1 padding, are not keys), rank keys by
+    (count desc, key asc), keep the first ``sample_size`` of them that occur
+    at least once, and return them ascending, padded with -1 to
+    ``sample_size`` (int32)."""
+    v = np.asarray(prev_idx, dtype=np.int64).ravel()
+    v = v[(v >= 0) & (v < num_keys)]
+    counts = np.bincount(v, minlength=num_keys)
+    rank = np.lexsort((np.arange(num_keys), -counts))
+    chosen = rank[:sample_size]
+    chosen = np.sort(chosen[counts[chosen] >= 1])
+    out = np.full(sample_size, -1, dtype=np.int32)
+    out[: chosen.size] = chosen
+    return out

@@ -15,6 +15,7 @@ constexpr int kDefaultBins = 256;
 constexpr int kFallbackGridFused = 64;      // rows re-scored concurrently (scratch rows)
 constexpr int kFallbackGridScores = 256;
 constexpr int kTargetBlocks = 256;          // one block per CU before key splitting stops
+constexpr int kMinSplitKeys = 4096;         // shortest key split the automatic choice makes
 constexpr size_t kHistLdsBudget = 96 * 1024;
 constexpr size_t kLdsPerBlock = 160 * 1024;   // gfx950 LDS per workgroup
 constexpr int kSampleBlockScores = 64;      // scores-in sample: runs of 64 consecutive keys
@@ -27,10 +28,12 @@ struct Resolved {
   uint64_t seed;
   void** ev;
   int32_t* stats;
+  const int32_t* keys_in;  // caller's sample list, or NULL for the random sample
+  int status;              // LT_OK, or the error the options produce
 };
 
 struct Layout {
-  size_t qctl, queue, params, samp, cnt, hist, cand, scratch, total;
+  size_t qctl, queue, params, list, samp, cnt, hist, cand, scratch, total;
 };
 
 Layout carve(int nq, int nk, const Resolved& r, bool fused) {
@@ -44,6 +47,7 @@ Layout carve(int nq, int nk, const Resolved& r, bool fused) {
   L.qctl = take(256);
   L.queue = take((size_t)nq * 4);
   L.params = take((size_t)nq * sizeof(RowParam));
+  L.list = take((size_t)r.ns * 4);
   L.samp = fused ? take((size_t)nq * r.ns * 4) : 0;
   L.cnt = take((size_t)nq * r.S * 4);
   L.hist = take((size_t)nq * r.S * r.m * 4);
@@ -70,6 +74,20 @@ void resolve_common(const lt_options* o, int k, Resolved& r) {
   r.ev = o->stage_events;
   r.stats = o->row_stats;
   r.E = select_entries(k);
+  r.keys_in = o->sample_keys;
+  r.status = LT_OK;
+  if (r.keys_in && (o->sample_size < 1 || o->sample_size > LT_SAMPLE_LIST_MAX)) r.status = LT_EINVAL;
+}
+
+// Sample size: the caller's list length, or k' from the options and mode.
+int resolve_sample(const lt_options* o, const Resolved& r, int nk, int k, int mode, bool fused) {
+  if (r.keys_in) return r.status == LT_OK ? o->sample_size : 0;
+  int ns = o->sample_size;
+  if (ns < 0) {
+    ns = 3 * k;  // sec. 3.2: k' = 3k
+    if (fused && mode == LT_SCORE_IP) ns = std::max(ns, std::min(nk / 64, 65536));
+  }
+  return sample_count(ns, nk);
 }
 
 Resolved resolve_fused(const lt_options* o, int nq, int nk, int k, int mode, const ScoreShape& sh) {
@@ -82,23 +100,19 @@ Resolved resolve_fused(const lt_options* o, int nq, int nk, int k, int mode, con
   const size_t room = kLdsPerBlock - sh.scan_lds - 64;
   const size_t mcap = std::min(kHistLdsBudget, room) / (4 * (size_t)sh.queries_per_block);
   if ((size_t)r.m > mcap) r.m = (int)std::max<size_t>(mcap, 1);
-  int ns = o->sample_size;
-  if (ns < 0) {
-    ns = 3 * k;  // sec. 3.2: k' = 3k
-    if (mode == LT_SCORE_IP) ns = std::max(ns, std::min(nk / 64, 65536));
-  }
-  r.ns = sample_count(ns, nk);
+  r.ns = resolve_sample(o, r, nk, k, mode, true);
   const int steps = (nk + sh.keys_per_step - 1) / sh.keys_per_step;
   const int tiles = (nq + sh.queries_per_block - 1) / sh.queries_per_block;
   int S = 1;
   if (o->key_splits > 0) {
     S = std::min(o->key_splits, std::max(steps, 1));
   } else {
-    // Split the key range only while the GPU is not yet full and every split
-    // still spans many times the sample (a split's threshold tightens only
-    // from its own histogram).
-    const long long span = 16LL * std::max(k, r.ns);
-    while ((long long)tiles * S < kTargetBlocks && (long long)nk / (2 * S) >= span) S *= 2;
+    // Split the key range while the GPU is not yet full (one block per CU)
+    // and every split keeps at least kMinSplitKeys keys. Each split tightens
+    // its threshold only from its own histogram, so a split adds survivors
+    // when the initial threshold is loose; a short launch that fills one
+    // CU in eight loses far more.
+    while ((long long)tiles * S < kTargetBlocks && (long long)nk / (2 * S) >= kMinSplitKeys) S *= 2;
   }
   r.S = S;
   const int per = (nk + S - 1) / S;
@@ -113,8 +127,7 @@ Resolved resolve_scores(const lt_options* o, int nq, int nk, int k) {
   lt_options d;
   lt_options_default(&d);
   if (!o) o = &d;
-  int ns = o->sample_size < 0 ? 3 * k : o->sample_size;
-  r.ns = sample_count(ns, nk);
+  r.ns = resolve_sample(o, r, nk, k, LT_SCORE_DSA, false);
   int S = 1;
   if (o->key_splits > 0) S = o->key_splits;
   r.S = std::max(1, std::min(S, (nk + 255) / 256 + 1));
@@ -127,6 +140,12 @@ Resolved resolve_scores(const lt_options* o, int nq, int nk, int k) {
 inline bool aligned(const void* p, size_t a) { return ((uintptr_t)p % a) == 0; }
 
 inline int hip_status(hipError_t e) { return e == hipSuccess ? LT_OK : LT_EHIP; }
+
+// The launch's sample list: the caller's, cleaned, or the random one.
+hipError_t make_list(const Resolved& r, int nk, int blk, int32_t* list, hipStream_t st) {
+  if (r.keys_in) return launch_list_clean(r.keys_in, r.ns, nk, list, st);
+  return launch_sample_list(list, r.ns, nk, blk, r.seed, st);
+}
 
 inline void record(const Resolved& r, int i, hipStream_t st) {
   if (r.ev && r.ev[i]) (void)hipEventRecord((hipEvent_t)r.ev[i], st);
@@ -159,6 +178,7 @@ void lt_options_default(lt_options* o) {
   o->seed = 0x5EED5EEDull;
   o->stage_events = nullptr;
   o->row_stats = nullptr;
+  o->sample_keys = nullptr;
 }
 
 const char* lt_strerror(int status) {
@@ -178,6 +198,7 @@ size_t lt_indexer_topk_workspace_size(int32_t nq, int32_t nk, int32_t h, int32_t
   ScoreShape sh = score_shape(dtype, mode, h, d);
   if (!sh.supported) return 0;
   Resolved r = resolve_fused(opts, nq, nk, k, mode, sh);
+  if (r.status) return 0;
   return carve(nq, nk, r, true).total;
 }
 
@@ -194,6 +215,7 @@ int lt_indexer_topk(const void* q, const float* q_scale, const float* w, const v
   if (!out_idx || !out_scores || !workspace || !aligned(workspace, 256)) return LT_EINVAL;
   const ScoreShape sh = score_shape(dtype, mode, h, d);
   const Resolved r = resolve_fused(opts, nq, nk, k, mode, sh);
+  if (r.status) return r.status;
   const Layout L = carve(nq, nk, r, true);
   if (workspace_bytes < L.total) return LT_EWORKSPACE;
   hipStream_t st = (hipStream_t)stream;
@@ -201,6 +223,7 @@ int lt_indexer_topk(const void* q, const float* q_scale, const float* w, const v
   uint32_t* qctl = reinterpret_cast<uint32_t*>(ws + L.qctl);
   int32_t* queue = reinterpret_cast<int32_t*>(ws + L.queue);
   RowParam* params = reinterpret_cast<RowParam*>(ws + L.params);
+  int32_t* list = reinterpret_cast<int32_t*>(ws + L.list);
   float* samp = reinterpret_cast<float*>(ws + L.samp);
   uint32_t* cnt = reinterpret_cast<uint32_t*>(ws + L.cnt);
   uint32_t* hist = reinterpret_cast<uint32_t*>(ws + L.hist);
@@ -211,9 +234,10 @@ int lt_indexer_topk(const void* q, const float* q_scale, const float* w, const v
   hipError_t e;
   record(r, LT_STAGE_SAMPLE, st);
   if ((e = launch_init(qctl, st)) != hipSuccess) return hip_status(e);
-  if (r.ns > 0 && (e = launch_sample_scores(a, r.ns, r.seed, samp, st)) != hipSuccess) return hip_status(e);
+  if ((e = make_list(r, nk, 1, list, st)) != hipSuccess) return hip_status(e);
+  if (r.ns > 0 && (e = launch_sample_scores(a, list, r.ns, samp, st)) != hipSuccess) return hip_status(e);
   record(r, LT_STAGE_RANGE, st);
-  if ((e = launch_range(false, samp, r.ns, nq, nk, offs, r.ns, 1, r.seed, r.m, k, params, st)) != hipSuccess)
+  if ((e = launch_range(false, samp, r.ns, nq, nk, offs, list, r.ns, r.m, k, params, st)) != hipSuccess)
     return hip_status(e);
   record(r, LT_STAGE_FILTER, st);
   if ((e = launch_fused_scan(a, params, r.S, r.L, r.cap, r.m, k, cnt, hist, cand, st)) != hipSuccess)
@@ -245,6 +269,7 @@ int lt_indexer_scores(const void* q, const float* q_scale, const float* w, const
 size_t lt_topk_select_workspace_size(int32_t nq, int32_t nk, int32_t k, const lt_options* opts) {
   if (nq < 0 || nk < 0 || k < 1 || k > LT_K_MAX) return 0;
   Resolved r = resolve_scores(opts, nq, nk, k);
+  if (r.status) return 0;
   return carve(nq, nk, r, false).total;
 }
 
@@ -264,6 +289,7 @@ int lt_topk_select(const float* scores, int64_t stride, int32_t nq, int32_t nk, 
   if (nq == 0) return LT_OK;
   if (!out_idx || !out_scores || !workspace || !aligned(workspace, 256)) return LT_EINVAL;
   const Resolved r = resolve_scores(opts, nq, nk, k);
+  if (r.status) return r.status;
   const Layout L = carve(nq, nk, r, false);
   if (workspace_bytes < L.total) return LT_EWORKSPACE;
   hipStream_t st = (hipStream_t)stream;
@@ -271,6 +297,7 @@ int lt_topk_select(const float* scores, int64_t stride, int32_t nq, int32_t nk, 
   uint32_t* qctl = reinterpret_cast<uint32_t*>(ws + L.qctl);
   int32_t* queue = reinterpret_cast<int32_t*>(ws + L.queue);
   RowParam* params = reinterpret_cast<RowParam*>(ws + L.params);
+  int32_t* list = reinterpret_cast<int32_t*>(ws + L.list);
   uint32_t* cnt = reinterpret_cast<uint32_t*>(ws + L.cnt);
   uint32_t* hist = reinterpret_cast<uint32_t*>(ws + L.hist);
   int2* cand = reinterpret_cast<int2*>(ws + L.cand);
@@ -278,9 +305,9 @@ int lt_topk_select(const float* scores, int64_t stride, int32_t nq, int32_t nk, 
   hipError_t e;
   record(r, LT_STAGE_SAMPLE, st);
   if ((e = launch_init(qctl, st)) != hipSuccess) return hip_status(e);
+  if ((e = make_list(r, nk, kSampleBlockScores, list, st)) != hipSuccess) return hip_status(e);
   record(r, LT_STAGE_RANGE, st);
-  if ((e = launch_range(true, scores, stride, nq, nk, offs, r.ns, kSampleBlockScores, r.seed, r.m, k, params,
-                        st)) != hipSuccess)
+  if ((e = launch_range(true, scores, stride, nq, nk, offs, list, r.ns, r.m, k, params, st)) != hipSuccess)
     return hip_status(e);
   record(r, LT_STAGE_FILTER, st);
   if ((e = launch_filter(scores, stride, nq, nk, offs, params, r.S, r.L, r.cap, r.m, k, cnt, hist, cand, st)) != hipSuccess)
@@ -304,6 +331,23 @@ int lt_topk_radix(const float* scores, int64_t stride, int32_t nq, int32_t nk, i
   if (nq == 0) return LT_OK;
   if (!out_idx || !out_scores) return LT_EINVAL;
   return hip_status(launch_radix(scores, stride, nq, nk, offs, k, flags, out_idx, out_scores, (hipStream_t)stream));
+}
+
+size_t lt_sample_from_topk_workspace_size(int32_t nk) {
+  if (nk < 0) return 0;
+  return freq_workspace_bytes(nk);
+}
+
+int lt_sample_from_topk(const int32_t* prev, int64_t ld, int32_t rows, int32_t pk, int32_t nk, int32_t ns,
+                        int32_t* out, void* workspace, size_t workspace_bytes, void* stream) {
+  if (rows < 0 || pk < 0 || nk < 0 || ld < pk) return LT_EINVAL;
+  if (ns < 1 || ns > LT_SAMPLE_LIST_MAX || !out) return LT_EINVAL;
+  if ((int64_t)rows * pk >= (1LL << 31)) return LT_EINVAL;
+  if (rows > 0 && pk > 0 && !prev) return LT_EINVAL;
+  if (!workspace || !aligned(workspace, 256)) return LT_EINVAL;
+  if (workspace_bytes < freq_workspace_bytes(nk)) return LT_EWORKSPACE;
+  if (pk == 0) rows = 0;
+  return hip_status(launch_sample_from_topk(prev, ld, rows, pk, nk, ns, out, workspace, (hipStream_t)stream));
 }
 
 int lt_event_create(void** ev) {

@@ -13,8 +13,8 @@ namespace lt {
 // ---- selection side (select.hip) ----
 hipError_t launch_init(uint32_t* qctl, hipStream_t st);
 hipError_t launch_range(bool from_scores, const float* src, int64_t stride, int nq, int nk,
-                        const int32_t* offs, int ns, int blk, uint64_t seed, int m, int k,
-                        RowParam* params, hipStream_t st);
+                        const int32_t* offs, const int32_t* list, int ns, int m, int k, RowParam* params,
+                        hipStream_t st);
 hipError_t launch_filter(const float* scores, int64_t stride, int nq, int nk, const int32_t* offs,
                          const RowParam* params, int S, int L, int cap, int m, int k, uint32_t* cnt,
                          uint32_t* hist, int2* cand, hipStream_t st);
@@ -28,6 +28,16 @@ hipError_t launch_fallback_scores(const float* scores, int64_t stride, int nk, c
                                   int32_t* out_i, float* out_s, int grid, hipStream_t st);
 hipError_t launch_radix(const float* scores, int64_t stride, int nq, int nk, const int32_t* offs,
                         int k, uint32_t flags, int32_t* out_i, float* out_s, hipStream_t st);
+
+// ---- sample lists (sample.hip) ----
+// list[i] = the i-th key of the stratified random sample (runs of blk keys).
+hipError_t launch_sample_list(int32_t* list, int ns, int nk, int blk, uint64_t seed, hipStream_t st);
+// out = the caller's list with out-of-range and repeated keys replaced by -1 (ns <= LT_SAMPLE_LIST_MAX).
+hipError_t launch_list_clean(const int32_t* in, int ns, int nk, int32_t* out, hipStream_t st);
+// The previous-chunk sample (lt_sample_from_topk); ws holds freq_workspace_bytes(nk).
+size_t freq_workspace_bytes(int nk);
+hipError_t launch_sample_from_topk(const int32_t* prev, int64_t ld, int rows, int pk, int nk, int ns,
+                                   int32_t* out, void* ws, hipStream_t st);
 
 // ---- score side (score.hip) ----
 struct ScoreArgs {
@@ -50,8 +60,8 @@ struct ScoreShape {
 };
 ScoreShape score_shape(int dtype, int mode, int h, int d);
 
-// Sample scores: samp[t * ns + i] = I(t, sample_key(i)), blk = 1.
-hipError_t launch_sample_scores(const ScoreArgs& a, int ns, uint64_t seed, float* samp, hipStream_t st);
+// Sample scores: samp[t * ns + i] = I(t, list[i]) (holes score key 0; never read).
+hipError_t launch_sample_scores(const ScoreArgs& a, const int32_t* list, int ns, float* samp, hipStream_t st);
 // Dense scores: out[t * ld + s] = I(t, s) for every key.
 hipError_t launch_dense_scores(const ScoreArgs& a, float* out, int64_t ld, hipStream_t st);
 // Fused score + gate + write-back scan over S key splits of L keys each.

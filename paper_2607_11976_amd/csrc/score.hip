@@ -310,10 +310,12 @@ __device__ __forceinline__ void schedule_half() {
 struct SrcContig {
   __device__ int key(int i) const { return i; }
 };
-struct SrcSample {
-  int ns, nk;
-  uint64_t seed;
-  __device__ int key(int i) const { return sample_key(i, ns, nk, 1, seed); }
+struct SrcList {
+  const int32_t* list;
+  __device__ int key(int i) const {
+    const int v = list[i];
+    return v < 0 ? 0 : v;
+  }
 };
 
 // The block-wide scan of positions [kbeg, kend) of `src` (key index =
@@ -593,14 +595,15 @@ struct FusedSink {
 // Kernels
 // ---------------------------------------------------------------------------
 template <class C>
-__global__ __launch_bounds__(C::NTHREADS) void k_sample(ScoreArgs a, int ns, uint64_t seed, float* samp, int slice) {
+__global__ __launch_bounds__(C::NTHREADS) void k_sample(ScoreArgs a, const int32_t* list, int ns, float* samp,
+                                                        int slice) {
   extern __shared__ __align__(16) uint8_t lds[];
   const int q0 = blockIdx.x * C::QT, wave = threadIdx.x / kWave, qbase = q0 + wave * C::QW;
   const int kb = blockIdx.y * slice, ke = min(kb + slice, ns);
   WaveQ<C> wq;
   load_q<C>(wq, a, qbase);
   DenseSink<C> sink{samp, ns, qbase, a.nq};
-  wg_scan<C>(a, SrcSample{ns, a.nk, seed}, kb, ke, lds, wq, sink);
+  wg_scan<C>(a, SrcList{list}, kb, ke, lds, wq, sink);
 }
 
 template <class C>
@@ -716,16 +719,24 @@ ScoreShape score_shape(int dtype, int mode, int h, int d) {
 }
 
 static constexpr int kSlice = 8192;   // positions per block in the sample / dense scorers
+static constexpr int kSampleBlocks = 256;  // the sample scorer aims at one block per CU at least
 
-hipError_t launch_sample_scores(const ScoreArgs& a, int ns, uint64_t seed, float* samp, hipStream_t st) {
+hipError_t launch_sample_scores(const ScoreArgs& a, const int32_t* list, int ns, float* samp, hipStream_t st) {
   hipError_t err = hipErrorInvalidValue;
   with_cfg(a.dtype, a.mode, a.h, a.d, [&]<class C>() {
-    dim3 grid((a.nq + C::QT - 1) / C::QT, (ns + kSlice - 1) / kSlice);
+    // few query tiles (a short chunk): cut the sample into more slices so
+    // that the launch still covers the GPU
+    const int tiles = (a.nq + C::QT - 1) / C::QT;
+    const int want = tiles > 0 ? (kSampleBlocks + tiles - 1) / tiles : 1;
+    int slice = (ns + want - 1) / want;
+    slice = ((slice + C::KT - 1) / C::KT) * C::KT;
+    slice = slice < C::KT ? C::KT : (slice > kSlice ? kSlice : slice);
+    dim3 grid(tiles, (ns + slice - 1) / slice);
     if (grid.x == 0 || grid.y == 0) {
       err = hipSuccess;
       return;
     }
-    hipLaunchKernelGGL(k_sample<C>, grid, dim3(C::NTHREADS), C::RING * C::TILE_BYTES, st, a, ns, seed, samp, kSlice);
+    hipLaunchKernelGGL(k_sample<C>, grid, dim3(C::NTHREADS), C::RING * C::TILE_BYTES, st, a, list, ns, samp, slice);
     err = hipGetLastError();
   });
   return err;

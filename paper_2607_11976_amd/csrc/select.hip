@@ -14,61 +14,105 @@ __global__ void k_init(uint32_t* qctl) {
 }
 
 // ---------------------------------------------------------------------------
-// Range and initial threshold (sec. 3.2 "Sampling"). One wave per row.
+// Range and initial threshold (sec. 3.2 "Sampling"). One block per row.
 // s_min / s_max over the row's visible, finite sample scores; delta = m /
 // (s_max - s_min); tau0 = bin of the k-th largest visible sample score, found
 // with the sample's histogram. The sample histogram is NOT carried into the
 // scan: every sampled key is scanned again, and counting it twice could
 // raise the threshold above the true k-th score.
-// FROM_SCORES: the sample is read from a score matrix (scores-in entry);
-// otherwise from the [nq, ns] matrix of sample scores the sample kernel wrote.
+// The sample is the key list `list` (holes < 0 skipped). FROM_SCORES: its
+// scores are read from a score matrix (scores-in entry); otherwise from the
+// [nq, ns] matrix of sample scores the sample kernel wrote. Each thread keeps
+// kRangeUnroll loads in flight: the kernel is bound by load latency.
 // ---------------------------------------------------------------------------
+constexpr int kRangeThreads = 256;
+constexpr int kRangeUnroll = 8;
+
 template <bool FROM_SCORES>
-__global__ __launch_bounds__(256) void k_range(const float* src, int64_t stride, int nq, int nk,
-                                               const int32_t* offs, int ns, int blk, uint64_t seed,
-                                               int m, int k, RowParam* params) {
-  __shared__ uint32_t hist_all[4][kMaxBins];
-  const int wave = threadIdx.x / kWave, l = lane_id();
-  const int row = blockIdx.x * 4 + wave;
-  if (row >= nq) return;
-  uint32_t* hist = hist_all[wave];
+__device__ __forceinline__ void range_load(const float* rp, const int32_t* list, int ns, int e, int base,
+                                           float (&s)[kRangeUnroll], bool (&vis)[kRangeUnroll]) {
+  int key[kRangeUnroll];
+#pragma unroll
+  for (int u = 0; u < kRangeUnroll; ++u) {
+    const int i = base + u * kRangeThreads + (int)threadIdx.x;
+    key[u] = i < ns ? list[i] : -1;
+  }
+#pragma unroll
+  for (int u = 0; u < kRangeUnroll; ++u) {
+    const int i = base + u * kRangeThreads + (int)threadIdx.x;
+    vis[u] = key[u] >= 0 && key[u] < e;
+    s[u] = vis[u] ? (FROM_SCORES ? rp[key[u]] : rp[i]) : 0.0f;
+  }
+}
+
+template <bool FROM_SCORES>
+__global__ __launch_bounds__(kRangeThreads) void k_range(const float* src, int64_t stride, int nq, int nk,
+                                                         const int32_t* offs, const int32_t* list, int ns, int m,
+                                                         int k, RowParam* params) {
+  constexpr int NW = kRangeThreads / kWave;
+  __shared__ uint32_t hist[kMaxBins];
+  __shared__ float red_mn[NW], red_mx[NW];
+  __shared__ uint32_t red_n[NW];
+  const int row = blockIdx.x, wave = threadIdx.x / kWave, l = lane_id();
   int e = offs ? offs[row] : nk;
   e = e < 0 ? 0 : (e > nk ? nk : e);
   const float* rp = src + (int64_t)row * stride;
 
+  for (int b = threadIdx.x; b < kMaxBins; b += kRangeThreads) hist[b] = 0u;
   float mn = __builtin_inff(), mx = -__builtin_inff();
   uint32_t nvis = 0;
-  for (int i = l; i < ns; i += kWave) {
-    int key = sample_key(i, ns, nk, blk, seed);
-    if (key >= e) continue;
-    float s = FROM_SCORES ? rp[key] : rp[i];
-    ++nvis;
-    if (__builtin_isfinite(s)) {
-      mn = fminf(mn, s);
-      mx = fmaxf(mx, s);
+  for (int base = 0; base < ns; base += kRangeThreads * kRangeUnroll) {
+    float s[kRangeUnroll];
+    bool vis[kRangeUnroll];
+    range_load<FROM_SCORES>(rp, list, ns, e, base, s, vis);
+#pragma unroll
+    for (int u = 0; u < kRangeUnroll; ++u) {
+      nvis += vis[u];
+      if (vis[u] && __builtin_isfinite(s[u])) {
+        mn = fminf(mn, s[u]);
+        mx = fmaxf(mx, s[u]);
+      }
     }
   }
   mn = wave_min(mn);
   mx = wave_max(mx);
   nvis = wave_sum(nvis);
+  if (l == 0) {
+    red_mn[wave] = mn;
+    red_mx[wave] = mx;
+    red_n[wave] = nvis;
+  }
+  __syncthreads();
+  mn = red_mn[0];
+  mx = red_mx[0];
+  nvis = red_n[0];
+#pragma unroll
+  for (int w = 1; w < NW; ++w) {
+    mn = fminf(mn, red_mn[w]);
+    mx = fmaxf(mx, red_mx[w]);
+    nvis += red_n[w];
+  }
   float delta = 1.0f, c = 0.0f;
   if (mx > mn) delta = (float)m / (mx - mn);
   if (!(delta > 0.0f) || !__builtin_isfinite(delta)) delta = 1.0f;
   if (__builtin_isfinite(mn)) c = -mn * delta;
   if (!__builtin_isfinite(c)) c = 0.0f;
 
-  for (int b = l; b < kMaxBins; b += kWave) hist[b] = 0u;
-  __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "wavefront");
-  for (int i = l; i < ns; i += kWave) {
-    int key = sample_key(i, ns, nk, blk, seed);
-    if (key >= e) continue;
-    float s = FROM_SCORES ? rp[key] : rp[i];
-    int b = bin_of(bin_x(s, delta, c), m);
-    if (b >= 0) atomicAdd(&hist[b], 1u);
+  for (int base = 0; base < ns; base += kRangeThreads * kRangeUnroll) {
+    float s[kRangeUnroll];
+    bool vis[kRangeUnroll];
+    range_load<FROM_SCORES>(rp, list, ns, e, base, s, vis);
+#pragma unroll
+    for (int u = 0; u < kRangeUnroll; ++u) {
+      const int b = bin_of(bin_x(s[u], delta, c), m);
+      if (vis[u] && b >= 0) atomicAdd(&hist[b], 1u);
+    }
   }
-  __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "wavefront");
-  int tau0 = wave_threshold(hist, m, (uint32_t)k, nullptr);
-  if (l == 0) params[row] = RowParam{delta, c, tau0, (int)nvis};
+  __syncthreads();
+  if (wave == 0) {
+    const int tau0 = wave_threshold(hist, m, (uint32_t)k, nullptr);
+    if (l == 0) params[row] = RowParam{delta, c, tau0, (int)nvis};
+  }
 }
 
 // ---------------------------------------------------------------------------
@@ -349,13 +393,13 @@ hipError_t launch_init(uint32_t* qctl, hipStream_t st) {
 }
 
 hipError_t launch_range(bool from_scores, const float* src, int64_t stride, int nq, int nk,
-                        const int32_t* offs, int ns, int blk, uint64_t seed, int m, int k,
-                        RowParam* params, hipStream_t st) {
-  dim3 grid((nq + 3) / 4);
+                        const int32_t* offs, const int32_t* list, int ns, int m, int k, RowParam* params,
+                        hipStream_t st) {
+  dim3 grid(nq);
   if (from_scores)
-    hipLaunchKernelGGL(k_range<true>, grid, dim3(256), 0, st, src, stride, nq, nk, offs, ns, blk, seed, m, k, params);
+    hipLaunchKernelGGL(k_range<true>, grid, dim3(kRangeThreads), 0, st, src, stride, nq, nk, offs, list, ns, m, k, params);
   else
-    hipLaunchKernelGGL(k_range<false>, grid, dim3(256), 0, st, src, stride, nq, nk, offs, ns, blk, seed, m, k, params);
+    hipLaunchKernelGGL(k_range<false>, grid, dim3(kRangeThreads), 0, st, src, stride, nq, nk, offs, list, ns, m, k, params);
   return hipGetLastError();
 }
 

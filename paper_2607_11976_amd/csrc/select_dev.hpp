@@ -34,16 +34,16 @@ __device__ __forceinline__ uint32_t block_scan_excl(uint32_t v, uint32_t* tmp, u
   return base + s - v;
 }
 
-// Descending bitonic sort of P (power of two) 64-bit keys in LDS.
-template <int NTH>
-__device__ __forceinline__ void bitonic_sort_desc(uint64_t* a, int P) {
+// Descending bitonic sort of P (power of two) unsigned keys in LDS.
+template <int NTH, typename T>
+__device__ __forceinline__ void bitonic_sort_desc(T* a, int P) {
   for (int size = 2; size <= P; size <<= 1) {
     for (int stride = size >> 1; stride > 0; stride >>= 1) {
       for (int t = threadIdx.x; t < (P >> 1); t += NTH) {
         int i = 2 * t - (t & (stride - 1));
         int j = i + stride;
         bool desc = (i & size) == 0;
-        uint64_t x = a[i], y = a[j];
+        T x = a[i], y = a[j];
         if ((x < y) == desc) {
           a[i] = y;
           a[j] = x;

@@ -28,12 +28,14 @@ LT_F32, LT_BF16, LT_FP8_E4M3FN = 0, 1, 2
 LT_SCORE_DSA, LT_SCORE_IP = 0, 1
 LT_SORTED_OUTPUT, LT_FORCE_FALLBACK = 1, 2
 LT_K_MAX = 8192
+LT_SAMPLE_LIST_MAX = 32768
 LT_NUM_STAGE_EVENTS = 6
 STAGES = ("sample", "range", "filter", "select", "fallback")
 
 EXPORTED = (
     "lt_options_default", "lt_indexer_topk_workspace_size", "lt_indexer_topk", "lt_indexer_scores",
-    "lt_topk_select_workspace_size", "lt_topk_select", "lt_topk_radix", "lt_event_create",
+    "lt_topk_select_workspace_size", "lt_topk_select", "lt_topk_radix",
+    "lt_sample_from_topk_workspace_size", "lt_sample_from_topk", "lt_event_create",
     "lt_event_destroy", "lt_event_record", "lt_event_elapsed_ms", "lt_strerror",
 )
 
@@ -48,6 +50,7 @@ class LtOptions(ctypes.Structure):
         ("seed", ctypes.c_uint64),
         ("stage_events", ctypes.c_void_p),
         ("row_stats", ctypes.c_void_p),
+        ("sample_keys", ctypes.c_void_p),
     ]
 
 
@@ -87,6 +90,10 @@ def load(path: str = LIB_PATH):
     lib.lt_topk_select.restype = ctypes.c_int
     lib.lt_topk_radix.argtypes = [_P, _I64, _I32, _I32, _I32, _P, _P, _P, ctypes.c_uint32, _P]
     lib.lt_topk_radix.restype = ctypes.c_int
+    lib.lt_sample_from_topk_workspace_size.argtypes = [_I32]
+    lib.lt_sample_from_topk_workspace_size.restype = _SZ
+    lib.lt_sample_from_topk.argtypes = [_P, _I64, _I32, _I32, _I32, _I32, _P, _P, _SZ, _P]
+    lib.lt_sample_from_topk.restype = ctypes.c_int
     lib.lt_event_create.argtypes = [ctypes.POINTER(ctypes.c_void_p)]
     lib.lt_event_create.restype = ctypes.c_int
     lib.lt_event_destroy.argtypes = [_P]
@@ -147,6 +154,16 @@ def lt_topk_radix(scores, row_stride, nq, nk, k, causal_offsets, out_idx, out_sc
     return load().lt_topk_radix(scores, row_stride, nq, nk, k, causal_offsets, out_idx, out_scores, flags, stream)
 
 
+def lt_sample_from_topk_workspace_size(nk) -> int:
+    return load().lt_sample_from_topk_workspace_size(nk)
+
+
+def lt_sample_from_topk(prev_idx, ld, prev_rows, prev_k, nk, sample_size, sample_keys, workspace, workspace_bytes,
+                        stream) -> int:
+    return load().lt_sample_from_topk(prev_idx, ld, prev_rows, prev_k, nk, sample_size, sample_keys, workspace,
+                                      workspace_bytes, stream)
+
+
 def lt_strerror(status: int) -> str:
     return load().lt_strerror(status).decode()
 
@@ -188,7 +205,11 @@ def _on_gpu(*ts):
 
 def make_options(num_bins=None, sample_size=None, capacity=None, key_splits=None,
                  sorted_output=False, force_fallback=False, seed=None, stage_events=None,
-                 row_stats: Optional[torch.Tensor] = None) -> LtOptions:
+                 row_stats: Optional[torch.Tensor] = None,
+                 sample_keys: Optional[torch.Tensor] = None) -> LtOptions:
+    """lt_options from keyword arguments. sample_keys: a GPU int32 list used
+    as the sample (its length becomes sample_size); the tensor must stay
+    alive until the call that uses these options has run."""
     o = lt_options_default()
     if num_bins is not None:
         o.num_bins = num_bins
@@ -205,6 +226,11 @@ def make_options(num_bins=None, sample_size=None, capacity=None, key_splits=None
         o.stage_events = ctypes.cast(stage_events.array, ctypes.c_void_p)
     if row_stats is not None:
         o.row_stats = row_stats.data_ptr()
+    if sample_keys is not None:
+        _on_gpu(sample_keys)
+        _need(sample_keys.dtype == torch.int32 and sample_keys.dim() == 1, "sample_keys must be int32 [n]")
+        o.sample_keys = sample_keys.data_ptr()
+        o.sample_size = sample_keys.numel()
     return o
 
 
@@ -337,4 +363,25 @@ def topk_radix(scores: torch.Tensor, k: int, num_keys: Optional[int] = None,
     st = lt_topk_radix(_ptr(scores), scores.stride(0), nq, nk, k, _ptr(causal_offsets), _ptr(out[0]), _ptr(out[1]),
                        LT_SORTED_OUTPUT if sorted_output else 0, _stream(stream))
     _check(st, "lt_topk_radix")
+    return out
+
+
+def sample_from_topk(prev_idx: torch.Tensor, num_keys: int, sample_size: int, out: Optional[torch.Tensor] = None,
+                     workspace: Optional[torch.Tensor] = None, stream=None) -> torch.Tensor:
+    """The previous chunk's sample (sec. 3.2 "Sampling"): the sample_size keys
+    that occur most often in prev_idx [rows, k] (int32, -1 padding ignored),
+    ascending, then -1. Returns int32 [sample_size]."""
+    _need(prev_idx.is_cuda and prev_idx.dtype == torch.int32 and prev_idx.dim() == 2
+          and (prev_idx.numel() == 0 or prev_idx.stride(1) == 1),
+          "prev_idx must be an int32 [rows, k] GPU matrix with unit column stride")
+    rows, pk = prev_idx.shape
+    if out is None:
+        out = torch.empty(sample_size, dtype=torch.int32, device=prev_idx.device)
+    _need(out.dtype == torch.int32 and out.numel() == sample_size and out.is_contiguous(), "bad out")
+    if workspace is None:
+        workspace = torch.empty(lt_sample_from_topk_workspace_size(num_keys), dtype=torch.uint8,
+                                device=prev_idx.device)
+    st = lt_sample_from_topk(_ptr(prev_idx), prev_idx.stride(0) if prev_idx.numel() else pk, rows, pk, num_keys,
+                             sample_size, _ptr(out), _ptr(workspace), workspace.numel(), _stream(stream))
+    _check(st, "lt_sample_from_topk")
     return out

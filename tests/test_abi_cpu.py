@@ -36,10 +36,10 @@ def test_library_exports_every_header_symbol(lib):
 
 
 def test_options_struct_layout_and_defaults(lib):
-    assert ctypes.sizeof(lt.LtOptions) == 48  # 5 x int32/uint32, pad, seed, 2 pointers
+    assert ctypes.sizeof(lt.LtOptions) == 56  # 5 x int32/uint32, pad, seed, 3 pointers
     o = lt.lt_options_default()
     assert o.num_bins == 256 and o.sample_size < 0 and o.capacity == 0 and o.key_splits == 0
-    assert o.flags == 0 and not o.stage_events and not o.row_stats
+    assert o.flags == 0 and not o.stage_events and not o.row_stats and not o.sample_keys
 
 
 def test_strerror(lib):
@@ -63,6 +63,18 @@ def test_workspace_sizes(lib):
     assert 0 < small < lt.lt_indexer_topk_workspace_size(64, 4096, 4, 64, lt.LT_F32, lt.LT_SCORE_DSA, 256)
     assert lt.lt_topk_select_workspace_size(128, 1000, 10) > 0
     assert lt.lt_topk_select_workspace_size(128, 1000, 0) == 0
+    # a sample list needs a length in [1, LT_SAMPLE_LIST_MAX]
+    o = lt.lt_options_default()
+    o.sample_keys = 256
+    o.sample_size = 0
+    assert lt.lt_topk_select_workspace_size(128, 1000, 10, o) == 0
+    o.sample_size = lt.LT_SAMPLE_LIST_MAX + 1
+    assert lt.lt_indexer_topk_workspace_size(64, 4096, 4, 64, lt.LT_F32, lt.LT_SCORE_DSA, 256, o) == 0
+    o.sample_size = 1000
+    assert lt.lt_indexer_topk_workspace_size(64, 4096, 4, 64, lt.LT_F32, lt.LT_SCORE_DSA, 256, o) > 0
+    # previous-chunk sampler: the per-key counts dominate
+    assert lt.lt_sample_from_topk_workspace_size(1 << 20) >= 4 << 20
+    assert lt.lt_sample_from_topk_workspace_size(-1) == 0
 
 
 def test_argument_checks_reject_before_any_device_work(lib):
@@ -98,6 +110,21 @@ def test_argument_checks_reject_before_any_device_work(lib):
     assert lt.lt_topk_radix(P, 8, 2, 8, 0, None, P, P, 0, None) == lt.LT_EINVAL
     assert lt.lt_indexer_scores(P, None, None, P, None, lt.LT_F32, lt.LT_SCORE_DSA, 2, 8, 4, 64, P, 4,
                                 None) == lt.LT_EINVAL
+    # sample list with a bad length
+    o = lt.lt_options_default()
+    o.sample_keys = P
+    o.sample_size = 0
+    assert lt.lt_indexer_topk(P, None, None, P, None, lt.LT_F32, lt.LT_SCORE_DSA, 4, 8, 4, 64, 2, None,
+                              P, P, P, 1 << 20, o, None) == lt.LT_EINVAL
+    assert lt.lt_topk_select(P, 8, 2, 8, 2, None, P, P, P, 1 << 20, o, None) == lt.LT_EINVAL
+    # previous-chunk sampler: sample size, ld < k, workspace
+    ws = lt.lt_sample_from_topk_workspace_size(100)
+    assert lt.lt_sample_from_topk(P, 4, 2, 4, 100, 0, P, P, ws, None) == lt.LT_EINVAL
+    assert lt.lt_sample_from_topk(P, 4, 2, 4, 100, lt.LT_SAMPLE_LIST_MAX + 1, P, P, ws, None) == lt.LT_EINVAL
+    assert lt.lt_sample_from_topk(P, 3, 2, 4, 100, 10, P, P, ws, None) == lt.LT_EINVAL
+    assert lt.lt_sample_from_topk(None, 4, 2, 4, 100, 10, P, P, ws, None) == lt.LT_EINVAL
+    assert lt.lt_sample_from_topk(P, 4, 2, 4, 100, 10, P, P, ws - 1, None) == lt.LT_EWORKSPACE
+    assert lt.lt_sample_from_topk(P, 4, 2, 4, 100, 10, P, P + 8, ws, None) == lt.LT_EINVAL
     # empty problems are valid and do nothing
     assert lt.lt_indexer_topk(None, None, None, None, None, lt.LT_F32, lt.LT_SCORE_DSA, 0, 0, 4, 64, 2, None,
                               None, None, None, 0, None, None) == lt.LT_OK

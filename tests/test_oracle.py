@@ -396,3 +396,116 @@ def test_pins_catch_planted_selection_mistakes(monkeypatch):
         monkeypatch.setattr(orc, "order", bad)
         with pytest.raises(AssertionError):
             test_select_matches_brute_force_on_tiny_rows()
+
+
+# --------------------------------------------------------------------------
+# previous-chunk sample (sec. 3.2 "Sampling")
+# --------------------------------------------------------------------------
+
+def test_golden_previous_chunk_sample():
+    with open(os.path.join(GOLDEN, "sample_from_topk.json")) as f:
+        g = json.load(f)
+    prev = np.array(g["prev_idx"], dtype=np.int32)
+    for case in g["cases"]:
+        got = orc.sample_from_topk(prev, g["num_keys"], case["sample_size"])
+        assert got.dtype == np.int32
+        assert got.tolist() == case["sample"]
+
+
+def _occurrences(prev, nk):
+    c = {}
+    for v in np.asarray(prev).ravel().tolist():
+        if 0 <= v < nk:
+            c[v] = c.get(v, 0) + 1
+    return c
+
+
+def check_sample_invariants(out, prev, nk, ns):
+    """What fixes the previous-chunk sample uniquely: its size, ascending
+    distinct keys that occur, and dominance -- every sampled key ranks above
+    every key left out under (count desc, key asc)."""
+    c = _occurrences(prev, nk)
+    assert out.dtype == np.int32 and out.shape == (ns,)
+    n = min(ns, len(c))
+    sel = out[:n].tolist()
+    assert np.all(out[n:] == -1)
+    assert sel == sorted(set(sel)) and all(s >= 0 for s in sel)
+    assert all(c.get(s, 0) >= 1 for s in sel)
+    left = set(c) - set(sel)
+    if sel and left:
+        worst_in = min((c[s], -s) for s in sel)
+        best_out = max((c[u], -u) for u in left)
+        assert worst_in > best_out
+
+
+SAMPLE_CASES = [
+    # rows, k, num_keys, sample_size, law
+    (8, 16, 50, 20, "zipf"),
+    (8, 16, 50, 200, "zipf"),
+    (32, 64, 5000, 300, "zipf"),
+    (16, 32, 400, 64, "uniform"),
+    (5, 7, 30, 3, "dirty"),
+    (0, 4, 30, 5, "zipf"),
+    (3, 5, 4, 10, "dirty"),
+]
+
+
+def sample_case_input(rows, k, nk, law, seed):
+    rng = np.random.default_rng(seed)
+    if law == "uniform":
+        p = rng.integers(0, nk, size=(rows, k))
+    else:
+        p = np.minimum(rng.zipf(1.3, size=(rows, k)) - 1, nk - 1)
+    p = p.astype(np.int32)
+    if law == "dirty" and p.size:
+        m = rng.random(p.shape)
+        p[m < 0.15] = -1
+        p[(m >= 0.15) & (m < 0.25)] = nk + 3
+    return p
+
+
+@pytest.mark.parametrize("case", SAMPLE_CASES, ids=[f"{c[0]}x{c[1]}-nk{c[2]}-ns{c[3]}-{c[4]}" for c in SAMPLE_CASES])
+def test_previous_chunk_sample_invariants(case):
+    rows, k, nk, ns, law = case
+    prev = sample_case_input(rows, k, nk, law, seed=rows * 31 + nk)
+    check_sample_invariants(orc.sample_from_topk(prev, nk, ns), prev, nk, ns)
+
+
+def test_pins_catch_planted_sample_mistakes(monkeypatch):
+    good = orc.sample_from_topk
+
+    def ties_high_key(prev, nk, ns):
+        v = np.asarray(prev, dtype=np.int64).ravel()
+        v = v[(v >= 0) & (v < nk)]
+        c = np.bincount(v, minlength=nk)
+        r = np.lexsort((-np.arange(nk), -c))[:ns]
+        r = np.sort(r[c[r] >= 1])
+        out = np.full(ns, -1, np.int32)
+        out[: r.size] = r
+        return out
+
+    def zero_counts_kept(prev, nk, ns):
+        v = np.asarray(prev, dtype=np.int64).ravel()
+        v = v[(v >= 0) & (v < nk)]
+        c = np.bincount(v, minlength=nk)
+        r = np.sort(np.lexsort((np.arange(nk), -c))[:ns])
+        out = np.full(ns, -1, np.int32)
+        out[: r.size] = r
+        return out
+
+    def padding_counted(prev, nk, ns):
+        p = np.where(np.asarray(prev) < 0, 0, prev)
+        return good(p, nk, ns)
+
+    def unsorted(prev, nk, ns):
+        out = good(prev, nk, ns)
+        n = int((out >= 0).sum())
+        out[:n] = out[:n][::-1].copy()
+        return out
+
+    for bad in (ties_high_key, zero_counts_kept, padding_counted, unsorted):
+        monkeypatch.setattr(orc, "sample_from_topk", bad)
+        with pytest.raises(AssertionError):
+            test_golden_previous_chunk_sample()
+            for case in SAMPLE_CASES:
+                test_previous_chunk_sample_invariants(case)
