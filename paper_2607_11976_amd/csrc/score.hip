@@ -99,6 +99,12 @@ struct Cfg {
   static constexpr int ROWB = D * M::ES;               // bytes per key row
   static constexpr int TILE_BYTES = KT * ROWB;         // LDS tile: rows of 16-B chunks, XOR-swizzled
   static constexpr int RING = 4;                       // LDS tiles in flight
+  // fp8: the key scales of each tile follow the tiles into LDS, in a ring of
+  // twice as many slots (the epilogue of tile t runs one step after its MFMAs,
+  // when the tile's own slot is already being refilled)
+  static constexpr int SCALE_RING = 2 * RING;
+  static constexpr int SCALE_BYTES = DT == DT_FP8 ? SCALE_RING * KT * 4 : 0;
+  static constexpr int SCAN_LDS = RING * TILE_BYTES + SCALE_BYTES;
   static constexpr int CPK = ROWB / 16;                // 16-byte chunks per key
   static constexpr int CHUNKS = KT * CPK;
   static constexpr int NTHREADS = WAVES * kWave;
@@ -307,6 +313,17 @@ __device__ __forceinline__ void schedule_half() {
   }
 }
 
+// Histogram increment in LDS, issued as plain ds_add_u32. Written as an
+// opaque instruction so that the compiler does not make it wait for the key
+// tiles still streaming into LDS (global_load_lds counts on vmcnt, and the
+// compiler cannot tell the histogram from the tile ring): LDS operations of
+// one wave complete in order, so the wave's later histogram reads still see
+// the increment, and no other wave reads this wave's histogram rows.
+__device__ __forceinline__ void lds_inc(uint32_t* p) {
+  const uint32_t a = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) uint32_t*)p;
+  asm volatile("ds_add_u32 %0, %1" ::"v"(a), "v"(1u) : "memory");
+}
+
 struct SrcContig {
   __device__ int key(int i) const { return i; }
 };
@@ -337,8 +354,19 @@ __device__ __forceinline__ void wg_scan(const ScoreArgs& a, const Src& src, int 
   // instruction of a wave fills 64 consecutive 16-byte chunk slots. Rows past
   // kend are clamped to the last valid row: their scores are never used
   // (every consumer masks positions >= kend).
-  const int wave = tid / kWave;
-  auto stage = [&](int slot, int k0) {
+  const int wave = __builtin_amdgcn_readfirstlane(tid / kWave);
+  auto stage = [&](int slot, int st_abs, int k0) {
+    if constexpr (C::DT == DT_FP8) {
+      // wave 0 copies the tile's key scales (64 lanes x 4 bytes) ahead of its
+      // key chunks, so the key chunks stay the newest loads in flight
+      if (wave == 0) {
+        const int i = min(k0 + l, kend - 1);
+        const float* g = a.k_scale + src.key(i);
+        uint8_t* d = tiles + C::RING * C::TILE_BYTES + (st_abs & (C::SCALE_RING - 1)) * C::KT * 4;
+        __builtin_amdgcn_global_load_lds((const void __attribute__((address_space(1)))*)g,
+                                         (void __attribute__((address_space(3)))*)d, 4, 0, 0);
+      }
+    }
 #pragma unroll
     for (int c = 0; c < C::CPT; ++c) {
       const int u0 = (c * C::WAVES + wave) * kWave;  // first chunk slot of this instruction
@@ -365,20 +393,19 @@ __device__ __forceinline__ void wg_scan(const ScoreArgs& a, const Src& src, int 
   auto scores = [&](int st, const float (&h0)[C::NIH], const float (&h1)[C::NIH], float (&sc)[C::NI]) {
     combine<C>(h0, h1, sc);
     if constexpr (C::DT == DT_FP8) {
-      const int k0 = kbeg + st * C::KT;
 #pragma unroll
       for (int it = 0; it < C::NI; ++it) {
         const int nt = h ? C::item_nt(it, 1) : C::item_nt(it, 0);
-        int pos = k0 + nt * 32 + r32;
-        pos = pos < kbeg ? kbeg : (pos < kend ? pos : kend - 1);
-        sc[it] *= a.k_scale[src.key(pos)];
+        const float* sl = reinterpret_cast<const float*>(tiles + C::RING * C::TILE_BYTES) +
+                          (st & (C::SCALE_RING - 1)) * C::KT;
+        sc[it] *= sl[nt * 32 + r32];
       }
     }
   };
 
-  stage(0, kbeg);
-  stage(1, kbeg + C::KT);
-  stage(2, kbeg + 2 * C::KT);
+  stage(0, 0, kbeg);
+  stage(1, 1, kbeg + C::KT);
+  stage(2, 2, kbeg + 2 * C::KT);
   sync_tiles(1);  // tiles 0 and 1 landed (tile 2 may still be in flight)
   Frag b0[C::KS], b1[C::KS];
   f32x16_t acc0[C::MT], acc1[C::MT];
@@ -392,7 +419,7 @@ __device__ __forceinline__ void wg_scan(const ScoreArgs& a, const Src& src, int 
     const uint8_t* tl = tiles + (st & (C::RING - 1)) * C::TILE_BYTES;
     const uint8_t* tn = tiles + ((st + 1) & (C::RING - 1)) * C::TILE_BYTES;
     // slot of tile st-1 is free: every wave passed the barrier after reading it
-    stage((st + 3) & (C::RING - 1), kbeg + (st + 3) * C::KT);
+    stage((st + 3) & (C::RING - 1), st + 3, kbeg + (st + 3) * C::KT);
     // half step A: MFMA sub-tile 0 of tile st || epilogue of sub-tile 1 of st-1,
     // B fragments of sub-tile 1 read as the slots free up
     mma_half<C>(wq, b0, acc0);
@@ -483,6 +510,7 @@ struct FusedSink {
   uint32_t tail[C::QW], above[C::QW];
   uint32_t* hist;     // LDS, [QW][m] for this wave
   int2* cand;
+  int2* crow[C::QW];  // this split's candidate list of each query
   int qbase, nq, S, split, cap, m, k;
 
   __device__ void set_tau(int q, int t) {
@@ -507,6 +535,7 @@ struct FusedSink {
         t0 = p.tau0;
       }
       e[q] = ev < kend ? ev : kend;
+      crow[q] = cand + ((int64_t)(t < nq ? t : 0) * S + split) * cap;
       delta[q] = dl;
       cc[q] = c;
       set_tau(q, t0);
@@ -555,10 +584,10 @@ struct FusedSink {
       if (pass) {
         const int key = k0 + (h ? nb : na) * 32 + r32;
         const int q = h ? qb : qa;
-        if (pos < (uint32_t)cap)
-          cand[((int64_t)(qbase + q) * S + split) * cap + pos] = make_int2(key, __float_as_int(sc[it]));
-        const int b = bin_of(x[it], m);
-        if (b >= 0) atomicAdd(&hist[q * m + b], 1u);
+        if (pos < (uint32_t)cap) crow[q][pos] = make_int2(key, __float_as_int(sc[it]));
+        // bin_of without branches: x >= 0 excludes NaN and the below-range scores
+        const float xv = x[it];
+        if (xv >= 0.0f) lds_inc(&hist[q * m + min(__float2int_rz(xv), m - 1)]);
       }
     });
 #pragma unroll
@@ -622,7 +651,7 @@ __global__ __launch_bounds__(C::NTHREADS) void k_fused(ScoreArgs a, const RowPar
                                                        int m, int k, uint32_t* cnt,
                                                        uint32_t* hist_out, int2* cand) {
   extern __shared__ __align__(16) uint8_t lds[];
-  uint32_t* hist = reinterpret_cast<uint32_t*>(lds + C::RING * C::TILE_BYTES);
+  uint32_t* hist = reinterpret_cast<uint32_t*>(lds + C::SCAN_LDS);
   int* emax = reinterpret_cast<int*>(hist + C::QT * m);
   const int tile = blockIdx.x / S, split = blockIdx.x - tile * S;
   const int q0 = tile * C::QT, wave = threadIdx.x / kWave, qbase = q0 + wave * C::QW;
@@ -713,7 +742,7 @@ ScoreShape score_shape(int dtype, int mode, int h, int d) {
     s.queries_per_block = C::QT;
     s.keys_per_step = C::KT;
     s.threads = C::NTHREADS;
-    s.scan_lds = C::RING * C::TILE_BYTES;
+    s.scan_lds = C::SCAN_LDS;
   });
   return s;
 }
@@ -736,7 +765,7 @@ hipError_t launch_sample_scores(const ScoreArgs& a, const int32_t* list, int ns,
       err = hipSuccess;
       return;
     }
-    hipLaunchKernelGGL(k_sample<C>, grid, dim3(C::NTHREADS), C::RING * C::TILE_BYTES, st, a, list, ns, samp, slice);
+    hipLaunchKernelGGL(k_sample<C>, grid, dim3(C::NTHREADS), C::SCAN_LDS, st, a, list, ns, samp, slice);
     err = hipGetLastError();
   });
   return err;
@@ -750,7 +779,7 @@ hipError_t launch_dense_scores(const ScoreArgs& a, float* out, int64_t ld, hipSt
       err = hipSuccess;
       return;
     }
-    hipLaunchKernelGGL(k_dense<C>, grid, dim3(C::NTHREADS), C::RING * C::TILE_BYTES, st, a, out, ld, kSlice);
+    hipLaunchKernelGGL(k_dense<C>, grid, dim3(C::NTHREADS), C::SCAN_LDS, st, a, out, ld, kSlice);
     err = hipGetLastError();
   });
   return err;
@@ -765,7 +794,7 @@ hipError_t launch_fused_scan(const ScoreArgs& a, const RowParam* params, int S, 
       err = hipSuccess;
       return;
     }
-    const size_t lds = C::RING * C::TILE_BYTES + (size_t)C::QT * m * 4 + 16;
+    const size_t lds = C::SCAN_LDS + (size_t)C::QT * m * 4 + 16;
     if (lds > 65536)
       (void)hipFuncSetAttribute((const void*)k_fused<C>, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
     hipLaunchKernelGGL(k_fused<C>, dim3(tiles * S), dim3(C::NTHREADS), lds, st, a, params, S, L, cap, m, k,
@@ -780,7 +809,7 @@ hipError_t launch_fused_fallback(const ScoreArgs& a, int k, uint32_t flags, cons
                                  hipStream_t st) {
   hipError_t err = hipErrorInvalidValue;
   with_cfg(a.dtype, a.mode, a.h, a.d, [&]<class C>() {
-    size_t lds = C::RING * C::TILE_BYTES;
+    size_t lds = C::SCAN_LDS;
     const size_t rl = radix_lds_bytes(k);
     if (rl > lds) lds = rl;
     if (lds > 65536)
