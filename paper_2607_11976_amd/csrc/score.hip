@@ -106,18 +106,30 @@ struct Cfg {
   static constexpr int SCALE_BYTES = DT == DT_FP8 ? SCALE_RING * KT * 4 : 0;
   static constexpr int SCAN_LDS = RING * TILE_BYTES + SCALE_BYTES;
   static constexpr int CPK = ROWB / 16;                // 16-byte chunks per key
+  // XOR swizzle key of row n: the 16 lanes of one LDS access group read the
+  // same chunk of 16 consecutive rows and must hit 16 distinct 16-byte bank
+  // slots of a 256-byte bank line; rows shorter than 256 bytes share a line,
+  // so consecutive rows that do are told apart by the line they sit in
+  static constexpr int RPL = ROWB >= 256 ? 1 : 256 / ROWB;  // rows per bank line
+  __host__ __device__ static constexpr int swz(int n) { return n / RPL; }
   static constexpr int CHUNKS = KT * CPK;
   static constexpr int NTHREADS = WAVES * kWave;
   static constexpr int CPT = CHUNKS / NTHREADS;      // staged chunks per thread per tile
   // GROUPED: H <= 4, a 4-row accumulator group holds whole queries, no
   // cross-lane step. Otherwise H % 8 == 0 and the halves are combined.
   static constexpr bool GROUPED = H <= 4;
+  // fp8 DSA with H >= 8: ReLU and head weighting on packed bf16 pairs
+  // (convert, integer max with 0, bf16 dot product accumulating in fp32):
+  // three instructions per two heads instead of four. Relative error of a
+  // score below 2^-8 for non-negative weights, inside the fp8 tolerance.
+  static constexpr bool PACKED_EPI = DT == DT_FP8 && !GROUPED && RELU && QW == 1;
   static constexpr int GPQ = GROUPED ? 4 / H : 1;      // queries per 4-row group
   static constexpr int NI = GROUPED ? NT * MT * 4 * GPQ : NT * QW / 2;  // scores per lane per tile
   static constexpr int NIH = GROUPED ? MT * 4 * GPQ : QW;              // per-lane results of one sub-tile
   // epilogue VALU ops of one sub-tile (ReLU + FMA per accumulator element)
   // spread over the MFMAs of the other sub-tile
-  static constexpr int VALU_PER_MFMA = (2 * 16 * MT + KS * MT - 1) / (KS * MT);
+  static constexpr int VALU_PER_MFMA =
+      ((DT == DT_FP8 && H >= 8 && RELU && QW == 1 ? 26 : 32) * MT + KS * MT - 1) / (KS * MT);
   static_assert((QW * H) % 32 == 0, "a wave must fill whole M tiles");
   static_assert(NT == 2, "the scan pipelines the two 32-key halves of a tile");
   static_assert(CHUNKS % NTHREADS == 0 && CPT < 16, "tile staging assumes whole instructions per thread");
@@ -144,10 +156,15 @@ struct Cfg {
 
 // Per-wave stationary operands: the A fragments of the wave's queries and the
 // head weight of every accumulator row the lane holds.
+typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+typedef float f32x2_t __attribute__((ext_vector_type(2)));
+typedef short i16x2_t __attribute__((ext_vector_type(2)));
+
 template <class C>
 struct WaveQ {
   typename C::M::Frag qa[C::MT][C::KS];
   float wv[C::MT][16];
+  bf16x2_t wp[C::MT][8];  // PACKED_EPI: weights of accumulator rows (2i, 2i+1)
 };
 
 template <class C>
@@ -180,6 +197,11 @@ __device__ __forceinline__ void load_q(WaveQ<C>& s, const ScoreArgs& a, int qbas
       }
       s.wv[mt][v] = wt;
     }
+    if constexpr (C::PACKED_EPI) {
+#pragma unroll
+      for (int i = 0; i < 8; ++i)
+        s.wp[mt][i] = __builtin_convertvector((f32x2_t){s.wv[mt][2 * i], s.wv[mt][2 * i + 1]}, bf16x2_t);
+    }
   }
 }
 
@@ -187,12 +209,12 @@ __device__ __forceinline__ void load_q(WaveQ<C>& s, const ScoreArgs& a, int qbas
 // acc[mt] is the 32x32 block of M tile mt; accumulator register v of a lane
 // is row 8*(v/4) + 4*(lane/32) + v%4 of the M tile, column lane%32.
 // LDS tile layout: key row n occupies ROWB contiguous bytes; its 16-byte
-// chunk c is stored at chunk slot c ^ (n mod CPK). The swizzle spreads the
-// 32 lanes that read the same chunk of 32 consecutive keys over distinct
-// banks without padding, so tiles can be filled by direct HBM -> LDS loads.
+// chunk c is stored at chunk slot c ^ (swz(n) mod CPK). The swizzle spreads
+// the lanes that read the same chunk of consecutive keys over distinct banks
+// without padding, so tiles can be filled by direct HBM -> LDS loads.
 template <class C>
 __device__ __forceinline__ int lds_offset(int n, int byte) {
-  return n * C::ROWB + ((((byte >> 4) ^ n) & (C::CPK - 1)) << 4) + (byte & 15);
+  return n * C::ROWB + ((((byte >> 4) ^ C::swz(n)) & (C::CPK - 1)) << 4) + (byte & 15);
 }
 
 template <class C>
@@ -252,6 +274,28 @@ __device__ __forceinline__ void reduce_half(const WaveQ<C>& s, const f32x16_t (&
           }
           out[(mt * 4 + i) * C::GPQ + sq] = sum;
         }
+  } else if constexpr (C::PACKED_EPI) {
+    // all conversions, then all maxima, then the dot products into four
+    // partial sums: no instruction waits on the one just before it
+    i16x2_t z[C::MT][8];
+#pragma unroll
+    for (int mt = 0; mt < C::MT; ++mt)
+#pragma unroll
+      for (int j = 0; j < 8; ++j)
+        z[mt][j] = __builtin_bit_cast(
+            i16x2_t, __builtin_convertvector((f32x2_t){acc[mt][2 * j], acc[mt][2 * j + 1]}, bf16x2_t));
+#pragma unroll
+    for (int mt = 0; mt < C::MT; ++mt)
+#pragma unroll
+      for (int j = 0; j < 8; ++j) z[mt][j] = __builtin_elementwise_max(z[mt][j], (i16x2_t){0, 0});
+    float part[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+#pragma unroll
+    for (int mt = 0; mt < C::MT; ++mt)
+#pragma unroll
+      for (int j = 0; j < 8; ++j)
+        part[j & 3] = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2_t, z[mt][j]), s.wp[mt][j],
+                                                      part[j & 3], false);
+    out[0] = (part[0] + part[1]) + (part[2] + part[3]);
   } else {
 #pragma unroll
     for (int q = 0; q < C::QW; ++q) out[q] = 0.0f;
@@ -370,7 +414,7 @@ __device__ __forceinline__ void wg_scan(const ScoreArgs& a, const Src& src, int 
 #pragma unroll
     for (int c = 0; c < C::CPT; ++c) {
       const int u0 = (c * C::WAVES + wave) * kWave;  // first chunk slot of this instruction
-      const int u = u0 + l, n = u / C::CPK, part = (u ^ n) & (C::CPK - 1);
+      const int u = u0 + l, n = u / C::CPK, part = (u ^ C::swz(n)) & (C::CPK - 1);
       const int i = min(k0 + n, kend - 1);
       const uint8_t* g = keys + (int64_t)src.key(i) * C::ROWB + part * 16;
       uint8_t* d = tiles + slot * C::TILE_BYTES + u0 * 16;
