@@ -40,11 +40,15 @@ from paper_2607_11976_amd import workloads  # noqa: E402
 METRIC = "query-key pairs scored+selected/s at 128K/1M ctx; % MFMA & HBM roofline"
 PEAK_TFLOPS = {"bf16": 2500.0, "fp8": 5000.0, "f32": 157.3}
 HBM_PEAK_GBS = 8000.0
-# FETCH_SIZE / WRITE_SIZE of the fused scan kernel (KiB per dispatch, from
-# rocprofv3 --pmc runs of this benchmark) and the counter/actual-byte factor
-# of a plain device copy measured the same way. None until measured.
-TRAFFIC_KIB = {"dsa_bf16_128k": None}
-COPY_FACTOR = None
+# FETCH_SIZE / WRITE_SIZE of the fused scan kernel (KiB per dispatch, mean of
+# two dispatches, from `rocprofv3 --pmc FETCH_SIZE` and `--pmc WRITE_SIZE` runs
+# of `bench.py --profile-only <workload> --steps 2`), and what the same two
+# counters read per byte actually moved by a plain 1 GiB device copy
+# (`bench.py --copy-calib 1024 --steps 3`): FETCH_SIZE reads half the bytes,
+# WRITE_SIZE all of them. A kernel change since these were taken makes them
+# stale: set the entry to None until they are taken again.
+TRAFFIC_KIB = {"dsa_bf16_128k": (293450.7, 281896.0), "dsa_fp8_1m": (549479.8, 209533.7)}
+COPY_FACTOR = (0.5000, 1.0000)
 
 
 def visible_pairs(cfg) -> int:
@@ -189,7 +193,7 @@ def roofline(cfg, res):
     traffic = None
     kib = TRAFFIC_KIB.get(cfg.name)
     if kib is not None and COPY_FACTOR is not None:
-        traffic = (kib[0] + kib[1]) * 1024.0 / COPY_FACTOR
+        traffic = round(kib[0] * 1024.0 / COPY_FACTOR[0] + kib[1] * 1024.0 / COPY_FACTOR[1])
     return {"bound": "mfma", "achieved": round(achieved, 2), "peak": peak, "unit": "TFLOP/s",
             "frac": round(achieved / peak, 4), "traffic": traffic, "kernel": "k_fused (score+filter scan)",
             "kernel_ms": round(filt_ms, 4), "algorithmic_flops": flops}
@@ -222,10 +226,14 @@ def cpu_oracle_rate(name: str, budget_s: float):
         orc.indexer_topk(qn, cfg.dtype, qs, wn, kn, ks, cfg.k, cfg.mode, offs, rows=rows)
         return time.perf_counter() - t0
 
-    probe = [0, cfg.nq - 1]
-    t = run(probe)
-    per_row = max(t / len(probe), 1e-3)
-    n = int(min(cfg.nq, max(4, budget_s / per_row)))
+    # per-row cost from two probe sizes (each call also dequantises every key
+    # once); a first call warms the BLAS thread pool and is not counted
+    run([0])
+    t1 = run([0, cfg.nq - 1])
+    t2 = run(np.linspace(0, cfg.nq - 1, 10).round().astype(int).tolist())
+    per_row = max((t2 - t1) / 8.0, 1e-4)
+    fixed = max(t1 - 2 * per_row, 0.0)
+    n = int(min(cfg.nq, max(4, (budget_s - fixed) / per_row)))
     rows = np.unique(np.linspace(0, cfg.nq - 1, n).round().astype(int)).tolist()
     t = run(rows)
     pr = float(e[rows].sum())
