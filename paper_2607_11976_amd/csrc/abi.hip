@@ -16,6 +16,7 @@ constexpr int kFallbackGridFused = 64;      // rows re-scored concurrently (scra
 constexpr int kFallbackGridScores = 256;
 constexpr int kTargetBlocks = 256;          // one block per CU before key splitting stops
 constexpr int kMinSplitKeys = 4096;         // shortest key split the automatic choice makes
+constexpr int kMaxAutoSplits = 64;
 constexpr size_t kHistLdsBudget = 96 * 1024;
 constexpr size_t kLdsPerBlock = 160 * 1024;   // gfx950 LDS per workgroup
 constexpr int kSampleBlockScores = 64;      // scores-in sample: runs of 64 consecutive keys
@@ -107,12 +108,18 @@ Resolved resolve_fused(const lt_options* o, int nq, int nk, int k, int mode, con
   if (o->key_splits > 0) {
     S = std::min(o->key_splits, std::max(steps, 1));
   } else {
-    // Split the key range while the GPU is not yet full (one block per CU)
-    // and every split keeps at least kMinSplitKeys keys. Each split tightens
-    // its threshold only from its own histogram, so a split adds survivors
-    // when the initial threshold is loose; a short launch that fills one
-    // CU in eight loses far more.
-    while ((long long)tiles * S < kTargetBlocks && (long long)nk / (2 * S) >= kMinSplitKeys) S *= 2;
+    // The fewest key splits whose launch keeps at least 90% of the block
+    // slots busy in its last round (one block per CU), each split keeping at
+    // least kMinSplitKeys keys. Each split tightens its threshold only from
+    // its own histogram, so a split adds survivors when the initial threshold
+    // is loose; a launch that leaves most CUs idle loses far more.
+    const int smax = std::max(1, std::min(kMaxAutoSplits, nk / kMinSplitKeys));
+    for (int s = 1; s <= smax; ++s) {
+      const long long blocks = (long long)tiles * s;
+      const long long rounds = (blocks + kTargetBlocks - 1) / kTargetBlocks;
+      S = s;
+      if (blocks * 10 >= rounds * kTargetBlocks * 9) break;
+    }
   }
   r.S = S;
   const int per = (nk + S - 1) / S;

@@ -17,6 +17,8 @@
 // 32-lane halves, arranged so that after it every lane holds a full score.
 #include <utility>
 
+#include <type_traits>
+
 #include "internal.hpp"
 #include "select_dev.hpp"
 
@@ -363,6 +365,18 @@ __device__ __forceinline__ void schedule_half() {
 // compiler cannot tell the histogram from the tile ring): LDS operations of
 // one wave complete in order, so the wave's later histogram reads still see
 // the increment, and no other wave reads this wave's histogram rows.
+// OR of a 32-bit value over the wave: inclusive scans in rows of 16 lanes,
+// then across rows (row_bcast); lane 63 ends with the total.
+__device__ __forceinline__ uint32_t wave_or(uint32_t v) {
+  v |= (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x111, 0xF, 0xF, false);  // row_shr:1
+  v |= (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x112, 0xF, 0xF, false);  // row_shr:2
+  v |= (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x114, 0xF, 0xF, false);  // row_shr:4
+  v |= (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x118, 0xF, 0xF, false);  // row_shr:8
+  v |= (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x142, 0xA, 0xF, false);  // row_bcast:15
+  v |= (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x143, 0xC, 0xF, false);  // row_bcast:31
+  return (uint32_t)__builtin_amdgcn_readlane((int)v, 63);
+}
+
 __device__ __forceinline__ void lds_inc(uint32_t* p) {
   const uint32_t a = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) uint32_t*)p;
   asm volatile("ds_add_u32 %0, %1" ::"v"(a), "v"(1u) : "memory");
@@ -664,6 +678,197 @@ struct FusedSink {
   }
 };
 
+// The fused filter for layouts where a lane holds whole scores of many queries
+// (H <= 4: up to 32 queries per wave, 32 scores per lane per tile, e.g. the
+// one-head inner-product retrieval scorer). The per-query state lives one
+// query per lane (lane q holds query q's range, bin map, threshold, list
+// tail and count above the threshold), read with readlane and written by a
+// lane select, so it costs a handful of registers instead of QW of each.
+// Gate in the score domain: bin(fma(I, delta, c)) >= tau holds for every
+// I >= (tau - c) / delta (real division; fma rounding is monotone and tau is
+// a float), so the lane compares each score with T, that quotient lowered by
+// far more than its float rounding error: one compare per score, never
+// dropping a key whose bin is >= tau. A key let through just below the bin
+// edge is written and counted in its true (lower) bin, which changes neither
+// the refresh (it only reads bins above tau) nor the final select (it keeps
+// bins >= the final threshold, whose counts stay complete). Scores that pass
+// the compare are re-checked against the causal end of their row before they
+// are written. NaN passes the compare (as in the bin gate) and is never
+// counted.
+template <class C>
+struct GroupedSink {
+  static_assert(C::GROUPED && C::QW <= kWave, "one query per lane");
+  // lane q: state of query qbase + q
+  float delta_v, c_v, t_v;
+  int tau_v, e_v;
+  uint32_t tail_v, above_v;
+  float tq[C::NIH];   // T of the query of item j (items j and j + NIH share it)
+  bool ungated;       // some row of the wave has no gate (tau = -1)
+  uint32_t* hist;     // LDS, [QW][m] for this wave
+  int2* cand;
+  int qbase, nq, S, split, cap, m, k;
+
+  // value `val` into lane q of a per-lane register
+  template <typename T>
+  __device__ static T set_lane(T v, int q, T val) {
+    return lane_id() == q ? val : v;
+  }
+
+  __device__ static float gate_floor(float delta, float c, int tau) {
+    if (tau < 0) return -__builtin_inff();
+    const float t = (float)tau, i0 = (t - c) / delta;
+    const float err = ((fabsf(t) + fabsf(c)) / delta + fabsf(i0)) * 0x1p-20f;
+    return i0 - err;
+  }
+
+  __device__ void refresh_items() {
+    const int h = lane_id() >> 5;
+    static_for<C::NIH>([&](auto J) {
+      constexpr int j = decltype(J)::value;
+      constexpr int qa = C::item_q(j, 0), qb = C::item_q(j, 1);
+      const float a = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, t_v), qa));
+      const float b = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, t_v), qb));
+      tq[j] = h ? b : a;
+    });
+  }
+
+  __device__ void init(const ScoreArgs& a, const RowParam* params, int kend) {
+    const int l = lane_id(), t = qbase + l;
+    int ev = 0;
+    float dl = 1.0f, c = 0.0f;
+    int t0 = -1;
+    if (l < C::QW && t < nq) {
+      ev = a.offs ? a.offs[t] : a.nk;
+      ev = ev < 0 ? 0 : (ev > a.nk ? a.nk : ev);
+      const RowParam p = params[t];
+      dl = p.delta;
+      c = p.c;
+      t0 = p.tau0;
+    }
+    e_v = ev < kend ? ev : kend;
+    delta_v = dl;
+    c_v = c;
+    tau_v = t0;
+    tail_v = 0;
+    above_v = 0;
+    update_gates();
+  }
+
+  // T of every row (+inf for rows past the end: they never pass), the
+  // ungated flag, and the per-item copies
+  __device__ void update_gates() {
+    const int l = lane_id();
+    const bool valid = l < C::QW && qbase + l < nq;
+    t_v = valid ? gate_floor(delta_v, c_v, tau_v) : __builtin_inff();
+    ungated = __ballot(valid && tau_v < 0) != 0;
+    refresh_items();
+  }
+
+  // Query of item it in lane half h, with a run-time item index.
+  __device__ static int item_query(int it, int h) {
+    const int s = it % C::GPQ, g = it / C::GPQ, i = g % 4, mt = (g / 4) % C::MT;
+    return (32 * mt + 8 * i + 4 * h + s * C::H) / C::H;
+  }
+
+  __device__ void consume(int, int k0, int, const float (&sc)[C::NI], bool live) {
+    if (!live) return;
+    static_assert(C::NI <= 32, "one bit per item");
+    typedef float fNI __attribute__((ext_vector_type(C::NI)));
+    typedef float fNIH __attribute__((ext_vector_type(C::NIH)));
+    const int l = lane_id(), h = l >> 5, r32 = l & 31;
+    // fast path, vector ALU only (a chain of per-item ballots would stall on
+    // every scalar read of a compare result): the largest margin score - T
+    // over the lane's items; T - T' < 0 for every non-NaN score below its T.
+    // A NaN score only matters to an ungated row, and then the fast path is
+    // skipped.
+    if (!ungated) {
+      float mx = -__builtin_inff();
+#pragma unroll
+      for (int it = 0; it < C::NI; ++it) mx = fmaxf(mx, sc[it] - tq[it % C::NIH]);
+      if (__ballot(mx >= 0.0f) == 0) return;  // wave-uniform: nothing passes
+    }
+    // bit it of `items` = some lane's score of item it passed
+    uint32_t bits = 0;
+#pragma unroll
+    for (int it = 0; it < C::NI; ++it) bits |= !(sc[it] < tq[it % C::NIH]) ? (1u << it) : 0u;
+    const uint32_t items = wave_or(bits);
+    if (items == 0) return;
+    // slow path, one item at a time (a run-time loop keeps the code small)
+    fNI scv;
+    fNIH tqv;
+#pragma unroll
+    for (int it = 0; it < C::NI; ++it) scv[it] = sc[it];
+#pragma unroll
+    for (int j = 0; j < C::NIH; ++j) tqv[j] = tq[j];
+    for (uint32_t rem = items; rem; rem &= rem - 1) {
+      const int it = __builtin_ctz(rem);
+      const int j = it % C::NIH, nt = it / C::NIH;
+      const int qa = item_query(j, 0), qb = item_query(j, 1);
+      const float s_it = scv[it];
+      const int key = k0 + nt * 32 + r32;
+      const int ea = __builtin_amdgcn_readlane(e_v, qa), eb = __builtin_amdgcn_readlane(e_v, qb);
+      const bool pass = !(s_it < tqv[j]) && key < (h ? eb : ea);
+      const uint64_t m2 = __ballot(pass);
+      if (m2 == 0) continue;
+      const uint32_t lo = (uint32_t)__popcll(m2 & 0xFFFFFFFFull), hi = (uint32_t)__popcll(m2) - lo;
+      const uint32_t ta = (uint32_t)__builtin_amdgcn_readlane((int)tail_v, qa);
+      const uint32_t tb = (uint32_t)__builtin_amdgcn_readlane((int)tail_v, qb);
+      const int q = h ? qb : qa;
+      // (readlane takes a wave-uniform lane: read both queries, then select)
+      const float da = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, delta_v), qa));
+      const float db = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, delta_v), qb));
+      const float ca = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, c_v), qa));
+      const float cb = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, c_v), qb));
+      const int ua = __builtin_amdgcn_readlane(tau_v, qa), ub = __builtin_amdgcn_readlane(tau_v, qb);
+      const float x = fmaf(s_it, h ? db : da, h ? cb : ca);
+      if (pass) {
+        const uint32_t pos = h ? tb + mbcnt64(m2) - lo : ta + mbcnt64(m2);
+        if (pos < (uint32_t)cap)
+          cand[((int64_t)(qbase + q) * S + split) * cap + pos] = make_int2(key, __float_as_int(s_it));
+        if (x >= 0.0f) lds_inc(&hist[q * m + min(__float2int_rz(x), m - 1)]);
+      }
+      // counted candidates strictly above the query's threshold bin
+      const uint64_t up = __ballot(pass && x >= (float)((h ? ub : ua) + 1));
+      const uint32_t ulo = (uint32_t)__popcll(up & 0xFFFFFFFFull), uhi = (uint32_t)__popcll(up) - ulo;
+      tail_v = set_lane(tail_v, qa, ta + lo);
+      tail_v = set_lane(tail_v, qb, tb + hi);
+      const uint32_t aa = (uint32_t)__builtin_amdgcn_readlane((int)above_v, qa);
+      const uint32_t ab = (uint32_t)__builtin_amdgcn_readlane((int)above_v, qb);
+      above_v = set_lane(above_v, qa, aa + ulo);
+      above_v = set_lane(above_v, qb, ab + uhi);
+    }
+    // threshold refresh of every query whose count above tau reached k
+    uint64_t adv = __ballot(l < C::QW && above_v >= (uint32_t)k && tau_v < m - 1);
+    if (adv == 0) return;
+    __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "wavefront");
+    while (adv) {
+      const int q = __builtin_ctzll(adv);
+      adv &= adv - 1;
+      int t = __builtin_amdgcn_readlane(tau_v, q);
+      uint32_t ab = (uint32_t)__builtin_amdgcn_readlane((int)above_v, q);
+      while (ab >= (uint32_t)k && t < m - 1) {
+        ++t;
+        ab -= hist[q * m + t];
+      }
+      tau_v = set_lane(tau_v, q, t);
+      above_v = set_lane(above_v, q, ab);
+    }
+    update_gates();
+  }
+
+  __device__ void finish(uint32_t* cnt, uint32_t* hist_out) {
+    __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "wavefront");
+    const int l = lane_id();
+    for (int q = 0; q < C::QW; ++q) {
+      const int t = qbase + q;
+      if (t >= nq) break;
+      const int64_t u = (int64_t)t * S + split;
+      for (int b = l; b < m; b += kWave) hist_out[u * m + b] = hist[q * m + b];
+    }
+    if (l < C::QW && qbase + l < nq) cnt[(int64_t)(qbase + l) * S + split] = tail_v;
+  }
+};
+
 // ---------------------------------------------------------------------------
 // Kernels
 // ---------------------------------------------------------------------------
@@ -712,7 +917,7 @@ __global__ __launch_bounds__(C::NTHREADS) void k_fused(ScoreArgs a, const RowPar
   const int ke = min(min(kb + L, a.nk), *emax);
   WaveQ<C> wq;
   load_q<C>(wq, a, qbase);
-  FusedSink<C> sink;
+  std::conditional_t<C::GROUPED, GroupedSink<C>, FusedSink<C>> sink;
   sink.hist = hist + wave * C::QW * m;
   sink.cand = cand;
   sink.qbase = qbase;
@@ -762,8 +967,8 @@ __global__ __launch_bounds__(C::NTHREADS) void k_fused_fallback(ScoreArgs a, int
   X(DT_F32, 1, 64, 32, 2, 4, false)      \
   X(DT_BF16, 64, 128, 1, 2, 8, true)     \
   X(DT_BF16, 4, 128, 8, 2, 4, true)      \
-  X(DT_BF16, 1, 128, 32, 2, 4, true)     \
-  X(DT_BF16, 1, 128, 32, 2, 4, false)    \
+  X(DT_BF16, 1, 128, 32, 2, 8, true)     \
+  X(DT_BF16, 1, 128, 32, 2, 8, false)    \
   X(DT_FP8, 64, 128, 1, 2, 8, true)
 
 template <class F>
