@@ -14,6 +14,8 @@ fallback, inputs resident in HBM. Prints ONE JSON line with
   cpu_baseline   the CPU oracle timed on an evenly spaced sample of rows;
   unfused        the materialising baseline (dense scores + radix select);
   ctx_1m         the same measurement for the 2048 x 1M fp8 workload;
+  dsa_union      LiteDSA's group union + membership masks (sec. 3.3) of the
+                 timed workload's top-k lists, groups of 4 / 8 / 16 queries;
   chunked_prefill  the same 4096 queries processed in chunks (sec. 4.2's
                  chunked-prefill protocol), with a random sample per chunk and
                  with the sample taken from the previous chunk's top-k
@@ -111,6 +113,18 @@ def measure(name: str, steps: int, warmup: int, unfused: bool):
     res = dict(ms=ms, pairs=pairs, stages=stages, survivors_mean=float(st[:, 0].mean()),
                survivors_max=int(st[:, 0].max()), fallback_rows=int((st[:, 2] != 0).sum()),
                tie_bin_mean=float(st[:, 3].mean()))
+
+    # LiteDSA union of the top-k lists over groups of neighbouring queries
+    # (sec. 3.3): time per call and union size relative to group * k
+    res["dsa_union"] = []
+    for group in (4, 8, 16):
+        if group * k > lt.LT_UNION_MAX:
+            continue
+        u = lt.dsa_union(out[0], group)
+        torch.cuda.synchronize()
+        ums = timed_steps(lambda: lt.dsa_union(out[0], group), 5, 1)
+        res["dsa_union"].append({"group": group, "ms": round(ums, 4),
+                                 "union_over_group_k": round(float(u[1].float().mean()) / (group * k), 4)})
 
     if unfused:
         dense = torch.empty((nq, nk), dtype=torch.float32, device=dev)
@@ -312,6 +326,7 @@ def main():
         "survivors_per_row": {"mean": round(res["survivors_mean"], 1), "max": res["survivors_max"],
                               "threshold_bin_mean": round(res["tie_bin_mean"], 1)},
         "fallback_rows": res["fallback_rows"],
+        "dsa_union": res["dsa_union"],
         "bytes_written_per_query": {
             "fused": round(res["survivors_mean"] * 8 + cfg.k * 8, 1),
             "unfused": cfg.nk * 4 + cfg.k * 8},

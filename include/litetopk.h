@@ -52,6 +52,7 @@ extern "C" {
 #define LT_K_MAX 8192         /* largest k (the paper's largest, sec. 4.1 retrieval) */
 #define LT_MAX_BINS 256
 #define LT_SAMPLE_LIST_MAX 32768  /* longest caller-supplied sample list */
+#define LT_UNION_MAX 32768        /* largest group * k for lt_dsa_union */
 
 /* ---- enums --------------------------------------------------------------- */
 typedef enum {
@@ -211,6 +212,27 @@ size_t lt_sample_from_topk_workspace_size(int32_t num_keys);
 int lt_sample_from_topk(const int32_t* prev_idx, int64_t ld, int32_t prev_rows, int32_t prev_k,
                         int32_t num_keys, int32_t sample_size, int32_t* sample_keys, void* workspace,
                         size_t workspace_bytes, void* stream);
+
+/* ---- LiteDSA union and membership masks (sec. 3.3) ------------------------ */
+
+/* For each group of `group` consecutive queries (the last group may be
+   shorter), the union of their top-k key lists as one ascending list of
+   distinct keys shared by the group, and for every query a bitmask over the
+   union's slots marking the keys of its own top-k (the per-query membership
+   mask LiteDSA's attention ANDs with each row, sec. 3.3).
+   topk_idx     DEVICE int32, query t's list at topk_idx[t * ld + j], j < k
+                (ld >= k); negative entries (the -1 padding) are not keys;
+                repeated keys in one list count once.
+   union_idx    DEVICE int32 [ceil(num_queries / group), group * k]: row g
+                holds group g's union ascending, then -1.
+   union_count  DEVICE int32 [ceil(num_queries / group)]: union sizes.
+   member_mask  DEVICE uint32 [num_queries, W], W = ceil(group * k / 32):
+                bit (j % 32) of word j / 32 of row t is set iff union slot j
+                of t's group holds a key of t's list; bits past the union
+                size are 0.
+   Limits: 1 <= group, 1 <= k, group * k <= LT_UNION_MAX. No workspace. */
+int lt_dsa_union(const int32_t* topk_idx, int64_t ld, int32_t num_queries, int32_t k, int32_t group,
+                 int32_t* union_idx, int32_t* union_count, uint32_t* member_mask, void* stream);
 
 /* ---- timing helpers ------------------------------------------------------- */
 

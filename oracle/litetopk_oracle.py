@@ -38,6 +38,12 @@ buffers): those cannot change an exact top-k, so the oracle leaves them out.
   happens when fewer than k' distinct keys occur; the oracle takes equal
   counts in ascending key order and returns only keys that occur at least
   once (then padding -1), listed in ascending key order.
+* LiteDSA union and membership masks -- sec. 3.3: a group of consecutive
+  queries attends over the union of their top-k keys, one shared list, and
+  each query keeps a bitmask over that list marking its own keys. The oracle
+  takes the union as a set, lists it ascending (the order the paper's bitmap
+  sweep produces), and sets bit j of a query's mask iff the union's j-th key
+  is in that query's list.
 """
 from __future__ import annotations
 
@@ -220,3 +226,32 @@ def sample_from_topk(prev_idx: np.ndarray, num_keys: int, sample_size: int) -> n
     out = np.full(sample_size, -1, dtype=np.int32)
     out[: chosen.size] = chosen
     return out
+
+
+def dsa_union(topk_idx: np.ndarray, group: int):
+    """LiteDSA union, sec. 3.3. topk_idx [Nq, k] (negative entries are
+    padding). For each group of ``group`` consecutive rows (the last may be
+    shorter): the ascending list of distinct keys in any of its rows, and per
+    row the slots of that list holding the row's keys. Returns (union_idx
+    [G, group * k] int32 padded with -1, union_count [G] int32, member_mask
+    [Nq, W] uint32 with W = ceil(group * k / 32), bit j % 32 of word j // 32
+    for slot j)."""
+    idx = np.asarray(topk_idx, dtype=np.int64)
+    nq, k = idx.shape
+    n = group * k
+    ngroups = -(-nq // group)
+    words = -(-n // 32)
+    union_idx = np.full((ngroups, n), -1, dtype=np.int32)
+    union_count = np.zeros(ngroups, dtype=np.int32)
+    mask = np.zeros((nq, words), dtype=np.uint32)
+    for g in range(ngroups):
+        rows = range(g * group, min(nq, (g + 1) * group))
+        keys = sorted({int(v) for t in rows for v in idx[t] if v >= 0})
+        union_idx[g, : len(keys)] = keys
+        union_count[g] = len(keys)
+        slot = {key: j for j, key in enumerate(keys)}
+        for t in rows:
+            for v in {int(v) for v in idx[t] if v >= 0}:
+                j = slot[v]
+                mask[t, j // 32] |= np.uint32(1 << (j % 32))
+    return union_idx, union_count, mask

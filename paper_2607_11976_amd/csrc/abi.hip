@@ -357,6 +357,16 @@ int lt_sample_from_topk(const int32_t* prev, int64_t ld, int32_t rows, int32_t p
   return hip_status(launch_sample_from_topk(prev, ld, rows, pk, nk, ns, out, workspace, (hipStream_t)stream));
 }
 
+int lt_dsa_union(const int32_t* idx, int64_t ld, int32_t nq, int32_t k, int32_t group, int32_t* union_idx,
+                 int32_t* union_count, uint32_t* member_mask, void* stream) {
+  if (nq < 0 || k < 1 || group < 1 || ld < k) return LT_EINVAL;
+  if ((int64_t)group * k > LT_UNION_MAX) return LT_EINVAL;
+  if (nq == 0) return LT_OK;
+  if (!idx || !union_idx || !union_count || !member_mask) return LT_EINVAL;
+  return hip_status(launch_dsa_union(idx, ld, nq, k, group, union_idx, union_count, member_mask,
+                                     (hipStream_t)stream));
+}
+
 int lt_event_create(void** ev) {
   if (!ev) return LT_EINVAL;
   hipEvent_t e;

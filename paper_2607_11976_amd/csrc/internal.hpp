@@ -39,6 +39,11 @@ size_t freq_workspace_bytes(int nk);
 hipError_t launch_sample_from_topk(const int32_t* prev, int64_t ld, int rows, int pk, int nk, int ns,
                                    int32_t* out, void* ws, hipStream_t st);
 
+// ---- LiteDSA union (union.hip) ----
+size_t union_lds_bytes(int group, int k);
+hipError_t launch_dsa_union(const int32_t* idx, int64_t ld, int nq, int k, int group, int32_t* uidx, int32_t* ucount,
+                            uint32_t* mask, hipStream_t st);
+
 // ---- score side (score.hip) ----
 struct ScoreArgs {
   const void* q;

@@ -29,13 +29,14 @@ LT_SCORE_DSA, LT_SCORE_IP = 0, 1
 LT_SORTED_OUTPUT, LT_FORCE_FALLBACK = 1, 2
 LT_K_MAX = 8192
 LT_SAMPLE_LIST_MAX = 32768
+LT_UNION_MAX = 32768
 LT_NUM_STAGE_EVENTS = 6
 STAGES = ("sample", "range", "filter", "select", "fallback")
 
 EXPORTED = (
     "lt_options_default", "lt_indexer_topk_workspace_size", "lt_indexer_topk", "lt_indexer_scores",
     "lt_topk_select_workspace_size", "lt_topk_select", "lt_topk_radix",
-    "lt_sample_from_topk_workspace_size", "lt_sample_from_topk", "lt_event_create",
+    "lt_sample_from_topk_workspace_size", "lt_sample_from_topk", "lt_dsa_union", "lt_event_create",
     "lt_event_destroy", "lt_event_record", "lt_event_elapsed_ms", "lt_strerror",
 )
 
@@ -94,6 +95,8 @@ def load(path: str = LIB_PATH):
     lib.lt_sample_from_topk_workspace_size.restype = _SZ
     lib.lt_sample_from_topk.argtypes = [_P, _I64, _I32, _I32, _I32, _I32, _P, _P, _SZ, _P]
     lib.lt_sample_from_topk.restype = ctypes.c_int
+    lib.lt_dsa_union.argtypes = [_P, _I64, _I32, _I32, _I32, _P, _P, _P, _P]
+    lib.lt_dsa_union.restype = ctypes.c_int
     lib.lt_event_create.argtypes = [ctypes.POINTER(ctypes.c_void_p)]
     lib.lt_event_create.restype = ctypes.c_int
     lib.lt_event_destroy.argtypes = [_P]
@@ -162,6 +165,10 @@ def lt_sample_from_topk(prev_idx, ld, prev_rows, prev_k, nk, sample_size, sample
                         stream) -> int:
     return load().lt_sample_from_topk(prev_idx, ld, prev_rows, prev_k, nk, sample_size, sample_keys, workspace,
                                       workspace_bytes, stream)
+
+
+def lt_dsa_union(topk_idx, ld, nq, k, group, union_idx, union_count, member_mask, stream) -> int:
+    return load().lt_dsa_union(topk_idx, ld, nq, k, group, union_idx, union_count, member_mask, stream)
 
 
 def lt_strerror(status: int) -> str:
@@ -385,3 +392,25 @@ def sample_from_topk(prev_idx: torch.Tensor, num_keys: int, sample_size: int, ou
                              sample_size, _ptr(out), _ptr(workspace), workspace.numel(), _stream(stream))
     _check(st, "lt_sample_from_topk")
     return out
+
+
+def dsa_union(topk_idx: torch.Tensor, group: int, stream=None):
+    """LiteDSA union (sec. 3.3) of each group of `group` consecutive rows of
+    topk_idx [Nq, k] (int32, -1 padding). Returns (union_idx int32
+    [G, group * k], union_count int32 [G], member_mask int32 [Nq, W]; the
+    mask words are uint32 bit patterns, W = ceil(group * k / 32))."""
+    _need(topk_idx.is_cuda and topk_idx.dtype == torch.int32 and topk_idx.dim() == 2
+          and (topk_idx.numel() == 0 or topk_idx.stride(1) == 1),
+          "topk_idx must be an int32 [Nq, k] GPU matrix with unit column stride")
+    nq, k = topk_idx.shape
+    _need(group >= 1 and k >= 1 and group * k <= LT_UNION_MAX, "need 1 <= group, group * k <= LT_UNION_MAX")
+    ngroups = (nq + group - 1) // group
+    words = (group * k + 31) // 32
+    dev = topk_idx.device
+    uidx = torch.empty((ngroups, group * k), dtype=torch.int32, device=dev)
+    ucnt = torch.empty((ngroups,), dtype=torch.int32, device=dev)
+    mask = torch.empty((nq, words), dtype=torch.int32, device=dev)
+    st = lt_dsa_union(_ptr(topk_idx), topk_idx.stride(0) if topk_idx.numel() else k, nq, k, group, _ptr(uidx),
+                      _ptr(ucnt), _ptr(mask), _stream(stream))
+    _check(st, "lt_dsa_union")
+    return uidx, ucnt, mask

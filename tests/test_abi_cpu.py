@@ -125,6 +125,12 @@ def test_argument_checks_reject_before_any_device_work(lib):
     assert lt.lt_sample_from_topk(None, 4, 2, 4, 100, 10, P, P, ws, None) == lt.LT_EINVAL
     assert lt.lt_sample_from_topk(P, 4, 2, 4, 100, 10, P, P, ws - 1, None) == lt.LT_EWORKSPACE
     assert lt.lt_sample_from_topk(P, 4, 2, 4, 100, 10, P, P + 8, ws, None) == lt.LT_EINVAL
+    # union builder: group * k over the limit, ld < k, null outputs
+    assert lt.lt_dsa_union(P, 8, 4, 8, lt.LT_UNION_MAX // 8 + 1, P, P, P, None) == lt.LT_EINVAL
+    assert lt.lt_dsa_union(P, 7, 4, 8, 2, P, P, P, None) == lt.LT_EINVAL
+    assert lt.lt_dsa_union(P, 8, 4, 8, 0, P, P, P, None) == lt.LT_EINVAL
+    assert lt.lt_dsa_union(P, 8, 4, 8, 2, P, None, P, None) == lt.LT_EINVAL
+    assert lt.lt_dsa_union(None, 8, 0, 8, 2, None, None, None, None) == lt.LT_OK
     # empty problems are valid and do nothing
     assert lt.lt_indexer_topk(None, None, None, None, None, lt.LT_F32, lt.LT_SCORE_DSA, 0, 0, 4, 64, 2, None,
                               None, None, None, 0, None, None) == lt.LT_OK

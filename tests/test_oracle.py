@@ -509,3 +509,94 @@ def test_pins_catch_planted_sample_mistakes(monkeypatch):
             test_golden_previous_chunk_sample()
             for case in SAMPLE_CASES:
                 test_previous_chunk_sample_invariants(case)
+
+
+# --------------------------------------------------------------------------
+# LiteDSA union and membership masks (sec. 3.3)
+# --------------------------------------------------------------------------
+
+def test_golden_dsa_union():
+    with open(os.path.join(GOLDEN, "dsa_union.json")) as f:
+        g = json.load(f)
+    u, c, m = orc.dsa_union(np.array(g["topk_idx"], dtype=np.int32), g["group"])
+    assert u.tolist() == g["union_idx"]
+    assert c.tolist() == g["union_count"]
+    assert m.astype(np.int64).tolist() == g["member_mask"]
+
+
+def check_union_invariants(u, c, m, idx, group):
+    """What fixes the union uniquely: per group, the listed keys are exactly
+    the set of keys of its rows, ascending and distinct, then -1; and each
+    row's mask decodes (through that list) to exactly its own key set."""
+    idx = np.asarray(idx)
+    nq, k = idx.shape
+    ng = -(-nq // group)
+    assert u.shape == (ng, group * k) and c.shape == (ng,) and m.shape == (nq, -(-group * k // 32))
+    for g in range(ng):
+        rows = list(range(g * group, min(nq, (g + 1) * group)))
+        want = set()
+        for t in rows:
+            want |= {int(v) for v in idx[t] if v >= 0}
+        n = int(c[g])
+        lst = [int(v) for v in u[g, :n]]
+        assert lst == sorted(want) and len(lst) == len(set(lst))
+        assert np.all(u[g, n:] == -1)
+        for t in rows:
+            bits = [j for j in range(group * k) if (int(m[t, j // 32]) >> (j % 32)) & 1]
+            assert all(j < n for j in bits)
+            assert {lst[j] for j in bits} == {int(v) for v in idx[t] if v >= 0}
+
+
+UNION_CASES = [
+    # nq, k, group, key range, padding fraction
+    (10, 8, 3, 40, 0.2),
+    (16, 16, 4, 1000, 0.0),
+    (7, 5, 1, 20, 0.3),
+    (9, 32, 16, 100, 0.1),
+]
+
+
+def union_case_input(nq, k, keys, pad, seed):
+    rng = np.random.default_rng(seed)
+    base = rng.integers(0, keys, size=k)
+    idx = np.empty((nq, k), dtype=np.int32)
+    for t in range(nq):  # neighbours share part of their keys, as in sparse attention
+        own = rng.integers(0, keys, size=k)
+        idx[t] = np.where(rng.random(k) < 0.5, base, own)
+    idx[rng.random((nq, k)) < pad] = -1
+    return idx
+
+
+@pytest.mark.parametrize("case", UNION_CASES, ids=[f"{c[0]}x{c[1]}-g{c[2]}" for c in UNION_CASES])
+def test_dsa_union_invariants(case):
+    nq, k, group, keys, pad = case
+    idx = union_case_input(nq, k, keys, pad, seed=nq * k + group)
+    u, c, m = orc.dsa_union(idx, group)
+    check_union_invariants(u, c, m, idx, group)
+
+
+def test_pins_catch_planted_union_mistakes(monkeypatch):
+    good = orc.dsa_union
+
+    def descending(idx, group):
+        u, c, m = good(idx, group)
+        for g in range(len(c)):
+            u[g, : c[g]] = u[g, : c[g]][::-1].copy()
+        return u, c, m
+
+    def slot_off_by_one(idx, group):
+        u, c, m = good(idx, group)
+        return u, c, (m.astype(np.uint64) << 1).astype(np.uint32)
+
+    def padding_is_a_key(idx, group):
+        return good(np.where(np.asarray(idx) < 0, 0, idx), group)
+
+    def groups_shifted(idx, group):
+        return good(np.asarray(idx)[1:], group)
+
+    for bad in (descending, slot_off_by_one, padding_is_a_key, groups_shifted):
+        monkeypatch.setattr(orc, "dsa_union", bad)
+        with pytest.raises(Exception):
+            test_golden_dsa_union()
+            for case in UNION_CASES:
+                test_dsa_union_invariants(case)
