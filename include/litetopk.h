@@ -23,9 +23,10 @@
  *  - Total order used for selection (Eq. 2 of sec. 3.1 leaves ties open):
  *    higher score first; -0.0 equals +0.0; NaN ranks below -inf; equal scores
  *    go to the lower key index. The selected SET is therefore unique.
- *  - Output rows: row t holds min(k, e_t) selected entries followed by padding
- *    (index -1, score -inf). e_t = clamp(causal_offsets[t], 0, num_keys), or
- *    num_keys when causal_offsets is NULL: row t sees keys [0, e_t). Scores are
+ *  - Output rows: row t holds min(k, e_t - s_t) selected entries followed by
+ *    padding (index -1, score -inf). e_t = clamp(causal_offsets[t], 0,
+ *    num_keys), or num_keys when causal_offsets is NULL; s_t = 0 unless
+ *    lt_options.visible_start is set: row t sees keys [s_t, e_t). Scores are
  *    the raw float32 index scores I (never bin-space values). Without
  *    LT_SORTED_OUTPUT the selected entries come in an unspecified but
  *    deterministic order (the paper's select writes the above-threshold bins
@@ -114,6 +115,11 @@ typedef struct lt_options {
                               row t uses only the entries below e_t. The list is
                               read on the stream; it must stay valid until the
                               call's work has run.                              */
+  const int32_t* visible_start; /* NULL, or a DEVICE int32 [num_queries]: row t
+                              sees keys [s_t, e_t) with s_t =
+                              clamp(visible_start[t], 0, e_t) -- several
+                              sequences packed into one key array, each query
+                              seeing its own sequence. NULL = 0.                */
 } lt_options;
 
 /* Fills *opts with the defaults (k-dependent fields are resolved per call). */

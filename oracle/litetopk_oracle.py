@@ -26,7 +26,9 @@ buffers): those cannot change an exact top-k, so the oracle leaves them out.
 * Visibility -- the query chunk attends to the preceding context (sec. 1, the
   DSA prefill description): row t sees keys [0, e_t) with
   e_t = clamp(causal_offsets[t], 0, Nk), or all Nk keys when no offsets are
-  given.
+  given. Optional per-row starts narrow this to [s_t, e_t),
+  s_t = clamp(visible_start[t], 0, e_t): several sequences packed into one
+  key array, each query seeing its own sequence's keys.
 * fp8 inputs are OCP E4M3FN bytes (decoded here from the format definition:
   1 sign bit, 4 exponent bits with bias 7, 3 mantissa bits, no infinities,
   S.1111.111 is NaN) times a positive float32 per-token scale; the product is
@@ -104,6 +106,19 @@ def visible_counts(causal_offsets: Optional[np.ndarray], nq: int, nk: int) -> np
     return np.clip(np.asarray(causal_offsets, dtype=np.int64), 0, nk)
 
 
+def visible_ranges(causal_offsets: Optional[np.ndarray], visible_start: Optional[np.ndarray], nq: int,
+                   nk: int) -> Tuple[np.ndarray, np.ndarray]:
+    """(s_t, e_t) for every row: row t sees keys [s_t, e_t), e_t as in
+    visible_counts and s_t = clamp(visible_start[t], 0, e_t) (0 without
+    starts). Several sequences packed into one key array give each query its
+    own sequence's span this way."""
+    e = visible_counts(causal_offsets, nq, nk)
+    if visible_start is None:
+        return np.zeros(nq, dtype=np.int64), e
+    s = np.minimum(np.maximum(np.asarray(visible_start, dtype=np.int64), 0), e)
+    return s, e
+
+
 # ----------------------------------------------------------------------------
 # Scores -- Eq. (1)
 # ----------------------------------------------------------------------------
@@ -151,38 +166,39 @@ def order(scores: np.ndarray) -> np.ndarray:
     return np.lexsort((idx, neg, nan))
 
 
-def select_row(scores: np.ndarray, e: int, k: int) -> Tuple[np.ndarray, np.ndarray]:
-    """Exact top-k of the visible prefix scores[:e] of one row.
+def select_row(scores: np.ndarray, e: int, k: int, s: int = 0) -> Tuple[np.ndarray, np.ndarray]:
+    """Exact top-k of the visible keys [s, e) of one row, scores[s:e].
 
     Returns (idx int32 [k], score float32 [k]) sorted by the total order, with
-    min(k, e) real entries followed by padding (-1, -inf)."""
-    vis = np.asarray(scores[:e], dtype=np.float32)
+    min(k, e - s) real entries (key indices) followed by padding (-1, -inf)."""
+    vis = np.asarray(scores[s:e], dtype=np.float32)
     o = order(vis)[:k]
     idx = np.full(k, PAD_INDEX, dtype=np.int32)
     sc = np.full(k, PAD_SCORE, dtype=np.float32)
-    idx[:o.size] = o
+    idx[:o.size] = o + s
     sc[:o.size] = vis[o]
     return idx, sc
 
 
 def topk_select(scores: np.ndarray, nk: int, k: int, causal_offsets: Optional[np.ndarray] = None,
-                rows: Optional[Sequence[int]] = None) -> Tuple[np.ndarray, np.ndarray]:
+                rows: Optional[Sequence[int]] = None,
+                visible_start: Optional[np.ndarray] = None) -> Tuple[np.ndarray, np.ndarray]:
     """Scores-in selection: exact top-k of every requested row of a float32
     score matrix whose first ``nk`` columns are keys."""
     nq = scores.shape[0]
     rows = list(range(nq)) if rows is None else list(rows)
-    e = visible_counts(causal_offsets, nq, nk)
+    s0, e = visible_ranges(causal_offsets, visible_start, nq, nk)
     out_i = np.empty((len(rows), k), dtype=np.int32)
     out_s = np.empty((len(rows), k), dtype=np.float32)
     for i, t in enumerate(rows):
-        out_i[i], out_s[i] = select_row(scores[t, :nk], int(e[t]), k)
+        out_i[i], out_s[i] = select_row(scores[t, :nk], int(e[t]), k, int(s0[t]))
     return out_i, out_s
 
 
 def indexer_topk(q: np.ndarray, q_dtype: str, q_scale: Optional[np.ndarray], w: Optional[np.ndarray],
                  keys: np.ndarray, k_scale: Optional[np.ndarray], k: int, mode: str = "dsa",
                  causal_offsets: Optional[np.ndarray] = None, rows: Optional[Sequence[int]] = None,
-                 return_scores: bool = False):
+                 return_scores: bool = False, visible_start: Optional[np.ndarray] = None):
     """Fused operation, defined plainly: Eq. (1) scores for the visible keys of
     each requested row, then the exact top-k of Eq. (2).
 
@@ -193,7 +209,7 @@ def indexer_topk(q: np.ndarray, q_dtype: str, q_scale: Optional[np.ndarray], w: 
     ``return_scores``."""
     nq, nk = q.shape[0], keys.shape[0]
     rows = list(range(nq)) if rows is None else list(rows)
-    e = visible_counts(causal_offsets, nq, nk)
+    s0, e = visible_ranges(causal_offsets, visible_start, nq, nk)
     kd = dequantize(keys, q_dtype, k_scale)
     wd = None if w is None else np.asarray(w, dtype=np.float32).astype(np.float64)
     out_i = np.empty((len(rows), k), dtype=np.int32)
@@ -201,10 +217,14 @@ def indexer_topk(q: np.ndarray, q_dtype: str, q_scale: Optional[np.ndarray], w: 
     full = []
     for i, t in enumerate(rows):
         qd = dequantize(q[t], q_dtype, None if q_scale is None else q_scale[t])
-        s = row_scores(qd, None if wd is None else wd[t], kd[: e[t]], mode)
-        out_i[i], out_s[i] = select_row(s, int(e[t]), k)
+        # scores of the visible keys [s_t, e_t) only; full rows keep zeros
+        # before s_t so that row[j] is key j's score
+        vis = row_scores(qd, None if wd is None else wd[t], kd[s0[t]: e[t]], mode)
+        sr = np.zeros(int(e[t]), dtype=np.float32)
+        sr[s0[t]:] = vis
+        out_i[i], out_s[i] = select_row(sr, int(e[t]), k, int(s0[t]))
         if return_scores:
-            full.append(s)
+            full.append(sr)
     if return_scores:
         return out_i, out_s, full
     return out_i, out_s

@@ -30,6 +30,7 @@ struct Resolved {
   void** ev;
   int32_t* stats;
   const int32_t* keys_in;  // caller's sample list, or NULL for the random sample
+  const int32_t* starts;   // per-row visible starts, or NULL
   int status;              // LT_OK, or the error the options produce
 };
 
@@ -76,6 +77,7 @@ void resolve_common(const lt_options* o, int k, Resolved& r) {
   r.stats = o->row_stats;
   r.E = select_entries(k);
   r.keys_in = o->sample_keys;
+  r.starts = o->visible_start;
   r.status = LT_OK;
   if (r.keys_in && (o->sample_size < 1 || o->sample_size > LT_SAMPLE_LIST_MAX)) r.status = LT_EINVAL;
 }
@@ -186,6 +188,7 @@ void lt_options_default(lt_options* o) {
   o->stage_events = nullptr;
   o->row_stats = nullptr;
   o->sample_keys = nullptr;
+  o->visible_start = nullptr;
 }
 
 const char* lt_strerror(int status) {
@@ -236,7 +239,7 @@ int lt_indexer_topk(const void* q, const float* q_scale, const float* w, const v
   uint32_t* hist = reinterpret_cast<uint32_t*>(ws + L.hist);
   int2* cand = reinterpret_cast<int2*>(ws + L.cand);
   float* scratch = reinterpret_cast<float*>(ws + L.scratch);
-  ScoreArgs a{q, q_scale, w, keys, k_scale, (int)dtype, (int)mode, nq, nk, h, d, offs};
+  ScoreArgs a{q, q_scale, w, keys, k_scale, (int)dtype, (int)mode, nq, nk, h, d, offs, r.starts};
 
   hipError_t e;
   record(r, LT_STAGE_SAMPLE, st);
@@ -244,7 +247,7 @@ int lt_indexer_topk(const void* q, const float* q_scale, const float* w, const v
   if ((e = make_list(r, nk, 1, list, st)) != hipSuccess) return hip_status(e);
   if (r.ns > 0 && (e = launch_sample_scores(a, list, r.ns, samp, st)) != hipSuccess) return hip_status(e);
   record(r, LT_STAGE_RANGE, st);
-  if ((e = launch_range(false, samp, r.ns, nq, nk, offs, list, r.ns, r.m, k, params, st)) != hipSuccess)
+  if ((e = launch_range(false, samp, r.ns, nq, nk, offs, r.starts, list, r.ns, r.m, k, params, st)) != hipSuccess)
     return hip_status(e);
   record(r, LT_STAGE_FILTER, st);
   if ((e = launch_fused_scan(a, params, r.S, r.L, r.cap, r.m, k, cnt, hist, cand, st)) != hipSuccess)
@@ -269,7 +272,7 @@ int lt_indexer_scores(const void* q, const float* q_scale, const float* w, const
   if (ld < nk) return LT_EINVAL;
   if (nq == 0 || nk == 0) return LT_OK;
   if (!scores) return LT_EINVAL;
-  ScoreArgs a{q, q_scale, w, keys, k_scale, (int)dtype, (int)mode, nq, nk, h, d, nullptr};
+  ScoreArgs a{q, q_scale, w, keys, k_scale, (int)dtype, (int)mode, nq, nk, h, d, nullptr, nullptr};
   return hip_status(launch_dense_scores(a, scores, ld, (hipStream_t)stream));
 }
 
@@ -314,17 +317,19 @@ int lt_topk_select(const float* scores, int64_t stride, int32_t nq, int32_t nk, 
   if ((e = launch_init(qctl, st)) != hipSuccess) return hip_status(e);
   if ((e = make_list(r, nk, kSampleBlockScores, list, st)) != hipSuccess) return hip_status(e);
   record(r, LT_STAGE_RANGE, st);
-  if ((e = launch_range(true, scores, stride, nq, nk, offs, list, r.ns, r.m, k, params, st)) != hipSuccess)
+  if ((e = launch_range(true, scores, stride, nq, nk, offs, r.starts, list, r.ns, r.m, k, params, st)) !=
+      hipSuccess)
     return hip_status(e);
   record(r, LT_STAGE_FILTER, st);
-  if ((e = launch_filter(scores, stride, nq, nk, offs, params, r.S, r.L, r.cap, r.m, k, cnt, hist, cand, st)) != hipSuccess)
+  if ((e = launch_filter(scores, stride, nq, nk, offs, r.starts, params, r.S, r.L, r.cap, r.m, k, cnt, hist, cand,
+                         st)) != hipSuccess)
     return hip_status(e);
   record(r, LT_STAGE_SELECT, st);
   if ((e = launch_select(params, cnt, hist, cand, nq, r.S, r.cap, r.m, k, r.E, r.flags, out_idx, out_scores, qctl,
                          queue, r.stats, st)) != hipSuccess)
     return hip_status(e);
   record(r, LT_STAGE_FALLBACK, st);
-  if ((e = launch_fallback_scores(scores, stride, nk, offs, k, r.flags, qctl, queue, out_idx, out_scores,
+  if ((e = launch_fallback_scores(scores, stride, nk, offs, r.starts, k, r.flags, qctl, queue, out_idx, out_scores,
                                   kFallbackGridScores, st)) != hipSuccess)
     return hip_status(e);
   record(r, LT_NUM_STAGE_EVENTS - 1, st);

@@ -63,6 +63,20 @@ __device__ __forceinline__ int sample_key(int i, int ns, int nk, int blk, uint64
   return (int)(lo + (int64_t)(r % (uint64_t)room)) + o;
 }
 
+// Visible key range [s, e) of a row: e = clamp(end[row], 0, nk) (nk without
+// ends), s = clamp(start[row], 0, e) (0 without starts).
+struct RowRange {
+  int s, e;
+};
+__device__ __forceinline__ RowRange row_range(const int32_t* ends, const int32_t* starts, int row, int nk) {
+  int e = ends ? ends[row] : nk;
+  e = e < 0 ? 0 : (e > nk ? nk : e);
+  int s = starts ? starts[row] : 0;
+  s = s < 0 ? 0 : (s > e ? e : s);
+  return RowRange{s, e};
+}
+
+
 // ---------------------------------------------------------------------------
 // Equal-width bins (sec. 3.2 "Sampling"): bin = floor((I - s_min) * delta),
 // evaluated as x = fma(I, delta, c) with c = -s_min * delta. Any such x is

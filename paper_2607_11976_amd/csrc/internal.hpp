@@ -12,20 +12,22 @@ namespace lt {
 
 // ---- selection side (select.hip) ----
 hipError_t launch_init(uint32_t* qctl, hipStream_t st);
+// Visibility: row t sees keys [s_t, e_t) (row_range); `offs` holds the ends
+// (NULL = num_keys) and `starts` the starts (NULL = 0).
 hipError_t launch_range(bool from_scores, const float* src, int64_t stride, int nq, int nk,
-                        const int32_t* offs, const int32_t* list, int ns, int m, int k, RowParam* params,
-                        hipStream_t st);
+                        const int32_t* offs, const int32_t* starts, const int32_t* list, int ns, int m, int k,
+                        RowParam* params, hipStream_t st);
 hipError_t launch_filter(const float* scores, int64_t stride, int nq, int nk, const int32_t* offs,
-                         const RowParam* params, int S, int L, int cap, int m, int k, uint32_t* cnt,
-                         uint32_t* hist, int2* cand, hipStream_t st);
+                         const int32_t* starts, const RowParam* params, int S, int L, int cap, int m, int k,
+                         uint32_t* cnt, uint32_t* hist, int2* cand, hipStream_t st);
 size_t select_lds_bytes(int E);
 hipError_t launch_select(const RowParam* params, const uint32_t* cnt, const uint32_t* hist,
                          const int2* cand, int nq, int S, int cap, int m, int k, int E,
                          uint32_t flags, int32_t* out_i, float* out_s, uint32_t* qctl,
                          int32_t* queue, int32_t* stats, hipStream_t st);
 hipError_t launch_fallback_scores(const float* scores, int64_t stride, int nk, const int32_t* offs,
-                                  int k, uint32_t flags, const uint32_t* qctl, const int32_t* queue,
-                                  int32_t* out_i, float* out_s, int grid, hipStream_t st);
+                                  const int32_t* starts, int k, uint32_t flags, const uint32_t* qctl,
+                                  const int32_t* queue, int32_t* out_i, float* out_s, int grid, hipStream_t st);
 hipError_t launch_radix(const float* scores, int64_t stride, int nq, int nk, const int32_t* offs,
                         int k, uint32_t flags, int32_t* out_i, float* out_s, hipStream_t st);
 
@@ -52,7 +54,8 @@ struct ScoreArgs {
   const void* keys;
   const float* k_scale;
   int dtype, mode, nq, nk, h, d;
-  const int32_t* offs;
+  const int32_t* offs;    // row ends (NULL = nk)
+  const int32_t* starts;  // row starts (NULL = 0)
 };
 
 // Static shape of one compiled score configuration.

@@ -564,7 +564,7 @@ struct RowSink {
 template <class C>
 struct FusedSink {
   float delta[C::QW], cc[C::QW], thr[C::QW], thr_up[C::QW];
-  int tau[C::QW], e[C::QW];
+  int tau[C::QW], e[C::QW], sv[C::QW];
   uint32_t tail[C::QW], above[C::QW];
   uint32_t* hist;     // LDS, [QW][m] for this wave
   int2* cand;
@@ -581,18 +581,18 @@ struct FusedSink {
 #pragma unroll
     for (int q = 0; q < C::QW; ++q) {
       const int t = qbase + q;
-      int ev = 0;
+      RowRange rr{0, 0};
       float dl = 1.0f, c = 0.0f;
       int t0 = -1;
       if (t < nq) {
-        ev = a.offs ? a.offs[t] : a.nk;
-        ev = ev < 0 ? 0 : (ev > a.nk ? a.nk : ev);
+        rr = row_range(a.offs, a.starts, t, a.nk);
         const RowParam p = params[t];
         dl = p.delta;
         c = p.c;
         t0 = p.tau0;
       }
-      e[q] = ev < kend ? ev : kend;
+      e[q] = rr.e < kend ? rr.e : kend;
+      sv[q] = rr.s;
       crow[q] = cand + ((int64_t)(t < nq ? t : 0) * S + split) * cap;
       delta[q] = dl;
       cc[q] = c;
@@ -613,7 +613,8 @@ struct FusedSink {
       constexpr int na = C::item_nt(it, 0), nb = C::item_nt(it, 1);
       const int key = k0 + (h ? nb : na) * 32 + r32;
       x[it] = bin_x(sc[it], h ? delta[qb] : delta[qa], h ? cc[qb] : cc[qa]);
-      ps[it] = live && key < (h ? e[qb] : e[qa]) && !(x[it] < (h ? thr[qb] : thr[qa]));
+      ps[it] = live && key < (h ? e[qb] : e[qa]) && key >= (h ? sv[qb] : sv[qa]) &&
+               !(x[it] < (h ? thr[qb] : thr[qa]));
       any |= __ballot(ps[it]);
     });
     if (any == 0) return;  // wave-uniform: nothing passed this tile
@@ -700,7 +701,7 @@ struct GroupedSink {
   static_assert(C::GROUPED && C::QW <= kWave, "one query per lane");
   // lane q: state of query qbase + q
   float delta_v, c_v, t_v;
-  int tau_v, e_v;
+  int tau_v, e_v, s_v;
   uint32_t tail_v, above_v;
   float tq[C::NIH];   // T of the query of item j (items j and j + NIH share it)
   bool ungated;       // some row of the wave has no gate (tau = -1)
@@ -734,18 +735,18 @@ struct GroupedSink {
 
   __device__ void init(const ScoreArgs& a, const RowParam* params, int kend) {
     const int l = lane_id(), t = qbase + l;
-    int ev = 0;
+    RowRange rr{0, 0};
     float dl = 1.0f, c = 0.0f;
     int t0 = -1;
     if (l < C::QW && t < nq) {
-      ev = a.offs ? a.offs[t] : a.nk;
-      ev = ev < 0 ? 0 : (ev > a.nk ? a.nk : ev);
+      rr = row_range(a.offs, a.starts, t, a.nk);
       const RowParam p = params[t];
       dl = p.delta;
       c = p.c;
       t0 = p.tau0;
     }
-    e_v = ev < kend ? ev : kend;
+    e_v = rr.e < kend ? rr.e : kend;
+    s_v = rr.s;
     delta_v = dl;
     c_v = c;
     tau_v = t0;
@@ -807,7 +808,8 @@ struct GroupedSink {
       const float s_it = scv[it];
       const int key = k0 + nt * 32 + r32;
       const int ea = __builtin_amdgcn_readlane(e_v, qa), eb = __builtin_amdgcn_readlane(e_v, qb);
-      const bool pass = !(s_it < tqv[j]) && key < (h ? eb : ea);
+      const int sa = __builtin_amdgcn_readlane(s_v, qa), sb = __builtin_amdgcn_readlane(s_v, qb);
+      const bool pass = !(s_it < tqv[j]) && key < (h ? eb : ea) && key >= (h ? sb : sa);
       const uint64_t m2 = __ballot(pass);
       if (m2 == 0) continue;
       const uint32_t lo = (uint32_t)__popcll(m2 & 0xFFFFFFFFull), hi = (uint32_t)__popcll(m2) - lo;
@@ -902,19 +904,26 @@ __global__ __launch_bounds__(C::NTHREADS) void k_fused(ScoreArgs a, const RowPar
   extern __shared__ __align__(16) uint8_t lds[];
   uint32_t* hist = reinterpret_cast<uint32_t*>(lds + C::SCAN_LDS);
   int* emax = reinterpret_cast<int*>(hist + C::QT * m);
+  int* smin = emax + 1;
   const int tile = blockIdx.x / S, split = blockIdx.x - tile * S;
   const int q0 = tile * C::QT, wave = threadIdx.x / kWave, qbase = q0 + wave * C::QW;
   for (int i = threadIdx.x; i < C::QT * m; i += C::NTHREADS) hist[i] = 0u;
-  if (threadIdx.x == 0) *emax = 0;
-  __syncthreads();
-  if (threadIdx.x < C::QT && q0 + (int)threadIdx.x < a.nq) {
-    int ev = a.offs ? a.offs[q0 + threadIdx.x] : a.nk;
-    ev = ev < 0 ? 0 : (ev > a.nk ? a.nk : ev);
-    atomicMax(emax, ev);
+  if (threadIdx.x == 0) {
+    *emax = 0;
+    *smin = a.nk;
   }
   __syncthreads();
-  const int kb = split * L;
-  const int ke = min(min(kb + L, a.nk), *emax);
+  if (threadIdx.x < C::QT && q0 + (int)threadIdx.x < a.nq) {
+    const RowRange rr = row_range(a.offs, a.starts, q0 + threadIdx.x, a.nk);
+    if (rr.e > rr.s) {
+      atomicMax(emax, rr.e);
+      atomicMin(smin, rr.s);
+    }
+  }
+  __syncthreads();
+  // the split's keys within the union of the block's rows' ranges
+  const int kb = max(split * L, *smin);
+  const int ke = min(min(split * L + L, a.nk), *emax);
   WaveQ<C> wq;
   load_q<C>(wq, a, qbase);
   std::conditional_t<C::GROUPED, GroupedSink<C>, FusedSink<C>> sink;
@@ -942,17 +951,16 @@ __global__ __launch_bounds__(C::NTHREADS) void k_fused_fallback(ScoreArgs a, int
   for (uint32_t r = blockIdx.x; r < n; r += gridDim.x) {
     const int row = queue[r];
     const int q0 = (row / C::QT) * C::QT, qbase = q0 + wave * C::QW;
-    int e = a.offs ? a.offs[row] : a.nk;
-    e = e < 0 ? 0 : (e > a.nk ? a.nk : e);
+    const RowRange rr = row_range(a.offs, a.starts, row, a.nk);
     float* srow = scratch + (int64_t)blockIdx.x * a.nk;
     WaveQ<C> wq;
     load_q<C>(wq, a, qbase);
     RowSink<C> sink{srow, qbase, row};
-    wg_scan<C>(a, SrcContig{}, 0, e, lds, wq, sink);
+    wg_scan<C>(a, SrcContig{}, rr.s, rr.e, lds, wq, sink);
     __threadfence_block();
     __syncthreads();
-    radix_select_row<C::NTHREADS>(srow, e, k, out_i + (int64_t)row * k, out_s + (int64_t)row * k,
-                                  flags & LT_SORTED_OUTPUT, lds);
+    radix_select_row<C::NTHREADS>(srow + rr.s, rr.e - rr.s, k, out_i + (int64_t)row * k, out_s + (int64_t)row * k,
+                                  flags & LT_SORTED_OUTPUT, lds, rr.s);
     __syncthreads();
   }
 }

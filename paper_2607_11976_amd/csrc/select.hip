@@ -29,7 +29,7 @@ constexpr int kRangeThreads = 256;
 constexpr int kRangeUnroll = 8;
 
 template <bool FROM_SCORES>
-__device__ __forceinline__ void range_load(const float* rp, const int32_t* list, int ns, int e, int base,
+__device__ __forceinline__ void range_load(const float* rp, const int32_t* list, int ns, RowRange rr, int base,
                                            float (&s)[kRangeUnroll], bool (&vis)[kRangeUnroll]) {
   int key[kRangeUnroll];
 #pragma unroll
@@ -40,22 +40,22 @@ __device__ __forceinline__ void range_load(const float* rp, const int32_t* list,
 #pragma unroll
   for (int u = 0; u < kRangeUnroll; ++u) {
     const int i = base + u * kRangeThreads + (int)threadIdx.x;
-    vis[u] = key[u] >= 0 && key[u] < e;
+    vis[u] = key[u] >= rr.s && key[u] < rr.e;
     s[u] = vis[u] ? (FROM_SCORES ? rp[key[u]] : rp[i]) : 0.0f;
   }
 }
 
 template <bool FROM_SCORES>
 __global__ __launch_bounds__(kRangeThreads) void k_range(const float* src, int64_t stride, int nq, int nk,
-                                                         const int32_t* offs, const int32_t* list, int ns, int m,
-                                                         int k, RowParam* params) {
+                                                         const int32_t* offs, const int32_t* starts,
+                                                         const int32_t* list, int ns, int m, int k,
+                                                         RowParam* params) {
   constexpr int NW = kRangeThreads / kWave;
   __shared__ uint32_t hist[kMaxBins];
   __shared__ float red_mn[NW], red_mx[NW];
   __shared__ uint32_t red_n[NW];
   const int row = blockIdx.x, wave = threadIdx.x / kWave, l = lane_id();
-  int e = offs ? offs[row] : nk;
-  e = e < 0 ? 0 : (e > nk ? nk : e);
+  const RowRange rr = row_range(offs, starts, row, nk);
   const float* rp = src + (int64_t)row * stride;
 
   for (int b = threadIdx.x; b < kMaxBins; b += kRangeThreads) hist[b] = 0u;
@@ -64,7 +64,7 @@ __global__ __launch_bounds__(kRangeThreads) void k_range(const float* src, int64
   for (int base = 0; base < ns; base += kRangeThreads * kRangeUnroll) {
     float s[kRangeUnroll];
     bool vis[kRangeUnroll];
-    range_load<FROM_SCORES>(rp, list, ns, e, base, s, vis);
+    range_load<FROM_SCORES>(rp, list, ns, rr, base, s, vis);
 #pragma unroll
     for (int u = 0; u < kRangeUnroll; ++u) {
       nvis += vis[u];
@@ -101,7 +101,7 @@ __global__ __launch_bounds__(kRangeThreads) void k_range(const float* src, int64
   for (int base = 0; base < ns; base += kRangeThreads * kRangeUnroll) {
     float s[kRangeUnroll];
     bool vis[kRangeUnroll];
-    range_load<FROM_SCORES>(rp, list, ns, e, base, s, vis);
+    range_load<FROM_SCORES>(rp, list, ns, rr, base, s, vis);
 #pragma unroll
     for (int u = 0; u < kRangeUnroll; ++u) {
       const int b = bin_of(bin_x(s[u], delta, c), m);
@@ -129,18 +129,20 @@ __global__ __launch_bounds__(kRangeThreads) void k_range(const float* src, int64
 constexpr int kFilterWaves = 4;
 
 __global__ __launch_bounds__(kFilterWaves * kWave) void k_filter(
-    const float* scores, int64_t stride, int nq, int nk, const int32_t* offs, const RowParam* params,
-    int S, int L, int cap, int m, int k, uint32_t* cnt, uint32_t* hist_out, int2* cand) {
+    const float* scores, int64_t stride, int nq, int nk, const int32_t* offs, const int32_t* starts,
+    const RowParam* params, int S, int L, int cap, int m, int k, uint32_t* cnt, uint32_t* hist_out, int2* cand) {
   __shared__ uint32_t hist_all[kFilterWaves][kMaxBins];
   const int wave = threadIdx.x / kWave, l = lane_id();
   const int unit = blockIdx.x * kFilterWaves + wave;
   if (unit >= nq * S) return;
   const int row = unit / S, split = unit - row * S;
   uint32_t* hist = hist_all[wave];
-  int e = offs ? offs[row] : nk;
-  e = e < 0 ? 0 : (e > nk ? nk : e);
-  const int lo = split * L;
-  const int hi = min(lo + L, e);
+  const RowRange rr = row_range(offs, starts, row, nk);
+  // the split's keys within the row's range; the first chunk starts on a
+  // 4-key boundary for the float4 loads, keys below the range are masked
+  const int lo = max(split * L, rr.s & ~3);
+  const int hi = min(split * L + L, rr.e);
+  const int klo = max(split * L, rr.s);
   const RowParam p = params[row];
   int tau = p.tau0;
   float thr = gate_thr(tau);
@@ -168,7 +170,7 @@ __global__ __launch_bounds__(kFilterWaves * kWave) void k_filter(
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
       x[j] = bin_x(v[j], p.delta, p.c);
-      ps[j] = (i0 + j < hi) && !(x[j] < thr);
+      ps[j] = (i0 + j >= klo) && (i0 + j < hi) && !(x[j] < thr);
       uint64_t mask = __ballot(ps[j]);
       below += mbcnt64(mask);
       total += (uint32_t)__popcll(mask);
@@ -358,16 +360,16 @@ __global__ __launch_bounds__(kSelThreads) void k_select(
 // queue entries b, b + grid, ...; the queue length is read on the device.
 // ---------------------------------------------------------------------------
 __global__ __launch_bounds__(kSelThreads) void k_fallback_scores(
-    const float* scores, int64_t stride, int nk, const int32_t* offs, int k, uint32_t flags,
-    const uint32_t* qctl, const int32_t* queue, int32_t* out_i, float* out_s) {
+    const float* scores, int64_t stride, int nk, const int32_t* offs, const int32_t* starts, int k,
+    uint32_t flags, const uint32_t* qctl, const int32_t* queue, int32_t* out_i, float* out_s) {
   extern __shared__ __align__(16) uint8_t lds[];
   const uint32_t n = qctl[0];
   for (uint32_t r = blockIdx.x; r < n; r += gridDim.x) {
     const int row = queue[r];
-    int e = offs ? offs[row] : nk;
-    e = e < 0 ? 0 : (e > nk ? nk : e);
-    radix_select_row<kSelThreads>(scores + (int64_t)row * stride, e, k, out_i + (int64_t)row * k,
-                                  out_s + (int64_t)row * k, flags & LT_SORTED_OUTPUT, lds);
+    const RowRange rr = row_range(offs, starts, row, nk);
+    radix_select_row<kSelThreads>(scores + (int64_t)row * stride + rr.s, rr.e - rr.s, k,
+                                  out_i + (int64_t)row * k, out_s + (int64_t)row * k,
+                                  flags & LT_SORTED_OUTPUT, lds, rr.s);
     __syncthreads();
   }
 }
@@ -393,22 +395,24 @@ hipError_t launch_init(uint32_t* qctl, hipStream_t st) {
 }
 
 hipError_t launch_range(bool from_scores, const float* src, int64_t stride, int nq, int nk,
-                        const int32_t* offs, const int32_t* list, int ns, int m, int k, RowParam* params,
-                        hipStream_t st) {
+                        const int32_t* offs, const int32_t* starts, const int32_t* list, int ns, int m, int k,
+                        RowParam* params, hipStream_t st) {
   dim3 grid(nq);
   if (from_scores)
-    hipLaunchKernelGGL(k_range<true>, grid, dim3(kRangeThreads), 0, st, src, stride, nq, nk, offs, list, ns, m, k, params);
+    hipLaunchKernelGGL(k_range<true>, grid, dim3(kRangeThreads), 0, st, src, stride, nq, nk, offs, starts, list, ns,
+                       m, k, params);
   else
-    hipLaunchKernelGGL(k_range<false>, grid, dim3(kRangeThreads), 0, st, src, stride, nq, nk, offs, list, ns, m, k, params);
+    hipLaunchKernelGGL(k_range<false>, grid, dim3(kRangeThreads), 0, st, src, stride, nq, nk, offs, starts, list, ns,
+                       m, k, params);
   return hipGetLastError();
 }
 
 hipError_t launch_filter(const float* scores, int64_t stride, int nq, int nk, const int32_t* offs,
-                         const RowParam* params, int S, int L, int cap, int m, int k, uint32_t* cnt,
-                         uint32_t* hist, int2* cand, hipStream_t st) {
+                         const int32_t* starts, const RowParam* params, int S, int L, int cap, int m, int k,
+                         uint32_t* cnt, uint32_t* hist, int2* cand, hipStream_t st) {
   const int units = nq * S;
   dim3 grid((units + kFilterWaves - 1) / kFilterWaves);
-  hipLaunchKernelGGL(k_filter, grid, dim3(kFilterWaves * kWave), 0, st, scores, stride, nq, nk, offs,
+  hipLaunchKernelGGL(k_filter, grid, dim3(kFilterWaves * kWave), 0, st, scores, stride, nq, nk, offs, starts,
                      params, S, L, cap, m, k, cnt, hist, cand);
   return hipGetLastError();
 }
@@ -427,13 +431,13 @@ hipError_t launch_select(const RowParam* params, const uint32_t* cnt, const uint
 }
 
 hipError_t launch_fallback_scores(const float* scores, int64_t stride, int nk, const int32_t* offs,
-                                  int k, uint32_t flags, const uint32_t* qctl, const int32_t* queue,
-                                  int32_t* out_i, float* out_s, int grid, hipStream_t st) {
+                                  const int32_t* starts, int k, uint32_t flags, const uint32_t* qctl,
+                                  const int32_t* queue, int32_t* out_i, float* out_s, int grid, hipStream_t st) {
   if (radix_lds_bytes(k) > 65536)
     (void)hipFuncSetAttribute((const void*)k_fallback_scores, hipFuncAttributeMaxDynamicSharedMemorySize,
                               (int)radix_lds_bytes(k));
   hipLaunchKernelGGL(k_fallback_scores, dim3(grid), dim3(kSelThreads), radix_lds_bytes(k), st, scores,
-                     stride, nk, offs, k, flags, qctl, queue, out_i, out_s);
+                     stride, nk, offs, starts, k, flags, qctl, queue, out_i, out_s);
   return hipGetLastError();
 }
 

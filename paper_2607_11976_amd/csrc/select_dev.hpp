@@ -90,8 +90,26 @@ __device__ void sort_output_row(int32_t* oi, float* os, int n, uint64_t* ent, Fe
 // one ordered pass keeps every key > K* and the lowest-index keys == K*.
 // Output order: ascending key index, or the total order when `sorted`.
 template <int NTH>
+__device__ void radix_select_row_at(const float* row, int n, int k, int32_t* oi, float* os, bool sorted,
+                                    uint8_t* lds);
+
+// radix_select_row over keys [base, base + n) of a row whose key `base` is at
+// row[0]: the written indices are shifted by `base`.
+template <int NTH>
 __device__ void radix_select_row(const float* row, int n, int k, int32_t* oi, float* os, bool sorted,
-                                 uint8_t* lds) {
+                                 uint8_t* lds, int base = 0) {
+  radix_select_row_at<NTH>(row, n, k, oi, os, sorted, lds);
+  if (base != 0) {
+    __threadfence_block();
+    __syncthreads();
+    for (int i = threadIdx.x; i < k; i += NTH)
+      if (oi[i] >= 0) oi[i] += base;
+  }
+}
+
+template <int NTH>
+__device__ void radix_select_row_at(const float* row, int n, int k, int32_t* oi, float* os, bool sorted,
+                                    uint8_t* lds) {
   uint32_t* hist = reinterpret_cast<uint32_t*>(lds);
   uint32_t* tmp = hist + 256;                // 16 words
   uint64_t* ent = reinterpret_cast<uint64_t*>(lds + 256 * 4 + 64);

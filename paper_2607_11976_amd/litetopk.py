@@ -52,6 +52,7 @@ class LtOptions(ctypes.Structure):
         ("stage_events", ctypes.c_void_p),
         ("row_stats", ctypes.c_void_p),
         ("sample_keys", ctypes.c_void_p),
+        ("visible_start", ctypes.c_void_p),
     ]
 
 
@@ -213,7 +214,8 @@ def _on_gpu(*ts):
 def make_options(num_bins=None, sample_size=None, capacity=None, key_splits=None,
                  sorted_output=False, force_fallback=False, seed=None, stage_events=None,
                  row_stats: Optional[torch.Tensor] = None,
-                 sample_keys: Optional[torch.Tensor] = None) -> LtOptions:
+                 sample_keys: Optional[torch.Tensor] = None,
+                 visible_start: Optional[torch.Tensor] = None) -> LtOptions:
     """lt_options from keyword arguments. sample_keys: a GPU int32 list used
     as the sample (its length becomes sample_size); the tensor must stay
     alive until the call that uses these options has run."""
@@ -238,6 +240,10 @@ def make_options(num_bins=None, sample_size=None, capacity=None, key_splits=None
         _need(sample_keys.dtype == torch.int32 and sample_keys.dim() == 1, "sample_keys must be int32 [n]")
         o.sample_keys = sample_keys.data_ptr()
         o.sample_size = sample_keys.numel()
+    if visible_start is not None:
+        _on_gpu(visible_start)
+        _need(visible_start.dtype == torch.int32 and visible_start.dim() == 1, "visible_start must be int32 [Nq]")
+        o.visible_start = visible_start.data_ptr()
     return o
 
 

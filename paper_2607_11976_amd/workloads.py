@@ -210,3 +210,27 @@ def score_rows(nq: int, nk: int, seed: int, kind: str = "normal", ld: Optional[i
     if ld > nk:
         s[:, nk:] = np.float32(1e30)
     return torch.from_numpy(s.astype(np.float32))
+
+
+def packed_batch(cfg: Workload, lens, nqs, seed: int):
+    """Several sequences of the ``cfg`` law packed into one batch: sequence b
+    has lens[b] keys and its last nqs[b] positions as queries. Keys are
+    concatenated ([sum(lens), d]), queries too; row t of sequence b sees its
+    own sequence's causal prefix [base_b, base_b + e_local) through
+    offsets (ends) and starts. Returns the generate() dict plus "starts"
+    (int32 [Nq]) and "bases"."""
+    parts = [generate(scaled(cfg, nq=n, nk=L), seed=seed + 7 * b) for b, (L, n) in enumerate(zip(lens, nqs))]
+    bases = np.cumsum([0] + list(lens[:-1])).astype(np.int64)
+    out = {}
+    for key in ("q", "w", "keys", "q_scale", "k_scale"):
+        vals = [p_[key] for p_ in parts]
+        out[key] = None if vals[0] is None else torch.cat(vals, 0).contiguous()
+    ends, starts = [], []
+    for b, (p_, L, n) in enumerate(zip(parts, lens, nqs)):
+        e_local = p_["offsets"].numpy().astype(np.int64) if p_["offsets"] is not None else np.full(n, L)
+        ends.append(bases[b] + e_local)
+        starts.append(np.full(n, bases[b]))
+    out["offsets"] = torch.from_numpy(np.concatenate(ends).astype(np.int32))
+    out["starts"] = torch.from_numpy(np.concatenate(starts).astype(np.int32))
+    out["bases"] = bases
+    return out

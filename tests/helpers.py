@@ -25,7 +25,8 @@ def oracle_topk(x: dict, dtype: str, k: int, mode: str, rows=None):
         storage_np(x["q"], dtype), dtype, None if x.get("q_scale") is None else x["q_scale"].numpy(),
         None if x.get("w") is None else x["w"].numpy(), storage_np(x["keys"], dtype),
         None if x.get("k_scale") is None else x["k_scale"].numpy(), k, mode,
-        None if x.get("offsets") is None else x["offsets"].numpy(), rows=rows, return_scores=True)
+        None if x.get("offsets") is None else x["offsets"].numpy(), rows=rows, return_scores=True,
+        visible_start=None if x.get("starts") is None else x["starts"].numpy())
 
 
 def oracle_dense(x: dict, dtype: str, mode: str, rows=None):
@@ -37,5 +38,5 @@ def oracle_dense(x: dict, dtype: str, mode: str, rows=None):
 
 
 def to_dev(x: dict, dev="cuda"):
-    keys = ("q", "q_scale", "w", "keys", "k_scale", "offsets")
+    keys = ("q", "q_scale", "w", "keys", "k_scale", "offsets", "starts")
     return {n: (None if x.get(n) is None else x[n].to(dev)) for n in keys}

@@ -36,10 +36,11 @@ def test_library_exports_every_header_symbol(lib):
 
 
 def test_options_struct_layout_and_defaults(lib):
-    assert ctypes.sizeof(lt.LtOptions) == 56  # 5 x int32/uint32, pad, seed, 3 pointers
+    assert ctypes.sizeof(lt.LtOptions) == 64  # 5 x int32/uint32, pad, seed, 4 pointers
     o = lt.lt_options_default()
     assert o.num_bins == 256 and o.sample_size < 0 and o.capacity == 0 and o.key_splits == 0
     assert o.flags == 0 and not o.stage_events and not o.row_stats and not o.sample_keys
+    assert not o.visible_start
 
 
 def test_strerror(lib):

@@ -231,6 +231,72 @@ def test_ramp_closed_form_top_k_is_last_visible_keys():
         np.testing.assert_allclose(sc[t, :m], want, rtol=1e-6)
 
 
+def test_ramp_closed_form_with_visible_starts():
+    # the ramp above with per-row starts: the top-k is the last min(k, e - s)
+    # keys of [s, e), i.e. e-1 down to max(s, e-k)
+    rng = np.random.default_rng(12)
+    H, d, nk, nq, k = 4, 8, 300, 7, 37
+    u = rng.integers(1, 3, size=d).astype(np.float32)
+    q = np.broadcast_to(u, (nq, H, d)).astype(np.float32).copy()
+    keys = (np.arange(1, nk + 1, dtype=np.float32)[:, None] * u[None, :]).astype(np.float32)
+    w = rng.random((nq, H)).astype(np.float32)
+    offs = np.array([300, 299, 150, 37, 10, 0, 200], dtype=np.int32)
+    starts = np.array([0, 280, 100, 30, 20, -5, 199], dtype=np.int32)
+    idx, sc = orc.indexer_topk(q, "f32", None, w, keys, None, k, "dsa", offs, visible_start=starts)
+    for t in range(nq):
+        e = int(offs[t])
+        s = min(max(int(starts[t]), 0), e)
+        m = min(k, e - s)
+        assert idx[t, :m].tolist() == list(range(e - 1, e - 1 - m, -1)), t
+        assert np.all(idx[t, m:] == -1)
+
+
+def test_select_with_starts_matches_brute_force():
+    rng = np.random.default_rng(17)
+    for trial in range(200):
+        n = int(rng.integers(1, 10))
+        row = special_row(rng, n)
+        e = int(rng.integers(0, n + 1))
+        s = int(rng.integers(0, e + 1))
+        k = int(rng.integers(1, n + 2))
+        idx, sc = orc.select_row(row, e, k, s)
+        want = [j + s for j in brute_topk(row[s:e], k)] if e > s else []
+        assert list(idx[: len(want)]) == want
+        assert np.all(idx[len(want):] == -1)
+
+
+def test_packed_sequences_equal_separate_sequences():
+    # keys of three sequences packed into one array, each query seeing only
+    # its own sequence (start = the sequence's base): the result is each
+    # sequence computed alone, with indices shifted by the base
+    rng = np.random.default_rng(21)
+    H, d, k = 4, 16, 20
+    lens = [50, 120, 33]
+    nqs = [5, 7, 4]
+    bases = np.cumsum([0] + lens[:-1])
+    keys = rng.standard_normal((sum(lens), d)).astype(np.float32)
+    qs = [rng.standard_normal((n, H, d)).astype(np.float32) for n in nqs]
+    ws = [rng.random((n, H)).astype(np.float32) for n in nqs]
+    q = np.concatenate(qs)
+    w = np.concatenate(ws)
+    ends, starts = [], []
+    for b, (L, n) in enumerate(zip(lens, nqs)):
+        e_local = L - n + np.arange(n) + 1
+        ends.append(bases[b] + e_local)
+        starts.append(np.full(n, bases[b]))
+    ends = np.concatenate(ends).astype(np.int32)
+    starts = np.concatenate(starts).astype(np.int32)
+    pi, ps = orc.indexer_topk(q, "f32", None, w, keys, None, k, "dsa", ends, visible_start=starts)
+    r = 0
+    for b, (L, n) in enumerate(zip(lens, nqs)):
+        kb = keys[bases[b]: bases[b] + L]
+        si, ss = orc.indexer_topk(qs[b], "f32", None, ws[b], kb, None, k, "dsa", L - n + np.arange(n) + 1)
+        want = np.where(si >= 0, si + bases[b], -1)
+        np.testing.assert_array_equal(pi[r: r + n], want)
+        np.testing.assert_array_equal(ps[r: r + n].view(np.uint32), ss.view(np.uint32))
+        r += n
+
+
 def test_one_hot_weights_reduce_to_one_head():
     rng = np.random.default_rng(4)
     H, d, n = 5, 16, 40
