@@ -20,6 +20,13 @@ fallback, inputs resident in HBM. Prints ONE JSON line with
                  chunked-prefill protocol), with a random sample per chunk and
                  with the sample taken from the previous chunk's top-k
                  (sec. 3.2 "Sampling"), total time over all chunks.
+  retrieval_e7   the retrieval sweep of sec. 4.1 ("Large-Scale Retrieval
+                 Benchmark"): 64 queries x corpora of 1M, 2M, 4M, 5M passages
+                 of 768-dimensional bf16 embeddings, k = 128, 1024, 4096,
+                 8192; per point the call time, the fused scan's time and its
+                 HBM rate against the 8 TB/s peak, survivors per row, and the
+                 unfused paths (dense scores + radix select; torch GEMM +
+                 torch.topk).
 """
 from __future__ import annotations
 
@@ -199,6 +206,78 @@ def chunked_prefill(name: str, chunk: int, reps: int):
     return res
 
 
+def retrieval_sweep(steps: int):
+    """The sec. 4.1 retrieval sweep on one 5M-passage corpus (smaller corpora
+    are its prefixes; the 64 queries are passages among the first 1M)."""
+    cfg = workloads.CONFIGS["retrieval_e7_bf16_5m"]
+    dev = torch.device("cuda")
+    x = workloads.unit_corpus_gpu(cfg, seed=workloads.CONFIG_SEEDS[cfg.name], device=dev)
+    q, keys = x["q"], x["keys"]
+    qt = q[:, 0, :].t().contiguous()
+    points = []
+    for n in (1000000, 2000000, 4000000, 5000000):
+        kv = keys[:n]
+        for k in (128, 1024, 4096, 8192):
+            evs = [lt.StageEvents() for _ in range(steps)]
+            opts = [lt.make_options(stage_events=e) for e in evs]
+            ws = lt.indexer_topk_workspace(cfg.nq, n, 1, cfg.d, lt._dtype_code(q), "ip", k, opts[0], dev)
+            out = (torch.empty((cfg.nq, k), dtype=torch.int32, device=dev),
+                   torch.empty((cfg.nq, k), dtype=torch.float32, device=dev))
+            run = lambda i: lt.indexer_topk(q, None, kv, k, None, mode="ip", options=opts[i], out=out,  # noqa: E731
+                                            workspace=ws)
+            run(0)
+            torch.cuda.synchronize()
+            t0 = time.perf_counter()
+            for i in range(steps):
+                run(i)
+            torch.cuda.synchronize()
+            ms = (time.perf_counter() - t0) * 1e3 / steps
+            stg = {s_: 0.0 for s_ in lt.STAGES}
+            for e in evs:
+                for s_, v in e.stage_ms().items():
+                    stg[s_] += v / steps
+                e.close()
+            stats = torch.zeros((cfg.nq, 4), dtype=torch.int32, device=dev)
+            lt.indexer_topk(q, None, kv, k, None, mode="ip", options=lt.make_options(row_stats=stats), out=out,
+                            workspace=ws)
+            st = stats.cpu().numpy()
+            gbs = n * cfg.d * 2 / (stg["filter"] * 1e-3) / 1e9
+            p = {"corpus": n, "k": k, "ms": round(ms, 4), "filter_ms": round(stg["filter"], 4),
+                 "stages_ms": {s_: round(v, 4) for s_, v in stg.items()},
+                 "filter_hbm_gbs": round(gbs, 1), "filter_hbm_frac": round(gbs / HBM_PEAK_GBS, 4),
+                 "survivors_per_row": round(float(st[:, 0].mean()), 1), "fallback_rows": int((st[:, 2] != 0).sum())}
+            del ws
+            # unfused: the library's dense scores + radix select, and torch
+            dense = torch.empty((cfg.nq, n), dtype=torch.float32, device=dev)
+
+            def unf():
+                lt.indexer_scores(q, None, kv, mode="ip", out=dense)
+                lt.topk_radix(dense, k)
+
+            p["unfused_ms"] = round(timed_steps(unf, 2, 1), 4)
+            del dense
+
+            def tor():
+                sc = torch.mm(kv, qt)                       # [n, 64] bf16 (fp32 accumulation)
+                torch.topk(sc.float(), k, dim=0)
+
+            p["torch_ms"] = round(timed_steps(tor, 2, 1), 4)
+            torch.cuda.empty_cache()
+            points.append(p)
+            print("[bench] retrieval_e7 N=%d k=%d: %.3f ms (scan %.3f ms, %.0f GB/s), unfused %.3f, torch %.3f" % (
+                n, k, ms, p["filter_ms"], gbs, p["unfused_ms"], p["torch_ms"]), file=sys.stderr, flush=True)
+    del x, q, keys, qt
+    torch.cuda.empty_cache()
+    ref = [p for p in points if p["corpus"] == 5000000 and p["k"] == 1024][0]
+    return {"workload": cfg.name, "num_queries": cfg.nq, "dim": cfg.d, "dtype": "bf16", "mode": "ip",
+            "data": "synthetic unit-normalised Gaussian passages (torch Philox, seeded); queries are corpus passages",
+            "roofline": {"bound": "hbm", "achieved": ref["filter_hbm_gbs"], "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                         "frac": ref["filter_hbm_frac"], "traffic": None,
+                         "kernel": "k_wide_fused (score+filter scan), 5M passages, k = 1024",
+                         "algorithmic_bytes": 5000000 * cfg.d * 2},
+            "points": points}
+
+
 def roofline(cfg, res):
     flops = 2.0 * cfg.h * cfg.d * res["pairs"]
     filt_ms = res["stages"]["filter"]
@@ -265,6 +344,8 @@ def main():
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
     ap.add_argument("--no-unfused", action="store_true", help="skip the unfused baseline")
     ap.add_argument("--no-chunked", action="store_true", help="skip the chunked-prefill measurement")
+    ap.add_argument("--no-retrieval", action="store_true", help="skip the 768-d retrieval sweep")
+    ap.add_argument("--retrieval-only", action="store_true", help="run only the 768-d retrieval sweep")
     ap.add_argument("--cpu-budget", type=float, default=15.0)
     ap.add_argument("--profile-only", default=None, metavar="WORKLOAD",
                     help="run only `steps` fused calls of one workload (for rocprofv3 counter passes)")
@@ -291,7 +372,10 @@ def main():
         return
     if args.profile_only:
         cfg = workloads.CONFIGS[args.profile_only]
-        x = workloads.generate(cfg, seed=workloads.CONFIG_SEEDS[args.profile_only])
+        if cfg.dist == "unit_self" and cfg.nk > workloads.QUERY_POOL:
+            x = workloads.unit_corpus_gpu(cfg, seed=workloads.CONFIG_SEEDS[cfg.name], device="cuda")
+        else:
+            x = workloads.generate(cfg, seed=workloads.CONFIG_SEEDS[args.profile_only])
         d = {kk: (None if v is None else v.to("cuda")) for kk, v in x.items()
              if kk in ("q", "w", "keys", "q_scale", "k_scale", "offsets")}
         for _ in range(max(1, args.steps)):
@@ -301,6 +385,9 @@ def main():
         print(json.dumps({"profiled": args.profile_only, "calls": max(1, args.steps)}))
         return
 
+    if args.retrieval_only:
+        print(json.dumps({"retrieval_e7": retrieval_sweep(max(1, args.steps))}), flush=True)
+        return
     cfg, res = measure("dsa_bf16_128k", args.steps, args.warmup, not args.no_unfused)
     print("[bench] dsa_bf16_128k: %.3f ms/step, stages %s" % (res["ms"], {k: round(v, 3) for k, v in
                                                                          res["stages"].items()}),
@@ -350,6 +437,8 @@ def main():
     if not args.no_chunked:
         line["chunked_prefill"] = [chunked_prefill("dsa_bf16_128k", c, 3) for c in (256, 1024)]
         print("[bench] chunked prefill done", file=sys.stderr, flush=True)
+    if not args.no_retrieval:
+        line["retrieval_e7"] = retrieval_sweep(3)
     if rank0 and not args.no_cpu:
         line["cpu_baseline"] = cpu_oracle_rate("dsa_bf16_128k", args.cpu_budget)
     if rank0:

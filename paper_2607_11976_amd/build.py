@@ -17,7 +17,7 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(HERE, "csrc")
 OUT = os.path.join(HERE, "liblitetopk.so")
 OBJDIR = os.path.join(HERE, "_build")
-SOURCES = ["abi.hip", "select.hip", "score.hip", "sample.hip", "union.hip"]
+SOURCES = ["abi.hip", "select.hip", "score.hip", "sample.hip", "union.hip", "wide.hip"]
 ARCH = os.environ.get("LT_OFFLOAD_ARCH", "gfx950")
 
 

@@ -20,11 +20,14 @@ constexpr int kMaxAutoSplits = 64;
 constexpr size_t kHistLdsBudget = 96 * 1024;
 constexpr size_t kLdsPerBlock = 160 * 1024;   // gfx950 LDS per workgroup
 constexpr int kSampleBlockScores = 64;      // scores-in sample: runs of 64 consecutive keys
+constexpr int kMinSharedSplitKeys = 1024;   // shortest key split of the shared-row (wide) scan
 
 inline size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 
 struct Resolved {
   int m, ns, cap, S, L, E;
+  int LS;                  // candidate lists (and histograms) per row: S, or 1 when shared
+  bool shared;             // the wide scan: one list, histogram and threshold per row
   uint32_t flags;
   uint64_t seed;
   void** ev;
@@ -35,7 +38,7 @@ struct Resolved {
 };
 
 struct Layout {
-  size_t qctl, queue, params, list, samp, cnt, hist, cand, scratch, total;
+  size_t qctl, queue, params, list, samp, cnt, hist, cand, gate, scratch, total;
 };
 
 Layout carve(int nq, int nk, const Resolved& r, bool fused) {
@@ -51,9 +54,10 @@ Layout carve(int nq, int nk, const Resolved& r, bool fused) {
   L.params = take((size_t)nq * sizeof(RowParam));
   L.list = take((size_t)r.ns * 4);
   L.samp = fused ? take((size_t)nq * r.ns * 4) : 0;
-  L.cnt = take((size_t)nq * r.S * 4);
-  L.hist = take((size_t)nq * r.S * r.m * 4);
-  L.cand = take((size_t)nq * r.S * r.cap * 8);
+  L.cnt = take((size_t)nq * r.LS * 4);
+  L.hist = take((size_t)nq * r.LS * r.m * 4);
+  L.cand = take((size_t)nq * r.LS * r.cap * 8);
+  L.gate = r.shared ? take((size_t)nq * 4) : 0;
   L.scratch = fused ? take((size_t)kFallbackGridFused * nk * 4) : 0;
   L.total = off;
   return L;
@@ -71,11 +75,12 @@ void resolve_common(const lt_options* o, int k, Resolved& r) {
   if (!o) o = &d;
   r.m = o->num_bins > 0 ? std::min(o->num_bins, LT_MAX_BINS) : kDefaultBins;
   r.cap = o->capacity > 0 ? o->capacity : std::max(12 * k, 2048);
-  r.flags = o->flags;
+  r.flags = o->flags & (LT_SORTED_OUTPUT | LT_FORCE_FALLBACK);
   r.seed = o->seed;
   r.ev = o->stage_events;
   r.stats = o->row_stats;
   r.E = select_entries(k);
+  r.shared = false;
   r.keys_in = o->sample_keys;
   r.starts = o->visible_start;
   r.status = LT_OK;
@@ -99,16 +104,28 @@ Resolved resolve_fused(const lt_options* o, int nq, int nk, int k, int mode, con
   lt_options d;
   lt_options_default(&d);
   if (!o) o = &d;
-  // per-row LDS histograms share the block's LDS with the key-tile ring
-  const size_t room = kLdsPerBlock - sh.scan_lds - 64;
-  const size_t mcap = std::min(kHistLdsBudget, room) / (4 * (size_t)sh.queries_per_block);
-  if ((size_t)r.m > mcap) r.m = (int)std::max<size_t>(mcap, 1);
+  r.shared = sh.shared_rows != 0;
+  if (!r.shared) {
+    // per-row LDS histograms share the block's LDS with the key-tile ring
+    const size_t room = kLdsPerBlock - sh.scan_lds - 64;
+    const size_t mcap = std::min(kHistLdsBudget, room) / (4 * (size_t)sh.queries_per_block);
+    if ((size_t)r.m > mcap) r.m = (int)std::max<size_t>(mcap, 1);
+  } else if (o->capacity <= 0) {
+    // one list per row collects every split's candidates: an online top-k
+    // over N keys admits about k (1 + ln(N / k)) of them, plus the ones the
+    // sample's threshold lets through before the first refresh
+    r.cap = std::max(16 * k, 65536);
+  }
   r.ns = resolve_sample(o, r, nk, k, mode, true);
   const int steps = (nk + sh.keys_per_step - 1) / sh.keys_per_step;
   const int tiles = (nq + sh.queries_per_block - 1) / sh.queries_per_block;
   int S = 1;
   if (o->key_splits > 0) {
     S = std::min(o->key_splits, std::max(steps, 1));
+  } else if (r.shared) {
+    // the splits share their thresholds, so splitting costs no survivors:
+    // enough blocks for one per CU, each split keeping kMinSharedSplitKeys
+    S = std::max(1, std::min((kTargetBlocks + tiles - 1) / tiles, nk / kMinSharedSplitKeys));
   } else {
     // The fewest key splits whose launch keeps at least 90% of the block
     // slots busy in its last round (one block per CU), each split keeping at
@@ -124,6 +141,7 @@ Resolved resolve_fused(const lt_options* o, int nq, int nk, int k, int mode, con
     }
   }
   r.S = S;
+  r.LS = r.shared ? 1 : S;
   const int per = (nk + S - 1) / S;
   r.L = ((per + sh.keys_per_step - 1) / sh.keys_per_step) * sh.keys_per_step;
   if (r.L == 0) r.L = sh.keys_per_step;
@@ -140,6 +158,7 @@ Resolved resolve_scores(const lt_options* o, int nq, int nk, int k) {
   int S = 1;
   if (o->key_splits > 0) S = o->key_splits;
   r.S = std::max(1, std::min(S, (nk + 255) / 256 + 1));
+  r.LS = r.S;
   const int per = (nk + r.S - 1) / r.S;
   r.L = std::max(256, ((per + 255) / 256) * 256);
   (void)nq;
@@ -239,6 +258,7 @@ int lt_indexer_topk(const void* q, const float* q_scale, const float* w, const v
   uint32_t* hist = reinterpret_cast<uint32_t*>(ws + L.hist);
   int2* cand = reinterpret_cast<int2*>(ws + L.cand);
   float* scratch = reinterpret_cast<float*>(ws + L.scratch);
+  int* gate = reinterpret_cast<int*>(ws + L.gate);
   ScoreArgs a{q, q_scale, w, keys, k_scale, (int)dtype, (int)mode, nq, nk, h, d, offs, r.starts};
 
   hipError_t e;
@@ -250,11 +270,12 @@ int lt_indexer_topk(const void* q, const float* q_scale, const float* w, const v
   if ((e = launch_range(false, samp, r.ns, nq, nk, offs, r.starts, list, r.ns, r.m, k, params, st)) != hipSuccess)
     return hip_status(e);
   record(r, LT_STAGE_FILTER, st);
-  if ((e = launch_fused_scan(a, params, r.S, r.L, r.cap, r.m, k, cnt, hist, cand, st)) != hipSuccess)
-    return hip_status(e);
+  e = r.shared ? launch_wide_fused(a, params, r.S, r.L, r.cap, r.m, k, gate, cnt, hist, cand, st)
+               : launch_fused_scan(a, params, r.S, r.L, r.cap, r.m, k, cnt, hist, cand, st);
+  if (e != hipSuccess) return hip_status(e);
   record(r, LT_STAGE_SELECT, st);
-  if ((e = launch_select(params, cnt, hist, cand, nq, r.S, r.cap, r.m, k, r.E, r.flags, out_idx, out_scores, qctl,
-                         queue, r.stats, st)) != hipSuccess)
+  if ((e = launch_select(params, cnt, hist, cand, nq, r.LS, r.cap, r.m, k, r.E, r.flags | (r.shared ? kSelKeyed : 0u),
+                         out_idx, out_scores, qctl, queue, r.stats, st)) != hipSuccess)
     return hip_status(e);
   record(r, LT_STAGE_FALLBACK, st);
   if ((e = launch_fused_fallback(a, k, r.flags, qctl, queue, scratch, kFallbackGridFused, out_idx, out_scores,

@@ -142,20 +142,25 @@ __device__ __forceinline__ uint32_t wave_sum(uint32_t v) {
   return v;
 }
 
+// OR of a 32-bit value over the wave: inclusive scans in rows of 16 lanes,
+// then across rows (row_bcast); lane 63 ends with the total.
+__device__ __forceinline__ uint32_t wave_or(uint32_t v) {
+  v |= (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x111, 0xF, 0xF, false);  // row_shr:1
+  v |= (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x112, 0xF, 0xF, false);  // row_shr:2
+  v |= (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x114, 0xF, 0xF, false);  // row_shr:4
+  v |= (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x118, 0xF, 0xF, false);  // row_shr:8
+  v |= (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x142, 0xA, 0xF, false);  // row_bcast:15
+  v |= (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x143, 0xC, 0xF, false);  // row_bcast:31
+  return (uint32_t)__builtin_amdgcn_readlane((int)v, 63);
+}
+
 // Threshold refresh (sec. 3.2 "Threshold Refresh"): walk the histogram from
 // the top bin down until the running count reaches k. Returns the largest bin
 // b with sum_{b' >= b} hist[b'] >= k, or -1 if there is none, and the count of
-// the bins strictly above it in *above. Called by a whole wave; lane l covers
-// bins [4l, 4l + 4). `hist` may be LDS or global memory.
-template <typename P>
-__device__ __forceinline__ int wave_threshold(P hist, int m, uint32_t k, uint32_t* above) {
+// the bins strictly above it in *above. Called by a whole wave; lane l holds
+// bins [4l, 4l + 4) in h[] (zero past the last bin).
+__device__ __forceinline__ int wave_threshold_vals(const uint32_t (&h)[4], uint32_t k, uint32_t* above) {
   const int l = lane_id();
-  uint32_t h[4];
-#pragma unroll
-  for (int j = 0; j < 4; ++j) {
-    int b = 4 * l + j;
-    h[j] = b < m ? hist[b] : 0u;
-  }
   uint32_t tot = h[0] + h[1] + h[2] + h[3];
   uint32_t excl = wave_suffix_sum_excl(tot);
   uint32_t suf[4];
@@ -169,13 +174,33 @@ __device__ __forceinline__ int wave_threshold(P hist, int m, uint32_t k, uint32_
   int tau = nge - 1;
   // count strictly above tau: suffix(tau + 1), or the total when tau = -1
   uint32_t a = 0;
-  int want = tau + 1;  // bin whose suffix we need (m => 0)
+  int want = tau + 1;  // bin whose suffix we need (past the last bin => 0)
 #pragma unroll
   for (int j = 0; j < 4; ++j)
     if (4 * l + j == want) a = suf[j];
-  a = wave_sum(a);  // exactly one lane (or none when want >= m) contributes
+  a = wave_sum(a);  // exactly one lane (or none when want is past the end) contributes
   if (above) *above = a;
   return tau;
+}
+
+// The same walk over a histogram of m bins in memory (LDS or global).
+template <typename P>
+__device__ __forceinline__ int wave_threshold(P hist, int m, uint32_t k, uint32_t* above) {
+  const int l = lane_id();
+  uint32_t h[4];
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    int b = 4 * l + j;
+    h[j] = b < m ? hist[b] : 0u;
+  }
+  return wave_threshold_vals(h, k, above);
+}
+
+// Inverse of ord_key on its image: the float with that order key (NaN maps
+// back to the canonical quiet NaN, and -0 was already merged into +0).
+__device__ __forceinline__ float ord_inv(uint32_t u) {
+  if (u == 0u) return __builtin_nanf("");
+  return __uint_as_float((u & 0x80000000u) ? (u & 0x7FFFFFFFu) : ~u);
 }
 
 }  // namespace lt

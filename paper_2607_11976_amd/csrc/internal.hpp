@@ -65,6 +65,8 @@ struct ScoreShape {
   int keys_per_step;      // keys per LDS tile
   int threads;            // block size
   size_t scan_lds;        // LDS bytes of the scan (tiles), excluding histograms
+  int shared_rows;        // 1: all key splits of a row share one histogram,
+                          // threshold and candidate list (the wide scan)
 };
 ScoreShape score_shape(int dtype, int mode, int h, int d);
 
@@ -79,5 +81,23 @@ hipError_t launch_fused_scan(const ScoreArgs& a, const RowParam* params, int S, 
 hipError_t launch_fused_fallback(const ScoreArgs& a, int k, uint32_t flags, const uint32_t* qctl,
                                  const int32_t* queue, float* scratch, int grid, int32_t* out_i,
                                  float* out_s, hipStream_t st);
+
+// ---- wide-vector scan (wide.hip): bf16, one head, long vectors ----
+// wide_shape(...).supported is 0 for shapes the wide scan does not build.
+ScoreShape wide_shape(int dtype, int mode, int h, int d);
+hipError_t launch_wide_sample(const ScoreArgs& a, const int32_t* list, int ns, float* samp, hipStream_t st);
+hipError_t launch_wide_dense(const ScoreArgs& a, float* out, int64_t ld, hipStream_t st);
+// Fused scan with shared row state: gate [nq] (published threshold bins),
+// tail [nq] (= per-row candidate counts), hist [nq, m], cand [nq, cap]; gate,
+// tail and hist are initialised here.
+hipError_t launch_wide_fused(const ScoreArgs& a, const RowParam* params, int S, int L, int cap, int m, int k,
+                             int* gate, uint32_t* tail, uint32_t* hist, int2* cand, hipStream_t st);
+hipError_t launch_wide_fallback(const ScoreArgs& a, int k, uint32_t flags, const uint32_t* qctl,
+                                const int32_t* queue, float* scratch, int grid, int32_t* out_i, float* out_s,
+                                hipStream_t st);
+
+// k_select flag (internal): candidate lists are not in key order (the wide
+// scan's shared lists), so equal scores are ordered by the key itself.
+constexpr uint32_t kSelKeyed = 1u << 30;
 
 }  // namespace lt

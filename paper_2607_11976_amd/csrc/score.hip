@@ -365,18 +365,6 @@ __device__ __forceinline__ void schedule_half() {
 // compiler cannot tell the histogram from the tile ring): LDS operations of
 // one wave complete in order, so the wave's later histogram reads still see
 // the increment, and no other wave reads this wave's histogram rows.
-// OR of a 32-bit value over the wave: inclusive scans in rows of 16 lanes,
-// then across rows (row_bcast); lane 63 ends with the total.
-__device__ __forceinline__ uint32_t wave_or(uint32_t v) {
-  v |= (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x111, 0xF, 0xF, false);  // row_shr:1
-  v |= (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x112, 0xF, 0xF, false);  // row_shr:2
-  v |= (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x114, 0xF, 0xF, false);  // row_shr:4
-  v |= (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x118, 0xF, 0xF, false);  // row_shr:8
-  v |= (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x142, 0xA, 0xF, false);  // row_bcast:15
-  v |= (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x143, 0xC, 0xF, false);  // row_bcast:31
-  return (uint32_t)__builtin_amdgcn_readlane((int)v, 63);
-}
-
 __device__ __forceinline__ void lds_inc(uint32_t* p) {
   const uint32_t a = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) uint32_t*)p;
   asm volatile("ds_add_u32 %0, %1" ::"v"(a), "v"(1u) : "memory");
@@ -993,21 +981,22 @@ static bool with_cfg(int dt, int mode, int h, int d, F&& f) {
 }
 
 ScoreShape score_shape(int dtype, int mode, int h, int d) {
-  ScoreShape s{0, 0, 0, 0, 0};
-  with_cfg(dtype, mode, h, d, [&]<class C>() {
+  ScoreShape s{0, 0, 0, 0, 0, 0};
+  const bool found = with_cfg(dtype, mode, h, d, [&]<class C>() {
     s.supported = 1;
     s.queries_per_block = C::QT;
     s.keys_per_step = C::KT;
     s.threads = C::NTHREADS;
     s.scan_lds = C::SCAN_LDS;
   });
-  return s;
+  return found ? s : wide_shape(dtype, mode, h, d);
 }
 
 static constexpr int kSlice = 8192;   // positions per block in the sample / dense scorers
 static constexpr int kSampleBlocks = 256;  // the sample scorer aims at one block per CU at least
 
 hipError_t launch_sample_scores(const ScoreArgs& a, const int32_t* list, int ns, float* samp, hipStream_t st) {
+  if (wide_shape(a.dtype, a.mode, a.h, a.d).supported) return launch_wide_sample(a, list, ns, samp, st);
   hipError_t err = hipErrorInvalidValue;
   with_cfg(a.dtype, a.mode, a.h, a.d, [&]<class C>() {
     // few query tiles (a short chunk): cut the sample into more slices so
@@ -1029,6 +1018,7 @@ hipError_t launch_sample_scores(const ScoreArgs& a, const int32_t* list, int ns,
 }
 
 hipError_t launch_dense_scores(const ScoreArgs& a, float* out, int64_t ld, hipStream_t st) {
+  if (wide_shape(a.dtype, a.mode, a.h, a.d).supported) return launch_wide_dense(a, out, ld, st);
   hipError_t err = hipErrorInvalidValue;
   with_cfg(a.dtype, a.mode, a.h, a.d, [&]<class C>() {
     dim3 grid((a.nq + C::QT - 1) / C::QT, (a.nk + kSlice - 1) / kSlice);
@@ -1064,6 +1054,8 @@ hipError_t launch_fused_scan(const ScoreArgs& a, const RowParam* params, int S, 
 hipError_t launch_fused_fallback(const ScoreArgs& a, int k, uint32_t flags, const uint32_t* qctl,
                                  const int32_t* queue, float* scratch, int grid, int32_t* out_i, float* out_s,
                                  hipStream_t st) {
+  if (wide_shape(a.dtype, a.mode, a.h, a.d).supported)
+    return launch_wide_fallback(a, k, flags, qctl, queue, scratch, grid, out_i, out_s, st);
   hipError_t err = hipErrorInvalidValue;
   with_cfg(a.dtype, a.mode, a.h, a.d, [&]<class C>() {
     size_t lds = C::SCAN_LDS;

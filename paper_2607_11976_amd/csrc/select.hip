@@ -228,6 +228,9 @@ __global__ __launch_bounds__(kSelThreads) void k_select(
   uint64_t* ent = reinterpret_cast<uint64_t*>(lds + kMaxBins * 4 + 64);  // [E]
   const int row = blockIdx.x, tid = threadIdx.x;
   const bool sorted = flags & LT_SORTED_OUTPUT;
+  // keyed: the lists are not in key order, so the tie-break position is the
+  // key itself and the output is rebuilt from the sort entries
+  const bool keyed = flags & kSelKeyed;
   int32_t* oi = out_i + (int64_t)row * k;
   float* os = out_s + (int64_t)row * k;
 
@@ -297,7 +300,8 @@ __global__ __launch_bounds__(kSelThreads) void k_select(
       }
       uint32_t tot;
       uint32_t ex = block_scan_excl<kSelThreads>(((uint32_t)ab << 16) | (uint32_t)ti, tmp, &tot);
-      const uint32_t gpos = (uint32_t)s * (uint32_t)cap + i;  // increases with key index
+      // increases with the key index (keyed: it is the key index)
+      const uint32_t gpos = keyed ? (uint32_t)ce.x : (uint32_t)s * (uint32_t)cap + i;
       if (sorted) {
         if (ab || ti) {
           uint32_t q = run_above + run_tie + (ex >> 16) + (ex & 0xFFFFu);
@@ -336,6 +340,11 @@ __global__ __launch_bounds__(kSelThreads) void k_select(
   const uint32_t take = sorted ? min(nent, (uint32_t)k) : min(need, nent);
   for (uint32_t i = tid; i < take; i += kSelThreads) {
     uint32_t gp = comp_pos(ent[i]);
+    if (keyed) {
+      oi[first + i] = (int32_t)gp;
+      os[first + i] = ord_inv((uint32_t)(ent[i] >> 32));
+      continue;
+    }
     uint32_t s = gp / (uint32_t)cap, j = gp - s * (uint32_t)cap;
     int2 ce = cand[((int64_t)row * S + s) * cap + j];
     oi[first + i] = ce.x;

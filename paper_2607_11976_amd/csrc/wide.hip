@@ -1,0 +1,647 @@
+// Wide-vector scan for the paper's retrieval shapes (sec. 4.1 "Large-Scale
+// Retrieval Benchmark": 768-dimensional passage embeddings, batches of 64
+// queries, corpora of millions of items, k up to 8192).
+//
+// The 128-dimensional scorer keeps each wave's queries stationary in VGPRs;
+// at 768 dimensions 32 queries alone would take 192 VGPRs. This scan turns
+// the layout around:
+//  * a block owns 64 queries, held in LDS as ready-made MFMA A fragments
+//    (2 M tiles x D/16 K steps x 1 KB, read conflict-free, one 16-byte read
+//    per lane per fragment);
+//  * each wave streams its own tiles of 32 items straight from HBM into B
+//    fragments (no LDS staging), keeping PD fragments in flight in a register
+//    ring that runs across tile boundaries;
+//  * a wave tile is the whole 64 x 32 score block, so each item is read from
+//    HBM once per block and the waves of a block need no barrier in the scan.
+// 64 queries make 64 flops per item byte, a fifth of the bf16 MFMA ridge
+// point: the scan is bound by HBM, and the design goal is bytes in flight.
+//
+// Fused filter (sec. 3.2 "Filtering", "Threshold Refresh"). A 64-query batch
+// needs about 256 key splits to fill the GPU, and a threshold refreshed from
+// one split's own histogram can only reach that split's local top-k, which
+// for large k admits most of the split. Here all splits of a row share one
+// histogram, one threshold bin and one candidate list in global memory (the
+// paper's per-CTA structure widened to the grid):
+//  * a tile's passing candidates reserve their slots with one atomic add per
+//    query and count themselves in the row's histogram with atomic adds
+//    whose results nobody waits for;
+//  * waves recompute the threshold bin of rows they added candidates to by
+//    walking the shared histogram from the top, and publish it with an atomic
+//    max; every wave re-reads the published bins once per tile.
+// A published bin b had, when it was computed, at least k counted candidates
+// in bins >= b. Counts only grow, so b never exceeds the final threshold bin
+// the select stage computes, and every key a gate drops lies below it. A
+// stale bin only loosens the gate.
+#include <utility>
+
+#include "internal.hpp"
+#include "select_dev.hpp"
+
+namespace lt {
+
+typedef __bf16 wbf16x8_t __attribute__((ext_vector_type(8)));
+typedef float wf32x16_t __attribute__((ext_vector_type(16)));
+typedef int wi32x4_t __attribute__((ext_vector_type(4)));
+
+template <int N, class F>
+__device__ __forceinline__ void wstatic_for(F&& f) {
+  [&]<int... I>(std::integer_sequence<int, I...>) {
+    (f(std::integral_constant<int, I>{}), ...);
+  }(std::make_integer_sequence<int, N>{});
+}
+
+template <int D_, bool RELU_>
+struct WCfg {
+  static constexpr int D = D_;
+  static constexpr bool RELU = RELU_;
+  static constexpr int KS = D / 16;          // bf16 32x32x16 K steps per item
+  static constexpr int ROWB = D * 2;         // bytes per item row
+  static constexpr int MT = 2;               // M tiles of 32 queries
+  static constexpr int QT = 32 * MT;         // queries per block
+  static constexpr int WAVES = 8;
+  static constexpr int NTHREADS = WAVES * kWave;
+  static constexpr int KT = 32;              // items per wave tile
+  static constexpr int STEP = KT * WAVES;    // items per block step
+  static constexpr int PD = 16;              // B fragments in flight per wave (16 KB)
+  static constexpr int NI = 16 * MT;         // scores per lane per tile
+  static constexpr int Q_LDS = MT * KS * kWave * 16;
+  static_assert(D % 16 == 0 && KS % PD == 0, "the fragment ring must divide the K steps");
+  static_assert(NI == 32, "one bit per score item");
+};
+
+// Query (within the block) of score item it = 16 * mt + v, accumulator
+// register v of M tile mt, in lane half h: row 8 * (v / 4) + 4 * h + v % 4 of
+// the M tile. Each query is exactly one (item, half) pair.
+__host__ __device__ constexpr int wq_of(int it, int h) {
+  return 32 * (it >> 4) + 8 * ((it & 15) >> 2) + 4 * h + (it & 3);
+}
+
+// Queries q0 .. q0 + 63 into LDS as A fragments: fragment (mt, ks) is 1 KB at
+// ((mt * KS + ks) * 64) * 16, lane l's 16 bytes are elements
+// [16 ks + 8 (l / 32), +8) of query 32 mt + l % 32 (zero past the last query).
+template <class C>
+__device__ __forceinline__ void wide_load_q(uint8_t* qlds, const ScoreArgs& a, int q0) {
+  const uint16_t* q = static_cast<const uint16_t*>(a.q);
+  for (int u = threadIdx.x; u < C::MT * C::KS * kWave; u += C::NTHREADS) {
+    const int f = u / kWave, l = u % kWave, mt = f / C::KS, ks = f % C::KS;
+    const int t = q0 + 32 * mt + (l & 31);
+    wi32x4_t v = {0, 0, 0, 0};
+    if (t < a.nq) v = *reinterpret_cast<const wi32x4_t*>(q + (int64_t)t * C::D + 16 * ks + 8 * (l >> 5));
+    *reinterpret_cast<wi32x4_t*>(qlds + (size_t)u * 16) = v;
+  }
+  __syncthreads();
+}
+
+// Weight of the query of each score item (1 without weights, 0 past the end).
+template <class C>
+__device__ __forceinline__ void wide_weights(float (&wv)[C::NI], const ScoreArgs& a, int q0) {
+  const int h = lane_id() >> 5;
+#pragma unroll
+  for (int it = 0; it < C::NI; ++it) {
+    const int t = q0 + wq_of(it, h);
+    wv[it] = t < a.nq ? (a.w ? a.w[t] : 1.0f) : 0.0f;
+  }
+}
+
+struct WSrcContig {
+  __device__ int key(int i) const { return i; }
+};
+struct WSrcList {
+  const int32_t* list;
+  __device__ int key(int i) const {
+    const int v = list[i];
+    return v < 0 ? 0 : v;
+  }
+};
+
+// One wave's share of the scan over positions [kbeg, kend) of `src`: tiles
+// wave, wave + WAVES, ... of 32 positions. Lane (r32, h) reads item
+// kbeg + 32 t + r32 (clamped to the last position; consumers mask it) and,
+// at K step ks, its 16 bytes at 32 ks + 16 h: the B operand layout of the
+// 32x32x16 MFMA. The ring slot of K step ks is ks % PD; the last PD steps of
+// a tile load the first PD steps of the wave's next tile (or re-read the same
+// tile after the last one; those loads are never used). Scores are
+// w * ReLU(q . k) (DSA with one head) or w * (q . k), computed as
+// fma(w, x, +0) so that a zero product is +0.
+template <class C, class Src, class Sink>
+__device__ __forceinline__ void wide_scan(const ScoreArgs& a, const Src& src, int kbeg, int kend,
+                                          const uint8_t* qlds, const float (&wv)[C::NI], Sink& sink) {
+  const int l = lane_id(), h = l >> 5, r32 = l & 31;
+  const int wave = __builtin_amdgcn_readfirstlane((int)(threadIdx.x / kWave));
+  const int ntiles = kend > kbeg ? (kend - kbeg + C::KT - 1) / C::KT : 0;
+  if (wave >= ntiles) return;
+  const uint8_t* keys = static_cast<const uint8_t*>(a.keys);
+  auto row_of = [&](int tile) {
+    const int i = min(kbeg + tile * C::KT + r32, kend - 1);
+    return keys + (int64_t)src.key(i) * C::ROWB + h * 16;
+  };
+  auto ldb = [](const uint8_t* p) { return *reinterpret_cast<const wbf16x8_t*>(p); };
+  const uint8_t* rp = row_of(wave);
+  wbf16x8_t bq[C::PD];
+  wstatic_for<C::PD>([&](auto J) { bq[J] = ldb(rp + J * 32); });
+  for (int t = wave; t < ntiles; t += C::WAVES) {
+    const int tn = t + C::WAVES < ntiles ? t + C::WAVES : t;
+    const uint8_t* np = row_of(tn);
+    sink.begin();
+    // the A fragments are the same every tile; an opaque offset keeps the
+    // compiler from hoisting all of them (KS * MT * 4 VGPRs) out of the loop
+    int qoff = l * 16;
+    asm volatile("" : "+v"(qoff));
+    const uint8_t* qa = qlds + qoff;
+    wf32x16_t acc[C::MT];
+#pragma unroll
+    for (int mt = 0; mt < C::MT; ++mt) acc[mt] = wf32x16_t{};
+    wstatic_for<C::KS>([&](auto KSI) {
+      constexpr int ks = decltype(KSI)::value;
+      const wbf16x8_t b = bq[ks % C::PD];
+      wstatic_for<C::MT>([&](auto MTI) {
+        constexpr int mt = decltype(MTI)::value;
+        const wbf16x8_t af = *reinterpret_cast<const wbf16x8_t*>(qa + (mt * C::KS + ks) * (kWave * 16));
+        acc[mt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af, b, acc[mt], 0, 0, 0);
+      });
+      constexpr int nx = ks + C::PD;
+      if constexpr (nx < C::KS) bq[ks % C::PD] = ldb(rp + nx * 32);
+      else bq[ks % C::PD] = ldb(np + (nx - C::KS) * 32);
+    });
+    // Issue order: the A fragments one K step ahead, then per K step its two
+    // MFMAs, the B load PD steps ahead and the next step's A fragments.
+    // Left alone, the scheduler sinks each B load down to its use, which
+    // collapses the ring to one or two fragments in flight.
+    __builtin_amdgcn_sched_group_barrier(0x100, C::MT, 0);  // DS read
+    wstatic_for<C::KS>([&](auto) {
+      __builtin_amdgcn_sched_group_barrier(0x008, C::MT, 0);  // MFMA
+      __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);      // VMEM read
+      __builtin_amdgcn_sched_group_barrier(0x100, C::MT, 0);  // DS read
+    });
+    float sc[C::NI];
+#pragma unroll
+    for (int it = 0; it < C::NI; ++it) {
+      const float x = acc[it >> 4][it & 15];
+      sc[it] = fmaf(wv[it], C::RELU ? __builtin_elementwise_maximum(x, 0.0f) : x, 0.0f);
+    }
+    sink.consume(kbeg + t * C::KT, kend, sc);
+    rp = np;
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Sinks. begin() runs before a tile's MFMAs, consume(k0, kend, sc) after them
+// with the lane's scores of positions k0 + lane % 32.
+// ---------------------------------------------------------------------------
+
+// Every score to out[t * ld + position] (sample and dense scorers).
+template <class C>
+struct WideDenseSink {
+  float* out;
+  int64_t ld;
+  int qbase, nq;
+  __device__ void begin() {}
+  __device__ void consume(int k0, int kend, const float (&sc)[C::NI]) {
+    const int h = lane_id() >> 5, pos = k0 + (lane_id() & 31);
+    if (pos >= kend) return;
+#pragma unroll
+    for (int it = 0; it < C::NI; ++it) {
+      const int t = qbase + wq_of(it, h);
+      if (t < nq) out[(int64_t)t * ld + pos] = sc[it];
+    }
+  }
+};
+
+// The scores of one query (the fallback's re-score): item it_t of half h_t.
+template <class C>
+struct WideRowSink {
+  float* out;
+  int it_t, h_t;
+  __device__ void begin() {}
+  __device__ void consume(int k0, int kend, const float (&sc)[C::NI]) {
+    const int h = lane_id() >> 5, pos = k0 + (lane_id() & 31);
+    float v = 0.0f;
+#pragma unroll
+    for (int it = 0; it < C::NI; ++it)
+      if (it == it_t) v = sc[it];
+    if (h == h_t && pos < kend) out[pos] = v;
+  }
+};
+
+__device__ __forceinline__ int wload(const int* p) {
+  return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ uint32_t wload(const uint32_t* p) {
+  return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+// Fused filter with the row state shared by all key splits (see the top of
+// the file). Lane q holds the state of query qbase + q: bin map (delta, c),
+// visible range [s, e), current threshold bin tau and its score-domain gate
+// T (the GroupedSink bound: bin(fma(I, delta, c)) >= tau holds for every
+// I >= (tau - c) / delta, lowered by far more than its rounding error, so a
+// compare never drops a key whose bin is >= tau; a key let through just below
+// the bin edge is written and counted in its true bin). tq[it] is T of the
+// query of item it in the lane's half.
+template <class C>
+struct WideFusedSink {
+  float delta_v, c_v, t_v;
+  int tau_v, e_v, s_v, gate_next;
+  uint32_t pend_v;      // candidates of query q counted since its last refresh
+  float tq[C::NI];
+  bool ungated;         // some row of the block has no gate (tau = -1)
+  int rq0, rq1;         // rows whose histograms were read for a refresh (-1: none)
+  int rot;              // where this wave's search for rows to refresh starts
+  uint32_t rh0[4], rh1[4];
+  int* gate;            // [nq] published threshold bins
+  uint32_t* hist;       // [nq, m] shared histograms
+  uint32_t* tail;       // [nq] candidates reserved per row
+  int2* cand;           // [nq, cap] (key, score) lists
+  int qbase, nq, cap, m, k;
+
+  __device__ static float gate_floor(float delta, float c, int tau) {
+    if (tau < 0) return -__builtin_inff();
+    const float t = (float)tau, i0 = (t - c) / delta;
+    const float err = ((fabsf(t) + fabsf(c)) / delta + fabsf(i0)) * 0x1p-20f;
+    return i0 - err;
+  }
+
+  __device__ void init(const ScoreArgs& a, const RowParam* params, int kend) {
+    const int l = lane_id(), t = qbase + l;
+    RowRange rr{0, 0};
+    float dl = 1.0f, c = 0.0f;
+    int t0 = -1;
+    if (t < nq) {
+      rr = row_range(a.offs, a.starts, t, a.nk);
+      const RowParam p = params[t];
+      dl = p.delta;
+      c = p.c;
+      t0 = p.tau0;
+    }
+    e_v = rr.e < kend ? rr.e : kend;
+    s_v = rr.s;
+    delta_v = dl;
+    c_v = c;
+    tau_v = t0;
+    gate_next = t0;
+    pend_v = 0;
+    rq0 = rq1 = -1;
+    // waves of the grid start their refresh rounds at different rows, so
+    // that every row is refreshed about equally often
+    rot = (int)((blockIdx.x * C::WAVES + threadIdx.x / kWave) * 2) & (kWave - 1);
+    update_gates();
+  }
+
+  __device__ void update_gates() {
+    const int l = lane_id(), h = l >> 5;
+    const bool valid = qbase + l < nq;
+    t_v = valid ? gate_floor(delta_v, c_v, tau_v) : __builtin_inff();
+    ungated = __ballot(valid && tau_v < 0) != 0;
+    wstatic_for<C::NI>([&](auto I) {
+      constexpr int it = decltype(I)::value;
+      const float x0 = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, t_v), wq_of(it, 0)));
+      const float x1 = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, t_v), wq_of(it, 1)));
+      tq[it] = h ? x1 : x0;
+    });
+  }
+
+  // the published bins, read while the tile's MFMAs run
+  __device__ void begin() {
+    const int t = qbase + lane_id();
+    gate_next = t < nq ? wload(gate + t) : -1;
+  }
+
+  // the threshold bin of row qbase + q from its histogram read one tile ago
+  __device__ bool finish_refresh(int q, const uint32_t (&hv)[4]) {
+    const int b = wave_threshold_vals(hv, (uint32_t)k, nullptr);
+    const int cur = __builtin_amdgcn_readlane(tau_v, q);
+    if (b <= cur) return false;
+    if (lane_id() == 0) __hip_atomic_fetch_max(gate + qbase + q, b, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    tau_v = lane_id() == q ? b : tau_v;
+    return true;
+  }
+
+  __device__ void start_refresh(int q, uint32_t (&hv)[4]) {
+    const uint32_t* hr = hist + (int64_t)(qbase + q) * m;
+    const int l = lane_id();
+#pragma unroll
+    for (int j = 0; j < 4; ++j) hv[j] = 4 * l + j < m ? wload(hr + 4 * l + j) : 0u;
+    pend_v = l == q ? 0u : pend_v;
+  }
+
+  __device__ bool lane_pass(int it, int key, uint32_t bits, int qa, int qb) const {
+    const int h = lane_id() >> 5;
+    const int ea = __builtin_amdgcn_readlane(e_v, qa), eb = __builtin_amdgcn_readlane(e_v, qb);
+    const int sa = __builtin_amdgcn_readlane(s_v, qa), sb = __builtin_amdgcn_readlane(s_v, qb);
+    return ((bits >> it) & 1u) && key < (h ? eb : ea) && key >= (h ? sb : sa);
+  }
+
+  // write-back of the items in `items` (wave-uniform bit set of score items
+  // some lane passed; bits = this lane's)
+  __device__ void emit(int key, uint32_t bits, uint32_t items, const float (&sc)[C::NI]) {
+    typedef float fNI __attribute__((ext_vector_type(C::NI)));
+    const int l = lane_id(), h = l >> 5;
+    fNI scv;
+#pragma unroll
+    for (int it = 0; it < C::NI; ++it) scv[it] = sc[it];
+    // passes per query (a query is one item of one lane half)
+    uint32_t cnt_v = 0;
+    for (uint32_t rem = items; rem; rem &= rem - 1) {
+      const int it = __builtin_ctz(rem), qa = wq_of(it, 0), qb = qa + 4;
+      const uint64_t m2 = __ballot(lane_pass(it, key, bits, qa, qb));
+      const uint32_t lo = (uint32_t)__popcll(m2 & 0xFFFFFFFFull), hi = (uint32_t)__popcll(m2 >> 32);
+      cnt_v = l == qa ? lo : (l == qb ? hi : cnt_v);
+    }
+    // one slot reservation per query with passes
+    uint32_t base_v = 0;
+    if (cnt_v != 0)
+      base_v = __hip_atomic_fetch_add(tail + qbase + l, cnt_v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    pend_v |= cnt_v;
+    for (uint32_t rem = items; rem; rem &= rem - 1) {
+      const int it = __builtin_ctz(rem), qa = wq_of(it, 0), qb = qa + 4;
+      const bool pass = lane_pass(it, key, bits, qa, qb);
+      const uint64_t m2 = __ballot(pass);
+      const uint32_t lo = (uint32_t)__popcll(m2 & 0xFFFFFFFFull);
+      const uint32_t ba = (uint32_t)__builtin_amdgcn_readlane((int)base_v, qa);
+      const uint32_t bb = (uint32_t)__builtin_amdgcn_readlane((int)base_v, qb);
+      const float da = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, delta_v), qa));
+      const float db = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, delta_v), qb));
+      const float ca = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, c_v), qa));
+      const float cb = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, c_v), qb));
+      if (pass) {
+        const float s = scv[it];
+        const uint32_t pos = h ? bb + mbcnt64(m2) - lo : ba + mbcnt64(m2);
+        const int64_t t = qbase + (h ? qb : qa);
+        if (pos < (uint32_t)cap) cand[t * cap + pos] = make_int2(key, __float_as_int(s));
+        const float x = fmaf(s, h ? db : da, h ? cb : ca);
+        if (x >= 0.0f)
+          __hip_atomic_fetch_add(hist + t * m + min(__float2int_rz(x), m - 1), 1u, __ATOMIC_RELAXED,
+                                 __HIP_MEMORY_SCOPE_AGENT);
+      }
+    }
+  }
+
+  __device__ void consume(int k0, int kend, const float (&sc)[C::NI]) {
+    const int l = lane_id(), key = k0 + (l & 31);
+    // 1. thresholds: the refresh whose histograms were read one tile ago,
+    //    then whatever other waves published
+    bool moved = false;
+    if (rq0 >= 0) moved |= finish_refresh(rq0, rh0);
+    if (rq1 >= 0) moved |= finish_refresh(rq1, rh1);
+    rq0 = rq1 = -1;
+    if (__ballot(gate_next > tau_v) != 0) {
+      tau_v = max(tau_v, gate_next);
+      moved = true;
+    }
+    if (moved) update_gates();
+    // 2. gate. Fast path on the vector ALU: the largest margin score - T of
+    //    the lane (a NaN score only matters to an ungated row, and then the
+    //    fast path is skipped)
+    bool any = true;
+    if (!ungated) {
+      float mx = -__builtin_inff();
+#pragma unroll
+      for (int it = 0; it < C::NI; ++it) mx = fmaxf(mx, sc[it] - tq[it]);
+      any = __ballot(mx >= 0.0f) != 0;
+    }
+    if (any) {
+      uint32_t bits = 0;
+#pragma unroll
+      for (int it = 0; it < C::NI; ++it) bits |= !(sc[it] < tq[it]) ? (1u << it) : 0u;
+      if (key >= kend) bits = 0;
+      const uint32_t items = wave_or(bits);
+      if (items) emit(key, bits, items, sc);
+    }
+    // 3. read the histograms of up to two rows this wave added to, the
+    //    next ones at or after `rot` (cyclically)
+    const uint64_t pm = __ballot(pend_v != 0);
+    if (pm) {
+      uint64_t r = rot ? (pm >> rot) | (pm << (kWave - rot)) : pm;
+      rq0 = (__builtin_ctzll(r) + rot) & (kWave - 1);
+      start_refresh(rq0, rh0);
+      r &= r - 1;
+      if (r) {
+        rq1 = (__builtin_ctzll(r) + rot) & (kWave - 1);
+        start_refresh(rq1, rh1);
+      }
+      rot = ((rq1 >= 0 ? rq1 : rq0) + 1) & (kWave - 1);
+    }
+  }
+};
+
+// ---------------------------------------------------------------------------
+// Kernels
+// ---------------------------------------------------------------------------
+template <class C>
+__global__ __launch_bounds__(C::NTHREADS) void k_wide_sample(ScoreArgs a, const int32_t* list, int ns, float* samp,
+                                                             int slice) {
+  extern __shared__ __align__(16) uint8_t lds[];
+  const int q0 = blockIdx.x * C::QT;
+  const int kb = blockIdx.y * slice, ke = min(kb + slice, ns);
+  wide_load_q<C>(lds, a, q0);
+  float wv[C::NI];
+  wide_weights<C>(wv, a, q0);
+  WideDenseSink<C> sink{samp, ns, q0, a.nq};
+  wide_scan<C>(a, WSrcList{list}, kb, ke, lds, wv, sink);
+}
+
+template <class C>
+__global__ __launch_bounds__(C::NTHREADS) void k_wide_dense(ScoreArgs a, float* out, int64_t ld, int slice) {
+  extern __shared__ __align__(16) uint8_t lds[];
+  const int q0 = blockIdx.x * C::QT;
+  const int kb = blockIdx.y * slice, ke = min(kb + slice, a.nk);
+  wide_load_q<C>(lds, a, q0);
+  float wv[C::NI];
+  wide_weights<C>(wv, a, q0);
+  WideDenseSink<C> sink{out, ld, q0, a.nq};
+  wide_scan<C>(a, WSrcContig{}, kb, ke, lds, wv, sink);
+}
+
+// Shared row state: empty histograms and lists, published bins = the sample's.
+__global__ void k_wide_init(const RowParam* params, int nq, int m, int* gate, uint32_t* tail, uint32_t* hist) {
+  const int64_t n = (int64_t)nq * m, stride = (int64_t)gridDim.x * blockDim.x;
+  const int64_t i0 = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  for (int64_t i = i0; i < n; i += stride) hist[i] = 0u;
+  for (int64_t i = i0; i < nq; i += stride) {
+    tail[i] = 0u;
+    gate[i] = params[i].tau0;
+  }
+}
+
+template <class C>
+__global__ __launch_bounds__(C::NTHREADS) void k_wide_fused(ScoreArgs a, const RowParam* params, int S, int L, int cap,
+                                                            int m, int k, int* gate, uint32_t* tail, uint32_t* hist,
+                                                            int2* cand) {
+  extern __shared__ __align__(16) uint8_t lds[];
+  int* rng = reinterpret_cast<int*>(lds + C::Q_LDS);  // [0] largest end, [1] smallest start
+  const int tile = blockIdx.x / S, split = blockIdx.x - tile * S, q0 = tile * C::QT;
+  if (threadIdx.x == 0) {
+    rng[0] = 0;
+    rng[1] = a.nk;
+  }
+  __syncthreads();
+  if (threadIdx.x < C::QT && q0 + (int)threadIdx.x < a.nq) {
+    const RowRange rr = row_range(a.offs, a.starts, q0 + threadIdx.x, a.nk);
+    if (rr.e > rr.s) {
+      atomicMax(&rng[0], rr.e);
+      atomicMin(&rng[1], rr.s);
+    }
+  }
+  wide_load_q<C>(lds, a, q0);  // ends with a barrier
+  // the split's keys within the union of the block's rows' ranges
+  const int kb = max(split * L, rng[1]);
+  const int ke = min(min(split * L + L, a.nk), rng[0]);
+  float wv[C::NI];
+  wide_weights<C>(wv, a, q0);
+  WideFusedSink<C> sink;
+  sink.gate = gate;
+  sink.hist = hist;
+  sink.tail = tail;
+  sink.cand = cand;
+  sink.qbase = q0;
+  sink.nq = a.nq;
+  sink.cap = cap;
+  sink.m = m;
+  sink.k = k;
+  sink.init(a, params, ke);
+  wide_scan<C>(a, WSrcContig{}, kb, ke, lds, wv, sink);
+}
+
+// Exact fallback for queued rows: one block per row at a time re-scores the
+// row's visible range into its scratch row, then radix-selects it.
+template <class C>
+__global__ __launch_bounds__(C::NTHREADS) void k_wide_fallback(ScoreArgs a, int k, uint32_t flags,
+                                                               const uint32_t* qctl, const int32_t* queue,
+                                                               float* scratch, int32_t* out_i, float* out_s) {
+  extern __shared__ __align__(16) uint8_t lds[];
+  const uint32_t n = qctl[0];
+  for (uint32_t r = blockIdx.x; r < n; r += gridDim.x) {
+    const int row = queue[r];
+    const int q0 = (row / C::QT) * C::QT, ql = row - q0;
+    const RowRange rr = row_range(a.offs, a.starts, row, a.nk);
+    float* srow = scratch + (int64_t)blockIdx.x * a.nk;
+    wide_load_q<C>(lds, a, q0);
+    float wv[C::NI];
+    wide_weights<C>(wv, a, q0);
+    WideRowSink<C> sink{srow, 16 * (ql >> 5) + 4 * ((ql & 31) >> 3) + (ql & 3), (ql >> 2) & 1};
+    wide_scan<C>(a, WSrcContig{}, rr.s, rr.e, lds, wv, sink);
+    __threadfence_block();
+    __syncthreads();
+    radix_select_row<C::NTHREADS>(srow + rr.s, rr.e - rr.s, k, out_i + (int64_t)row * k, out_s + (int64_t)row * k,
+                                  flags & LT_SORTED_OUTPUT, lds, rr.s);
+    __syncthreads();
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Variants and launchers
+// ---------------------------------------------------------------------------
+//                  d   ReLU
+#define LT_WIDE_VARIANTS(X) \
+  X(768, false)             \
+  X(768, true)
+
+template <class F>
+static bool with_wide(int dt, int mode, int h, int d, F&& f) {
+  if (dt != LT_BF16 || h != 1) return false;
+  const bool relu = mode == LT_SCORE_DSA;
+#define LT_WCASE(D, RELU)                          \
+  if (d == D && relu == RELU) {                    \
+    f.template operator()<WCfg<D, RELU>>();        \
+    return true;                                   \
+  }
+  LT_WIDE_VARIANTS(LT_WCASE)
+#undef LT_WCASE
+  return false;
+}
+
+template <class K>
+static void allow_lds(K kernel, size_t bytes) {
+  if (bytes > 65536) (void)hipFuncSetAttribute((const void*)kernel, hipFuncAttributeMaxDynamicSharedMemorySize, (int)bytes);
+}
+
+ScoreShape wide_shape(int dtype, int mode, int h, int d) {
+  ScoreShape s{0, 0, 0, 0, 0, 0};
+  with_wide(dtype, mode, h, d, [&]<class C>() {
+    s.supported = 1;
+    s.queries_per_block = C::QT;
+    s.keys_per_step = C::STEP;
+    s.threads = C::NTHREADS;
+    s.scan_lds = C::Q_LDS;
+    s.shared_rows = 1;
+  });
+  return s;
+}
+
+static constexpr int kWideSlice = 8192;      // positions per block in the dense scorer
+static constexpr int kWideSampleBlocks = 256;
+
+hipError_t launch_wide_sample(const ScoreArgs& a, const int32_t* list, int ns, float* samp, hipStream_t st) {
+  hipError_t err = hipErrorInvalidValue;
+  with_wide(a.dtype, a.mode, a.h, a.d, [&]<class C>() {
+    const int tiles = (a.nq + C::QT - 1) / C::QT;
+    const int want = tiles > 0 ? (kWideSampleBlocks + tiles - 1) / tiles : 1;
+    int slice = (ns + want - 1) / want;
+    slice = ((slice + C::STEP - 1) / C::STEP) * C::STEP;
+    slice = slice < C::STEP ? C::STEP : (slice > kWideSlice ? kWideSlice : slice);
+    const dim3 grid(tiles, (ns + slice - 1) / slice);
+    if (grid.x == 0 || grid.y == 0) {
+      err = hipSuccess;
+      return;
+    }
+    allow_lds(k_wide_sample<C>, C::Q_LDS);
+    hipLaunchKernelGGL(k_wide_sample<C>, grid, dim3(C::NTHREADS), C::Q_LDS, st, a, list, ns, samp, slice);
+    err = hipGetLastError();
+  });
+  return err;
+}
+
+hipError_t launch_wide_dense(const ScoreArgs& a, float* out, int64_t ld, hipStream_t st) {
+  hipError_t err = hipErrorInvalidValue;
+  with_wide(a.dtype, a.mode, a.h, a.d, [&]<class C>() {
+    const dim3 grid((a.nq + C::QT - 1) / C::QT, (a.nk + kWideSlice - 1) / kWideSlice);
+    if (grid.x == 0 || grid.y == 0) {
+      err = hipSuccess;
+      return;
+    }
+    allow_lds(k_wide_dense<C>, C::Q_LDS);
+    hipLaunchKernelGGL(k_wide_dense<C>, grid, dim3(C::NTHREADS), C::Q_LDS, st, a, out, ld, kWideSlice);
+    err = hipGetLastError();
+  });
+  return err;
+}
+
+hipError_t launch_wide_fused(const ScoreArgs& a, const RowParam* params, int S, int L, int cap, int m, int k,
+                             int* gate, uint32_t* tail, uint32_t* hist, int2* cand, hipStream_t st) {
+  hipError_t err = hipErrorInvalidValue;
+  with_wide(a.dtype, a.mode, a.h, a.d, [&]<class C>() {
+    const int tiles = (a.nq + C::QT - 1) / C::QT;
+    if (tiles == 0) {
+      err = hipSuccess;
+      return;
+    }
+    const int64_t n = (int64_t)a.nq * m;
+    const int ib = (int)std::min<int64_t>((n + 255) / 256, 1024);
+    hipLaunchKernelGGL(k_wide_init, dim3(ib < 1 ? 1 : ib), dim3(256), 0, st, params, a.nq, m, gate, tail, hist);
+    if ((err = hipGetLastError()) != hipSuccess) return;
+    const size_t lds = C::Q_LDS + 16;
+    allow_lds(k_wide_fused<C>, lds);
+    hipLaunchKernelGGL(k_wide_fused<C>, dim3(tiles * S), dim3(C::NTHREADS), lds, st, a, params, S, L, cap, m, k,
+                       gate, tail, hist, cand);
+    err = hipGetLastError();
+  });
+  return err;
+}
+
+hipError_t launch_wide_fallback(const ScoreArgs& a, int k, uint32_t flags, const uint32_t* qctl,
+                                const int32_t* queue, float* scratch, int grid, int32_t* out_i, float* out_s,
+                                hipStream_t st) {
+  hipError_t err = hipErrorInvalidValue;
+  with_wide(a.dtype, a.mode, a.h, a.d, [&]<class C>() {
+    size_t lds = C::Q_LDS;
+    const size_t rl = radix_lds_bytes(k);
+    if (rl > lds) lds = rl;
+    allow_lds(k_wide_fallback<C>, lds);
+    hipLaunchKernelGGL(k_wide_fallback<C>, dim3(grid), dim3(C::NTHREADS), lds, st, a, k, flags, qctl, queue,
+                       scratch, out_i, out_s);
+    err = hipGetLastError();
+  });
+  return err;
+}
+
+}  // namespace lt

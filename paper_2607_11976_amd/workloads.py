@@ -52,7 +52,16 @@ CONFIGS = {
     "dsa_fp8_1m": Workload("dsa_fp8_1m", 2048, 1048576, 64, 128, "fp8", 2048, "dsa", True, "dsa_mean"),
     "retrieval_bf16_4m": Workload("retrieval_bf16_4m", 10000, 4000000, 1, 128, "bf16", 100, "ip", False, "unit"),
     "adversarial_bf16_256k": Workload("adversarial_bf16_256k", 1024, 262144, 64, 128, "bf16", 2048, "dsa", True, "adversarial"),
+    # sec. 4.1 "Large-Scale Retrieval Benchmark": 768-dimensional passage
+    # embeddings, a batch of 64 queries that are themselves corpus passages,
+    # corpora of 1M-5M (the sweep takes prefixes), k from 128 to 8192
+    "retrieval_e7_bf16_5m": Workload("retrieval_e7_bf16_5m", 64, 5000000, 1, 768, "bf16", 1024, "ip", False,
+                                     "unit_self"),
 }
+
+# Queries of the "unit_self" law are drawn from the first QUERY_POOL corpus
+# rows, so that every corpus prefix of at least that size contains them.
+QUERY_POOL = 1000000
 
 CONFIG_SEEDS = {name: i for i, name in enumerate(CONFIGS)}
 
@@ -131,6 +140,15 @@ def generate(cfg: Workload, seed: int) -> dict:
         q /= np.linalg.norm(q, axis=-1, keepdims=True)
         keys = _normal(rng, (nk, d))
         keys /= np.linalg.norm(keys, axis=-1, keepdims=True)
+    elif cfg.dist == "unit_self":
+        # unit-normalised Gaussian passages; the queries are copies of
+        # distinct passages (the paper samples its queries from the corpus)
+        keys = _normal(rng, (nk, d))
+        for s0 in range(0, nk, 1 << 16):
+            blk = keys[s0:s0 + (1 << 16)]
+            blk /= np.linalg.norm(blk, axis=-1, keepdims=True)
+        pick = rng.choice(min(nk, QUERY_POOL), size=nq, replace=nq > min(nk, QUERY_POOL))
+        q = np.ascontiguousarray(keys[pick][:, None, :].repeat(h, axis=1))
     elif cfg.dist == "adversarial":
         # 99.9% N(0, 1) keys, 0.1% outliers scaled by 20, and 1% of keys
         # replaced by exact copies of other random keys (duplicate-score ties).
@@ -154,6 +172,33 @@ def generate(cfg: Workload, seed: int) -> dict:
     offsets = torch.from_numpy(causal_offsets(nq, nk)) if cfg.causal else None
     return dict(q=qs, q_scale=q_scale, w=w, keys=ks, k_scale=k_scale, offsets=offsets,
                 q_f32=torch.from_numpy(q), keys_f32=torch.from_numpy(keys))
+
+
+def unit_corpus_gpu(cfg: Workload, seed: int, device, nk: Optional[int] = None) -> dict:
+    """The "unit_self" law at corpus sizes numpy would take minutes to draw:
+    keys drawn on ``device`` by torch's seeded generator (Philox), in chunks of
+    2**20 rows, normalised in float32 and rounded to bfloat16; the nq queries
+    are copies of distinct rows among the first QUERY_POOL (picked by a seeded
+    CPU generator). It draws the same law as generate() but from a different
+    random stream, so its corpus is not generate()'s. Returns the generate()
+    keys q, w (None), keys, offsets (None) on ``device``, plus "pick" (the
+    query rows)."""
+    import torch as _t
+    nk = cfg.nk if nk is None else nk
+    g = _t.Generator(device=device)
+    g.manual_seed(seed)
+    keys = _t.empty((nk, cfg.d), dtype=_t.bfloat16, device=device)
+    for s0 in range(0, nk, 1 << 20):
+        n = min(1 << 20, nk - s0)
+        x = _t.randn((n, cfg.d), generator=g, device=device, dtype=_t.float32)
+        x /= x.norm(dim=1, keepdim=True)
+        keys[s0:s0 + n] = x.to(_t.bfloat16)
+        del x
+    rng = np.random.Generator(np.random.PCG64(seed))
+    pool = min(nk, QUERY_POOL)
+    pick = rng.choice(pool, size=cfg.nq, replace=cfg.nq > pool)
+    q = keys[_t.from_numpy(pick).to(device)].unsqueeze(1).repeat(1, cfg.h, 1).contiguous()
+    return dict(q=q, q_scale=None, w=None, keys=keys, k_scale=None, offsets=None, pick=pick)
 
 
 def exact_inputs(nq: int, nk: int, h: int, d: int, dtype: str, seed: int, causal: bool = True):

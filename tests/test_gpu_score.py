@@ -21,6 +21,8 @@ VARIANTS = [
     ("bf16", "dsa", 1, 128),
     ("bf16", "ip", 1, 128),
     ("fp8", "dsa", 64, 128),
+    ("bf16", "ip", 1, 768),
+    ("bf16", "dsa", 1, 768),
 ]
 
 
