@@ -21,13 +21,14 @@ constexpr size_t kHistLdsBudget = 96 * 1024;
 constexpr size_t kLdsPerBlock = 160 * 1024;   // gfx950 LDS per workgroup
 constexpr int kSampleBlockScores = 64;      // scores-in sample: runs of 64 consecutive keys
 constexpr int kMinSharedSplitKeys = 1024;   // shortest key split of the shared-row (wide) scan
+constexpr int kSharedSample = 65536;        // default sample of the shared-row scan (inner product)
 
 inline size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 
 struct Resolved {
   int m, ns, cap, S, L, E;
-  int LS;                  // candidate lists (and histograms) per row: S, or 1 when shared
-  bool shared;             // the wide scan: one list, histogram and threshold per row
+  int HS;                  // histograms per row: S, or 1 when shared by the splits
+  bool shared;             // the wide scan: one histogram and threshold per row
   uint32_t flags;
   uint64_t seed;
   void** ev;
@@ -54,9 +55,9 @@ Layout carve(int nq, int nk, const Resolved& r, bool fused) {
   L.params = take((size_t)nq * sizeof(RowParam));
   L.list = take((size_t)r.ns * 4);
   L.samp = fused ? take((size_t)nq * r.ns * 4) : 0;
-  L.cnt = take((size_t)nq * r.LS * 4);
-  L.hist = take((size_t)nq * r.LS * r.m * 4);
-  L.cand = take((size_t)nq * r.LS * r.cap * 8);
+  L.cnt = take((size_t)nq * r.S * 4);
+  L.hist = take((size_t)nq * r.HS * r.m * 4);
+  L.cand = take((size_t)nq * r.S * r.cap * 8);
   L.gate = r.shared ? take((size_t)nq * 4) : 0;
   L.scratch = fused ? take((size_t)kFallbackGridFused * nk * 4) : 0;
   L.total = off;
@@ -93,7 +94,12 @@ int resolve_sample(const lt_options* o, const Resolved& r, int nk, int k, int mo
   int ns = o->sample_size;
   if (ns < 0) {
     ns = 3 * k;  // sec. 3.2: k' = 3k
-    if (fused && mode == LT_SCORE_IP) ns = std::max(ns, std::min(nk / 64, 65536));
+    if (fused && mode == LT_SCORE_IP) {
+      // a random sample's k-th score sits at rank k * nk / ns of the corpus;
+      // with splits sharing their thresholds, the first tiles of every split
+      // run at that rank, so the wide scan samples kSharedSample keys
+      ns = std::max(ns, r.shared ? kSharedSample : std::min(nk / 64, 65536));
+    }
   }
   return sample_count(ns, nk);
 }
@@ -105,16 +111,16 @@ Resolved resolve_fused(const lt_options* o, int nq, int nk, int k, int mode, con
   lt_options_default(&d);
   if (!o) o = &d;
   r.shared = sh.shared_rows != 0;
-  if (!r.shared) {
-    // per-row LDS histograms share the block's LDS with the key-tile ring
-    const size_t room = kLdsPerBlock - sh.scan_lds - 64;
-    const size_t mcap = std::min(kHistLdsBudget, room) / (4 * (size_t)sh.queries_per_block);
-    if ((size_t)r.m > mcap) r.m = (int)std::max<size_t>(mcap, 1);
-  } else if (o->capacity <= 0) {
-    // one list per row collects every split's candidates: an online top-k
-    // over N keys admits about k (1 + ln(N / k)) of them, plus the ones the
-    // sample's threshold lets through before the first refresh
-    r.cap = std::max(16 * k, 65536);
+  // per-row LDS histograms share the block's LDS with the scan's own data
+  const size_t room = kLdsPerBlock - sh.scan_lds - 64;
+  const size_t mcap = std::min(kHistLdsBudget, room) / (4 * (size_t)sh.queries_per_block);
+  if ((size_t)r.m > mcap) r.m = (int)std::max<size_t>(mcap, 1);
+  if (r.shared && o->capacity <= 0) {
+    // a split's list holds its share of the row's candidates (an online top-k
+    // over N keys admits about k (1 + ln(N / k)), spread over the splits)
+    // plus what the sample's threshold lets through before the first
+    // refreshes; k more keeps a row whose whole top-k lies in one split
+    r.cap = k + std::max(1024, k / 2);
   }
   r.ns = resolve_sample(o, r, nk, k, mode, true);
   const int steps = (nk + sh.keys_per_step - 1) / sh.keys_per_step;
@@ -141,7 +147,7 @@ Resolved resolve_fused(const lt_options* o, int nq, int nk, int k, int mode, con
     }
   }
   r.S = S;
-  r.LS = r.shared ? 1 : S;
+  r.HS = r.shared ? 1 : S;
   const int per = (nk + S - 1) / S;
   r.L = ((per + sh.keys_per_step - 1) / sh.keys_per_step) * sh.keys_per_step;
   if (r.L == 0) r.L = sh.keys_per_step;
@@ -158,7 +164,7 @@ Resolved resolve_scores(const lt_options* o, int nq, int nk, int k) {
   int S = 1;
   if (o->key_splits > 0) S = o->key_splits;
   r.S = std::max(1, std::min(S, (nk + 255) / 256 + 1));
-  r.LS = r.S;
+  r.HS = r.S;
   const int per = (nk + r.S - 1) / r.S;
   r.L = std::max(256, ((per + 255) / 256) * 256);
   (void)nq;
@@ -274,8 +280,9 @@ int lt_indexer_topk(const void* q, const float* q_scale, const float* w, const v
                : launch_fused_scan(a, params, r.S, r.L, r.cap, r.m, k, cnt, hist, cand, st);
   if (e != hipSuccess) return hip_status(e);
   record(r, LT_STAGE_SELECT, st);
-  if ((e = launch_select(params, cnt, hist, cand, nq, r.LS, r.cap, r.m, k, r.E, r.flags | (r.shared ? kSelKeyed : 0u),
-                         out_idx, out_scores, qctl, queue, r.stats, st)) != hipSuccess)
+  if ((e = launch_select(params, cnt, hist, cand, nq, r.S, r.HS, r.cap, r.m, k, r.E,
+                         r.flags | (r.shared ? kSelKeyed : 0u), out_idx, out_scores, qctl, queue, r.stats, st)) !=
+      hipSuccess)
     return hip_status(e);
   record(r, LT_STAGE_FALLBACK, st);
   if ((e = launch_fused_fallback(a, k, r.flags, qctl, queue, scratch, kFallbackGridFused, out_idx, out_scores,
@@ -346,7 +353,7 @@ int lt_topk_select(const float* scores, int64_t stride, int32_t nq, int32_t nk, 
                          st)) != hipSuccess)
     return hip_status(e);
   record(r, LT_STAGE_SELECT, st);
-  if ((e = launch_select(params, cnt, hist, cand, nq, r.S, r.cap, r.m, k, r.E, r.flags, out_idx, out_scores, qctl,
+  if ((e = launch_select(params, cnt, hist, cand, nq, r.S, r.HS, r.cap, r.m, k, r.E, r.flags, out_idx, out_scores, qctl,
                          queue, r.stats, st)) != hipSuccess)
     return hip_status(e);
   record(r, LT_STAGE_FALLBACK, st);

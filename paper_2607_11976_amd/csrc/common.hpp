@@ -154,15 +154,27 @@ __device__ __forceinline__ uint32_t wave_or(uint32_t v) {
   return (uint32_t)__builtin_amdgcn_readlane((int)v, 63);
 }
 
+// Inclusive prefix sum over the lanes of the wave: scans within rows of 16
+// lanes (row_shr), then across rows (row_bcast), on the DPP path.
+__device__ __forceinline__ uint32_t wave_prefix_sum(uint32_t v) {
+  v += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x111, 0xF, 0xF, false);  // row_shr:1
+  v += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x112, 0xF, 0xF, false);  // row_shr:2
+  v += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x114, 0xF, 0xF, false);  // row_shr:4
+  v += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x118, 0xF, 0xF, false);  // row_shr:8
+  v += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x142, 0xA, 0xF, false);  // row_bcast:15
+  v += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x143, 0xC, 0xF, false);  // row_bcast:31
+  return v;
+}
+
 // Threshold refresh (sec. 3.2 "Threshold Refresh"): walk the histogram from
 // the top bin down until the running count reaches k. Returns the largest bin
 // b with sum_{b' >= b} hist[b'] >= k, or -1 if there is none, and the count of
 // the bins strictly above it in *above. Called by a whole wave; lane l holds
 // bins [4l, 4l + 4) in h[] (zero past the last bin).
 __device__ __forceinline__ int wave_threshold_vals(const uint32_t (&h)[4], uint32_t k, uint32_t* above) {
-  const int l = lane_id();
-  uint32_t tot = h[0] + h[1] + h[2] + h[3];
-  uint32_t excl = wave_suffix_sum_excl(tot);
+  const uint32_t tot = h[0] + h[1] + h[2] + h[3];
+  const uint32_t incl = wave_prefix_sum(tot);
+  const uint32_t excl = (uint32_t)__builtin_amdgcn_readlane((int)incl, kWave - 1) - incl;  // lanes above this one
   uint32_t suf[4];
   suf[3] = excl + h[3];
   suf[2] = suf[3] + h[2];
@@ -171,15 +183,13 @@ __device__ __forceinline__ int wave_threshold_vals(const uint32_t (&h)[4], uint3
   int nge = 0;
 #pragma unroll
   for (int j = 0; j < 4; ++j) nge += __popcll(__ballot(suf[j] >= k));
-  int tau = nge - 1;
-  // count strictly above tau: suffix(tau + 1), or the total when tau = -1
-  uint32_t a = 0;
-  int want = tau + 1;  // bin whose suffix we need (past the last bin => 0)
-#pragma unroll
-  for (int j = 0; j < 4; ++j)
-    if (4 * l + j == want) a = suf[j];
-  a = wave_sum(a);  // exactly one lane (or none when want is past the end) contributes
-  if (above) *above = a;
+  const int tau = nge - 1;
+  if (above) {
+    // count strictly above tau: the suffix of bin tau + 1 (0 past the end)
+    const int want = tau + 1, j = want & 3;
+    const uint32_t v = j == 0 ? suf[0] : j == 1 ? suf[1] : j == 2 ? suf[2] : suf[3];
+    *above = want < 4 * kWave ? (uint32_t)__builtin_amdgcn_readlane((int)v, want >> 2) : 0u;
+  }
   return tau;
 }
 

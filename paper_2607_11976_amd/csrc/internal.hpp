@@ -21,8 +21,10 @@ hipError_t launch_filter(const float* scores, int64_t stride, int nq, int nk, co
                          const int32_t* starts, const RowParam* params, int S, int L, int cap, int m, int k,
                          uint32_t* cnt, uint32_t* hist, int2* cand, hipStream_t st);
 size_t select_lds_bytes(int E);
+// S candidate lists per row (cnt [nq, S], cand [nq, S, cap]); HS histograms
+// per row (hist [nq, HS, m]), HS = S or 1.
 hipError_t launch_select(const RowParam* params, const uint32_t* cnt, const uint32_t* hist,
-                         const int2* cand, int nq, int S, int cap, int m, int k, int E,
+                         const int2* cand, int nq, int S, int HS, int cap, int m, int k, int E,
                          uint32_t flags, int32_t* out_i, float* out_s, uint32_t* qctl,
                          int32_t* queue, int32_t* stats, hipStream_t st);
 hipError_t launch_fallback_scores(const float* scores, int64_t stride, int nk, const int32_t* offs,
@@ -87,17 +89,19 @@ hipError_t launch_fused_fallback(const ScoreArgs& a, int k, uint32_t flags, cons
 ScoreShape wide_shape(int dtype, int mode, int h, int d);
 hipError_t launch_wide_sample(const ScoreArgs& a, const int32_t* list, int ns, float* samp, hipStream_t st);
 hipError_t launch_wide_dense(const ScoreArgs& a, float* out, int64_t ld, hipStream_t st);
-// Fused scan with shared row state: gate [nq] (published threshold bins),
-// tail [nq] (= per-row candidate counts), hist [nq, m], cand [nq, cap]; gate,
-// tail and hist are initialised here.
+// Fused scan with shared row state: gate [nq] (published threshold bins) and
+// hist [nq, m] shared by the S key splits of a row (initialised here); cnt
+// [nq, S] and cand [nq, S, cap] hold each split's own list, as in
+// launch_fused_scan.
 hipError_t launch_wide_fused(const ScoreArgs& a, const RowParam* params, int S, int L, int cap, int m, int k,
-                             int* gate, uint32_t* tail, uint32_t* hist, int2* cand, hipStream_t st);
+                             int* gate, uint32_t* cnt, uint32_t* hist, int2* cand, hipStream_t st);
 hipError_t launch_wide_fallback(const ScoreArgs& a, int k, uint32_t flags, const uint32_t* qctl,
                                 const int32_t* queue, float* scratch, int grid, int32_t* out_i, float* out_s,
                                 hipStream_t st);
 
 // k_select flag (internal): candidate lists are not in key order (the wide
-// scan's shared lists), so equal scores are ordered by the key itself.
+// scan's lists fill in arrival order), so equal scores are ordered by the key
+// itself and every row is output sorted.
 constexpr uint32_t kSelKeyed = 1u << 30;
 
 }  // namespace lt

@@ -206,41 +206,61 @@ __global__ __launch_bounds__(kFilterWaves * kWave) void k_filter(
 
 // ---------------------------------------------------------------------------
 // Final select (sec. 3.2 "Top-k Selection"). One block per row.
-//  1. Sum the row's per-split histograms; the final threshold bin tau is the
-//     largest bin whose suffix count reaches k (bins >= tau are complete:
-//     every key in them passed the gate, which never exceeded tau).
+//  1. Sum the row's HS histograms; the final threshold bin tau is the largest
+//     bin whose suffix count reaches k (bins >= tau are complete: every key in
+//     them passed the gate, which never exceeded tau).
 //  2. Candidates in bins above tau (fewer than k) go straight to the output,
-//     in key order.
+//     in list order.
 //  3. Candidates in bin tau are collected in LDS and only they are sorted;
 //     the best k - (count above) complete the row.
+// The row's S lists are walked as one sequence, NTH lists at a time (their
+// counts prefix-summed in LDS) and PER entries per thread per step, so many
+// short lists cost no more than one long one. Keyed rows (few rows with
+// hundreds of thousands of candidates each) run 1024 threads with 8 entries
+// per thread; the others 256 threads with 4.
 // Rows whose buffer overflowed, whose threshold bin does not fit in LDS, or
 // that are forced, are queued for the exact fallback instead.
 // ---------------------------------------------------------------------------
 constexpr int kSelThreads = 256;
+constexpr int kSelPer = 4;         // list entries per thread per step
+constexpr int kSelThreadsWide = 1024;  // keyed rows: few rows, many candidates each
+constexpr int kSelPerWide = 8;
 
-__global__ __launch_bounds__(kSelThreads) void k_select(
+// LDS byte offset of the sort entries of k_select with NTH threads.
+constexpr size_t select_ent_offset(int nth) { return ((size_t)kMaxBins + 32 + nth + 16) * 4; }
+
+template <int NTH, int PER>
+__global__ __launch_bounds__(NTH) void k_select(
     const RowParam* params, const uint32_t* cnt, const uint32_t* hist, const int2* cand, int nq,
-    int S, int cap, int m, int k, int E, uint32_t flags, int32_t* out_i, float* out_s,
+    int S, int HS, int cap, int m, int k, int E, uint32_t flags, int32_t* out_i, float* out_s,
     uint32_t* qctl, int32_t* queue, int32_t* stats) {
   extern __shared__ __align__(16) uint8_t lds[];
   uint32_t* hsum = reinterpret_cast<uint32_t*>(lds);          // [256]
-  uint32_t* tmp = hsum + kMaxBins;                             // [16]
-  uint64_t* ent = reinterpret_cast<uint64_t*>(lds + kMaxBins * 4 + 64);  // [E]
+  uint32_t* tmp = hsum + kMaxBins;                             // [32]
+  uint32_t* off = tmp + 32;                                    // [NTH + 1]: list offsets of a group
+  uint64_t* ent = reinterpret_cast<uint64_t*>(lds + select_ent_offset(NTH));  // [E]
   const int row = blockIdx.x, tid = threadIdx.x;
-  const bool sorted = flags & LT_SORTED_OUTPUT;
   // keyed: the lists are not in key order, so the tie-break position is the
-  // key itself and the output is rebuilt from the sort entries
+  // key itself, the output is rebuilt from the sort entries, and every row
+  // is sorted (the order of arrival would make it vary between calls)
   const bool keyed = flags & kSelKeyed;
+  const bool sorted = (flags & LT_SORTED_OUTPUT) || keyed;
   int32_t* oi = out_i + (int64_t)row * k;
   float* os = out_s + (int64_t)row * k;
 
   // ---- overflow / forced ----
   uint32_t total_c = 0;
   int reason = (flags & LT_FORCE_FALLBACK) ? 3 : 0;
-  for (int s = 0; s < S; ++s) {
-    uint32_t c = cnt[(int64_t)row * S + s];
-    total_c += c;
-    if (c > (uint32_t)cap && reason == 0) reason = 1;
+  {
+    uint32_t my = 0;
+    bool ovf = false;
+    for (int s = tid; s < S; s += NTH) {
+      const uint32_t c = cnt[(int64_t)row * S + s];
+      my += c;
+      ovf |= c > (uint32_t)cap;
+    }
+    (void)block_scan_excl<NTH>(my, tmp, &total_c);
+    if (__syncthreads_or(ovf) && reason == 0) reason = 1;
   }
   auto enqueue = [&](int why, int tau, uint32_t nt) {
     if (tid == 0) {
@@ -261,10 +281,10 @@ __global__ __launch_bounds__(kSelThreads) void k_select(
   }
 
   // ---- 1. final threshold bin ----
-  for (int b = tid; b < kMaxBins; b += kSelThreads) {
+  for (int b = tid; b < kMaxBins; b += NTH) {
     uint32_t h = 0;
     if (b < m)
-      for (int s = 0; s < S; ++s) h += hist[((int64_t)row * S + s) * m + b];
+      for (int s = 0; s < HS; ++s) h += hist[((int64_t)row * HS + s) * m + b];
     hsum[b] = h;
   }
   __syncthreads();
@@ -272,57 +292,84 @@ __global__ __launch_bounds__(kSelThreads) void k_select(
     uint32_t above = 0;
     int tau = wave_threshold(hsum, m, (uint32_t)k, &above);
     if (tid == 0) {
-      tmp[8] = (uint32_t)tau;
-      tmp[9] = above;
+      tmp[24] = (uint32_t)tau;
+      tmp[25] = above;
     }
   }
   __syncthreads();
-  const int tau = (int)tmp[8];
-  const uint32_t c_above = tmp[9];
+  const int tau = (int)tmp[24];
+  const uint32_t c_above = tmp[25];
   __syncthreads();
   const RowParam p = params[row];
 
   // ---- 2./3. one ordered pass over the candidates ----
   uint32_t run_above = 0, run_tie = 0;
   bool tie_ovf = false;
-  for (int s = 0; s < S; ++s) {
-    const uint32_t n_s = min(cnt[(int64_t)row * S + s], (uint32_t)cap);
-    const int2* cb = cand + ((int64_t)row * S + s) * cap;
-    for (uint32_t base = 0; base < n_s; base += kSelThreads) {
-      const uint32_t i = base + tid;
-      int2 ce = make_int2(0, 0);
-      bool ab = false, ti = false;
-      if (i < n_s) {
-        ce = cb[i];
-        int b = bin_of(bin_x(__int_as_float(ce.y), p.delta, p.c), m);
-        ab = b > tau;
-        ti = b == tau;
+  for (int g0 = 0; g0 < S; g0 += NTH) {
+    // offsets of the group's lists in their concatenation
+    const int sg = g0 + tid;
+    const uint32_t cg = sg < S ? min(cnt[(int64_t)row * S + sg], (uint32_t)cap) : 0u;
+    uint32_t gtot;
+    const uint32_t ex = block_scan_excl<NTH>(cg, tmp, &gtot);
+    off[tid] = ex;
+    if (tid == 0) off[NTH] = gtot;
+    __syncthreads();
+    const int ng = min(NTH, S - g0);
+    for (uint32_t base = 0; base < gtot; base += NTH * PER) {
+      int2 ce[PER];
+      uint32_t gpos[PER];
+      bool ab[PER], ti[PER];
+      uint32_t na = 0, nt = 0;
+#pragma unroll
+      for (int j = 0; j < PER; ++j) {
+        const uint32_t i = base + (uint32_t)(tid * PER + j);
+        ab[j] = ti[j] = false;
+        ce[j] = make_int2(0, 0);
+        gpos[j] = 0;
+        if (i < gtot) {
+          // the list holding position i: the last one whose offset is <= i
+          int lo = 0, hi = ng - 1;
+          while (lo < hi) {
+            const int mid = (lo + hi + 1) >> 1;
+            if (off[mid] <= i) lo = mid;
+            else hi = mid - 1;
+          }
+          const uint32_t pos = i - off[lo];
+          const int s = g0 + lo;
+          ce[j] = cand[((int64_t)row * S + s) * cap + pos];
+          // increases with the key index (keyed: it is the key index)
+          gpos[j] = keyed ? (uint32_t)ce[j].x : (uint32_t)s * (uint32_t)cap + pos;
+          const int b = bin_of(bin_x(__int_as_float(ce[j].y), p.delta, p.c), m);
+          ab[j] = b > tau;
+          ti[j] = b == tau;
+        }
+        na += ab[j];
+        nt += ti[j];
       }
       uint32_t tot;
-      uint32_t ex = block_scan_excl<kSelThreads>(((uint32_t)ab << 16) | (uint32_t)ti, tmp, &tot);
-      // increases with the key index (keyed: it is the key index)
-      const uint32_t gpos = keyed ? (uint32_t)ce.x : (uint32_t)s * (uint32_t)cap + i;
-      if (sorted) {
-        if (ab || ti) {
-          uint32_t q = run_above + run_tie + (ex >> 16) + (ex & 0xFFFFu);
-          if (q < (uint32_t)E) ent[q] = comp_key(__int_as_float(ce.y), gpos);
-        }
-      } else {
-        if (ab) {
-          uint32_t q = run_above + (ex >> 16);
-          if (q < (uint32_t)k) {
-            oi[q] = ce.x;
-            os[q] = __int_as_float(ce.y);
+      const uint32_t ex2 = block_scan_excl<NTH>((na << 16) | nt, tmp, &tot);
+      uint32_t ra = run_above + (ex2 >> 16), rt = run_tie + (ex2 & 0xFFFFu);
+#pragma unroll
+      for (int j = 0; j < PER; ++j) {
+        if (sorted) {
+          if (ab[j] || ti[j]) {
+            const uint32_t q = ra + rt;
+            if (q < (uint32_t)E) ent[q] = comp_key(__int_as_float(ce[j].y), gpos[j]);
           }
+        } else {
+          if (ab[j] && ra < (uint32_t)k) {
+            oi[ra] = ce[j].x;
+            os[ra] = __int_as_float(ce[j].y);
+          }
+          if (ti[j] && rt < (uint32_t)E) ent[rt] = comp_key(__int_as_float(ce[j].y), gpos[j]);
         }
-        if (ti) {
-          uint32_t q = run_tie + (ex & 0xFFFFu);
-          if (q < (uint32_t)E) ent[q] = comp_key(__int_as_float(ce.y), gpos);
-        }
+        ra += ab[j];
+        rt += ti[j];
       }
       run_above += tot >> 16;
       run_tie += tot & 0xFFFFu;
     }
+    __syncthreads();  // off[] is rewritten by the next group
   }
   const uint32_t nent = sorted ? run_above + run_tie : run_tie;
   tie_ovf = nent > (uint32_t)E;
@@ -332,13 +379,13 @@ __global__ __launch_bounds__(kSelThreads) void k_select(
   }
   const uint32_t need = (uint32_t)k - c_above;
   const int P = next_pow2((int)nent < 1 ? 1 : (int)nent);
-  for (int i = tid; i < P; i += kSelThreads)
+  for (int i = tid; i < P; i += NTH)
     if ((uint32_t)i >= nent) ent[i] = 0ull;
   __syncthreads();
-  bitonic_sort_desc<kSelThreads>(ent, P);
+  bitonic_sort_desc<NTH>(ent, P);
   const uint32_t first = sorted ? 0u : c_above;
   const uint32_t take = sorted ? min(nent, (uint32_t)k) : min(need, nent);
-  for (uint32_t i = tid; i < take; i += kSelThreads) {
+  for (uint32_t i = tid; i < take; i += NTH) {
     uint32_t gp = comp_pos(ent[i]);
     if (keyed) {
       oi[first + i] = (int32_t)gp;
@@ -350,7 +397,7 @@ __global__ __launch_bounds__(kSelThreads) void k_select(
     oi[first + i] = ce.x;
     os[first + i] = __int_as_float(ce.y);
   }
-  for (uint32_t i = first + take + tid; i < (uint32_t)k; i += kSelThreads) {
+  for (uint32_t i = first + take + tid; i < (uint32_t)k; i += NTH) {
     oi[i] = -1;
     os[i] = -__builtin_inff();
   }
@@ -426,16 +473,20 @@ hipError_t launch_filter(const float* scores, int64_t stride, int nq, int nk, co
   return hipGetLastError();
 }
 
-size_t select_lds_bytes(int E) { return kMaxBins * 4 + 64 + (size_t)E * 8; }
+size_t select_lds_bytes(int E) { return select_ent_offset(kSelThreadsWide) + (size_t)E * 8; }
 
 hipError_t launch_select(const RowParam* params, const uint32_t* cnt, const uint32_t* hist,
-                         const int2* cand, int nq, int S, int cap, int m, int k, int E,
+                         const int2* cand, int nq, int S, int HS, int cap, int m, int k, int E,
                          uint32_t flags, int32_t* out_i, float* out_s, uint32_t* qctl,
                          int32_t* queue, int32_t* stats, hipStream_t st) {
-  size_t lds = select_lds_bytes(E);
-  if (lds > 65536) (void)hipFuncSetAttribute((const void*)k_select, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
-  hipLaunchKernelGGL(k_select, dim3(nq), dim3(kSelThreads), lds, st, params, cnt, hist, cand, nq, S,
-                     cap, m, k, E, flags, out_i, out_s, qctl, queue, stats);
+  auto go = [&](auto kernel, int nth) {
+    const size_t lds = select_ent_offset(nth) + (size_t)E * 8;
+    if (lds > 65536) (void)hipFuncSetAttribute((const void*)kernel, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+    hipLaunchKernelGGL(kernel, dim3(nq), dim3(nth), lds, st, params, cnt, hist, cand, nq, S, HS, cap, m, k, E, flags,
+                       out_i, out_s, qctl, queue, stats);
+  };
+  if (flags & kSelKeyed) go(k_select<kSelThreadsWide, kSelPerWide>, kSelThreadsWide);
+  else go(k_select<kSelThreads, kSelPer>, kSelThreads);
   return hipGetLastError();
 }
 

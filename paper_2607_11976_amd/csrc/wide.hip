@@ -20,14 +20,21 @@
 // needs about 256 key splits to fill the GPU, and a threshold refreshed from
 // one split's own histogram can only reach that split's local top-k, which
 // for large k admits most of the split. Here all splits of a row share one
-// histogram, one threshold bin and one candidate list in global memory (the
-// paper's per-CTA structure widened to the grid):
-//  * a tile's passing candidates reserve their slots with one atomic add per
-//    query and count themselves in the row's histogram with atomic adds
-//    whose results nobody waits for;
-//  * waves recompute the threshold bin of rows they added candidates to by
-//    walking the shared histogram from the top, and publish it with an atomic
-//    max; every wave re-reads the published bins once per tile.
+// histogram and one threshold bin in global memory (the paper's per-CTA
+// structure widened to the grid), while each block keeps its own candidate
+// list per row:
+//  * a tile's passing candidates reserve their slots in the block's list with
+//    one LDS atomic add per query and count themselves in the block's LDS
+//    histogram of the row;
+//  * wave w of a block looks after rows w, w + 8, ..., one per tile in turn:
+//    it moves the block's LDS counts of the row into the row's shared
+//    histogram (one atomic add per non-empty bin), reads the shared
+//    histogram and the row's published bin, and one tile later walks the
+//    histogram from the top for the threshold bin, raises the block's bin in
+//    LDS and, when it beats the published one, publishes it with an atomic
+//    max; every wave takes the block's bins from LDS once per tile.
+// (Device-wide atomics and coherent reads per query and tile, or per
+// candidate, contended by 2048 waves for 64 rows, cost more than the scan.)
 // A published bin b had, when it was computed, at least k counted candidates
 // in bins >= b. Counts only grow, so b never exceeds the final threshold bin
 // the select stage computes, and every key a gate drops lies below it. A
@@ -40,6 +47,14 @@
 namespace lt {
 
 typedef __bf16 wbf16x8_t __attribute__((ext_vector_type(8)));
+typedef __attribute__((address_space(3))) uint32_t lds_u32_t;
+typedef __attribute__((address_space(3))) int lds_i32_t;
+typedef uint32_t wu32x4_t __attribute__((ext_vector_type(4)));
+
+// Raw buffer descriptor word 3 for gfx950 (32-bit data, no swizzle), and the
+// cache policy of a device-coherent load (sc1, as for agent-scope atomics).
+constexpr int kBufferFlags = 0x00020000;
+constexpr int kCoherent = 0x10;
 typedef float wf32x16_t __attribute__((ext_vector_type(16)));
 typedef int wi32x4_t __attribute__((ext_vector_type(4)));
 
@@ -64,6 +79,7 @@ struct WCfg {
   static constexpr int STEP = KT * WAVES;    // items per block step
   static constexpr int PD = 16;              // B fragments in flight per wave (16 KB)
   static constexpr int NI = 16 * MT;         // scores per lane per tile
+  static constexpr int REFRESH = 8;          // tiles between two refreshes of one wave
   static constexpr int Q_LDS = MT * KS * kWave * 16;
   static_assert(D % 16 == 0 && KS % PD == 0, "the fragment ring must divide the K steps");
   static_assert(NI == 32, "one bit per score item");
@@ -241,18 +257,22 @@ __device__ __forceinline__ uint32_t wload(const uint32_t* p) {
 template <class C>
 struct WideFusedSink {
   float delta_v, c_v, t_v;
-  int tau_v, e_v, s_v, gate_next;
-  uint32_t pend_v;      // candidates of query q counted since its last refresh
+  int tau_v, e_v, s_v;
   float tq[C::NI];
   bool ungated;         // some row of the block has no gate (tau = -1)
-  int rq0, rq1;         // rows whose histograms were read for a refresh (-1: none)
-  int rot;              // where this wave's search for rows to refresh starts
-  uint32_t rh0[4], rh1[4];
+  int rq;               // row whose histogram and published bin were read last tile (-1: none)
+  int rturn;            // the next of this wave's rows to refresh
+  int rg;               // its published bin as read
+  int gv;               // the published bin of query qbase + lane, read with it
+  int rcount;           // tiles consumed
+  uint32_t rh[4];       // its shared histogram, bins 4 * lane .. + 3
   int* gate;            // [nq] published threshold bins
   uint32_t* hist;       // [nq, m] shared histograms
-  uint32_t* tail;       // [nq] candidates reserved per row
-  int2* cand;           // [nq, cap] (key, score) lists
-  int qbase, nq, cap, m, k;
+  lds_u32_t* bh;        // [64, m] LDS: block counts not yet moved to `hist`
+  lds_i32_t* btau;      // [64] LDS: the block's threshold bins
+  lds_u32_t* btail;     // [64] LDS: slots taken in the block's list of each row
+  int2* cand;           // [nq, S, cap] (key, score) lists, this block's is `split`
+  int qbase, nq, S, split, cap, m, k;
 
   __device__ static float gate_floor(float delta, float c, int tau) {
     if (tau < 0) return -__builtin_inff();
@@ -278,12 +298,10 @@ struct WideFusedSink {
     delta_v = dl;
     c_v = c;
     tau_v = t0;
-    gate_next = t0;
-    pend_v = 0;
-    rq0 = rq1 = -1;
-    // waves of the grid start their refresh rounds at different rows, so
-    // that every row is refreshed about equally often
-    rot = (int)((blockIdx.x * C::WAVES + threadIdx.x / kWave) * 2) & (kWave - 1);
+    rq = -1;
+    rcount = (int)(threadIdx.x / kWave) % C::REFRESH;
+    // wave w refreshes rows w, w + WAVES, ...; blocks start at different ones
+    rturn = (int)(threadIdx.x / kWave) + C::WAVES * (int)(blockIdx.x % (C::QT / C::WAVES));
     update_gates();
   }
 
@@ -300,28 +318,43 @@ struct WideFusedSink {
     });
   }
 
-  // the published bins, read while the tile's MFMAs run
-  __device__ void begin() {
-    const int t = qbase + lane_id();
-    gate_next = t < nq ? wload(gate + t) : -1;
+  __device__ void begin() {}
+
+  // the threshold bin of row qbase + rq from its histogram read one tile
+  // ago: into the block's bins, and published when it beats the published one
+  __device__ void finish_refresh() {
+    const int b = wave_threshold_vals(rh, (uint32_t)k, nullptr);
+    const int l = lane_id();
+    // every row's published bin, and this row's own result, into the block's
+    const int nb = l == rq ? max(b, gv) : gv;
+    if (nb > btau[l]) __hip_atomic_fetch_max(btau + l, nb, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+    if (l == 0 && b > rg) __hip_atomic_fetch_max(gate + qbase + rq, b, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    rq = -1;
   }
 
-  // the threshold bin of row qbase + q from its histogram read one tile ago
-  __device__ bool finish_refresh(int q, const uint32_t (&hv)[4]) {
-    const int b = wave_threshold_vals(hv, (uint32_t)k, nullptr);
-    const int cur = __builtin_amdgcn_readlane(tau_v, q);
-    if (b <= cur) return false;
-    if (lane_id() == 0) __hip_atomic_fetch_max(gate + qbase + q, b, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    tau_v = lane_id() == q ? b : tau_v;
-    return true;
-  }
-
-  __device__ void start_refresh(int q, uint32_t (&hv)[4]) {
-    const uint32_t* hr = hist + (int64_t)(qbase + q) * m;
+  // move the block's counts of row qbase + q to the shared histogram (each
+  // LDS bin swapped with 0, so counts other waves add meanwhile stay for the
+  // next move), then read the shared histogram and the published bin
+  __device__ void start_refresh(int q) {
+    uint32_t* hr = hist + (int64_t)(qbase + q) * m;
     const int l = lane_id();
 #pragma unroll
-    for (int j = 0; j < 4; ++j) hv[j] = 4 * l + j < m ? wload(hr + 4 * l + j) : 0u;
-    pend_v = l == q ? 0u : pend_v;
+    for (int j = 0; j < 4; ++j) {
+      const int b = 4 * l + j;
+      if (b < m) {
+        const uint32_t v = __hip_atomic_exchange(bh + q * m + b, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+        if (v) __hip_atomic_fetch_add(hr + b, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      }
+    }
+    // one device-coherent 16-byte read per lane (bins past m read as 0: the
+    // buffer covers the row only)
+    const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(hr, 0, m * 4, kBufferFlags);
+    const wu32x4_t v = __builtin_amdgcn_raw_buffer_load_b128(rs, l * 16, 0, kCoherent);
+#pragma unroll
+    for (int j = 0; j < 4; ++j) rh[j] = 4 * l + j < m ? v[j] : 0u;
+    gv = qbase + l < nq ? wload(gate + qbase + l) : -1;
+    rg = __builtin_amdgcn_readlane(gv, q);
+    rq = q;
   }
 
   __device__ bool lane_pass(int it, int key, uint32_t bits, int qa, int qb) const {
@@ -347,11 +380,9 @@ struct WideFusedSink {
       const uint32_t lo = (uint32_t)__popcll(m2 & 0xFFFFFFFFull), hi = (uint32_t)__popcll(m2 >> 32);
       cnt_v = l == qa ? lo : (l == qb ? hi : cnt_v);
     }
-    // one slot reservation per query with passes
+    // one slot reservation per query with passes, in the block's list
     uint32_t base_v = 0;
-    if (cnt_v != 0)
-      base_v = __hip_atomic_fetch_add(tail + qbase + l, cnt_v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    pend_v |= cnt_v;
+    if (cnt_v != 0) base_v = __hip_atomic_fetch_add(btail + l, cnt_v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
     for (uint32_t rem = items; rem; rem &= rem - 1) {
       const int it = __builtin_ctz(rem), qa = wq_of(it, 0), qb = qa + 4;
       const bool pass = lane_pass(it, key, bits, qa, qb);
@@ -367,28 +398,25 @@ struct WideFusedSink {
         const float s = scv[it];
         const uint32_t pos = h ? bb + mbcnt64(m2) - lo : ba + mbcnt64(m2);
         const int64_t t = qbase + (h ? qb : qa);
-        if (pos < (uint32_t)cap) cand[t * cap + pos] = make_int2(key, __float_as_int(s));
+        if (pos < (uint32_t)cap) cand[(t * S + split) * cap + pos] = make_int2(key, __float_as_int(s));
         const float x = fmaf(s, h ? db : da, h ? cb : ca);
         if (x >= 0.0f)
-          __hip_atomic_fetch_add(hist + t * m + min(__float2int_rz(x), m - 1), 1u, __ATOMIC_RELAXED,
-                                 __HIP_MEMORY_SCOPE_AGENT);
+          __hip_atomic_fetch_add(bh + (h ? qb : qa) * m + min(__float2int_rz(x), m - 1), 1u, __ATOMIC_RELAXED,
+                                 __HIP_MEMORY_SCOPE_WORKGROUP);
       }
     }
   }
 
   __device__ void consume(int k0, int kend, const float (&sc)[C::NI]) {
     const int l = lane_id(), key = k0 + (l & 31);
-    // 1. thresholds: the refresh whose histograms were read one tile ago,
-    //    then whatever other waves published
-    bool moved = false;
-    if (rq0 >= 0) moved |= finish_refresh(rq0, rh0);
-    if (rq1 >= 0) moved |= finish_refresh(rq1, rh1);
-    rq0 = rq1 = -1;
-    if (__ballot(gate_next > tau_v) != 0) {
-      tau_v = max(tau_v, gate_next);
-      moved = true;
+    // 1. thresholds: finish this wave's refresh begun one tile ago, then take
+    //    the block's bins
+    if (rq >= 0) finish_refresh();
+    const int bt = btau[l];
+    if (__ballot(bt > tau_v) != 0) {
+      tau_v = max(tau_v, bt);
+      update_gates();
     }
-    if (moved) update_gates();
     // 2. gate. Fast path on the vector ALU: the largest margin score - T of
     //    the lane (a NaN score only matters to an ungated row, and then the
     //    fast path is skipped)
@@ -407,20 +435,12 @@ struct WideFusedSink {
       const uint32_t items = wave_or(bits);
       if (items) emit(key, bits, items, sc);
     }
-    // 3. read the histograms of up to two rows this wave added to, the
-    //    next ones at or after `rot` (cyclically)
-    const uint64_t pm = __ballot(pend_v != 0);
-    if (pm) {
-      uint64_t r = rot ? (pm >> rot) | (pm << (kWave - rot)) : pm;
-      rq0 = (__builtin_ctzll(r) + rot) & (kWave - 1);
-      start_refresh(rq0, rh0);
-      r &= r - 1;
-      if (r) {
-        rq1 = (__builtin_ctzll(r) + rot) & (kWave - 1);
-        start_refresh(rq1, rh1);
-      }
-      rot = ((rq1 >= 0 ? rq1 : rq0) + 1) & (kWave - 1);
-    }
+    // 3. every C::REFRESH tiles (the block's waves in turn), begin the
+    //    refresh of this wave's next row
+    if (++rcount % C::REFRESH != 0) return;
+    const int q = rturn;
+    rturn = (rturn + C::WAVES) & (C::QT - 1);
+    if (qbase + q < nq) start_refresh(q);
   }
 };
 
@@ -452,28 +472,33 @@ __global__ __launch_bounds__(C::NTHREADS) void k_wide_dense(ScoreArgs a, float* 
   wide_scan<C>(a, WSrcContig{}, kb, ke, lds, wv, sink);
 }
 
-// Shared row state: empty histograms and lists, published bins = the sample's.
-__global__ void k_wide_init(const RowParam* params, int nq, int m, int* gate, uint32_t* tail, uint32_t* hist) {
+// Shared row state: empty histograms, published bins = the sample's.
+__global__ void k_wide_init(const RowParam* params, int nq, int m, int* gate, uint32_t* hist) {
   const int64_t n = (int64_t)nq * m, stride = (int64_t)gridDim.x * blockDim.x;
   const int64_t i0 = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   for (int64_t i = i0; i < n; i += stride) hist[i] = 0u;
-  for (int64_t i = i0; i < nq; i += stride) {
-    tail[i] = 0u;
-    gate[i] = params[i].tau0;
-  }
+  for (int64_t i = i0; i < nq; i += stride) gate[i] = params[i].tau0;
 }
 
 template <class C>
 __global__ __launch_bounds__(C::NTHREADS) void k_wide_fused(ScoreArgs a, const RowParam* params, int S, int L, int cap,
-                                                            int m, int k, int* gate, uint32_t* tail, uint32_t* hist,
+                                                            int m, int k, int* gate, uint32_t* cnt, uint32_t* hist,
                                                             int2* cand) {
   extern __shared__ __align__(16) uint8_t lds[];
   int* rng = reinterpret_cast<int*>(lds + C::Q_LDS);  // [0] largest end, [1] smallest start
+  uint32_t* btail = reinterpret_cast<uint32_t*>(lds + C::Q_LDS + 16);           // [QT]
+  int* btau = reinterpret_cast<int*>(lds + C::Q_LDS + 16 + C::QT * 4);          // [QT]
+  uint32_t* bh = reinterpret_cast<uint32_t*>(lds + C::Q_LDS + 16 + C::QT * 8);  // [QT, m]
   const int tile = blockIdx.x / S, split = blockIdx.x - tile * S, q0 = tile * C::QT;
   if (threadIdx.x == 0) {
     rng[0] = 0;
     rng[1] = a.nk;
   }
+  if (threadIdx.x < C::QT) {
+    btail[threadIdx.x] = 0u;
+    btau[threadIdx.x] = q0 + (int)threadIdx.x < a.nq ? params[q0 + threadIdx.x].tau0 : -1;
+  }
+  for (int i = threadIdx.x; i < C::QT * m; i += C::NTHREADS) bh[i] = 0u;
   __syncthreads();
   if (threadIdx.x < C::QT && q0 + (int)threadIdx.x < a.nq) {
     const RowRange rr = row_range(a.offs, a.starts, q0 + threadIdx.x, a.nk);
@@ -491,15 +516,29 @@ __global__ __launch_bounds__(C::NTHREADS) void k_wide_fused(ScoreArgs a, const R
   WideFusedSink<C> sink;
   sink.gate = gate;
   sink.hist = hist;
-  sink.tail = tail;
+  sink.bh = (lds_u32_t*)bh;
+  sink.btau = (lds_i32_t*)btau;
+  sink.btail = (lds_u32_t*)btail;
   sink.cand = cand;
   sink.qbase = q0;
   sink.nq = a.nq;
+  sink.S = S;
+  sink.split = split;
   sink.cap = cap;
   sink.m = m;
   sink.k = k;
   sink.init(a, params, ke);
   wide_scan<C>(a, WSrcContig{}, kb, ke, lds, wv, sink);
+  __syncthreads();
+  if (threadIdx.x < C::QT && q0 + (int)threadIdx.x < a.nq)
+    cnt[(int64_t)(q0 + threadIdx.x) * S + split] = btail[threadIdx.x];
+  // the counts no refresh has moved yet
+  for (int i = threadIdx.x; i < C::QT * m; i += C::NTHREADS) {
+    const int q = i / m;
+    if (bh[i] != 0u && q0 + q < a.nq)
+      __hip_atomic_fetch_add(hist + (int64_t)(q0 + q) * m + (i - q * m), bh[i], __ATOMIC_RELAXED,
+                             __HIP_MEMORY_SCOPE_AGENT);
+  }
 }
 
 // Exact fallback for queued rows: one block per row at a time re-scores the
@@ -562,7 +601,7 @@ ScoreShape wide_shape(int dtype, int mode, int h, int d) {
     s.queries_per_block = C::QT;
     s.keys_per_step = C::STEP;
     s.threads = C::NTHREADS;
-    s.scan_lds = C::Q_LDS;
+    s.scan_lds = C::Q_LDS + 16 + C::QT * 8;  // queries, key range, list tails, bins
     s.shared_rows = 1;
   });
   return s;
@@ -607,7 +646,7 @@ hipError_t launch_wide_dense(const ScoreArgs& a, float* out, int64_t ld, hipStre
 }
 
 hipError_t launch_wide_fused(const ScoreArgs& a, const RowParam* params, int S, int L, int cap, int m, int k,
-                             int* gate, uint32_t* tail, uint32_t* hist, int2* cand, hipStream_t st) {
+                             int* gate, uint32_t* cnt, uint32_t* hist, int2* cand, hipStream_t st) {
   hipError_t err = hipErrorInvalidValue;
   with_wide(a.dtype, a.mode, a.h, a.d, [&]<class C>() {
     const int tiles = (a.nq + C::QT - 1) / C::QT;
@@ -617,12 +656,12 @@ hipError_t launch_wide_fused(const ScoreArgs& a, const RowParam* params, int S, 
     }
     const int64_t n = (int64_t)a.nq * m;
     const int ib = (int)std::min<int64_t>((n + 255) / 256, 1024);
-    hipLaunchKernelGGL(k_wide_init, dim3(ib < 1 ? 1 : ib), dim3(256), 0, st, params, a.nq, m, gate, tail, hist);
+    hipLaunchKernelGGL(k_wide_init, dim3(ib < 1 ? 1 : ib), dim3(256), 0, st, params, a.nq, m, gate, hist);
     if ((err = hipGetLastError()) != hipSuccess) return;
-    const size_t lds = C::Q_LDS + 16;
+    const size_t lds = C::Q_LDS + 16 + C::QT * 8 + (size_t)C::QT * m * 4;
     allow_lds(k_wide_fused<C>, lds);
     hipLaunchKernelGGL(k_wide_fused<C>, dim3(tiles * S), dim3(C::NTHREADS), lds, st, a, params, S, L, cap, m, k,
-                       gate, tail, hist, cand);
+                       gate, cnt, hist, cand);
     err = hipGetLastError();
   });
   return err;
