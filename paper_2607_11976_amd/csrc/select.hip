@@ -26,31 +26,33 @@ __global__ void k_init(uint32_t* qctl) {
 // kRangeUnroll loads in flight: the kernel is bound by load latency.
 // ---------------------------------------------------------------------------
 constexpr int kRangeThreads = 256;
+constexpr int kRangeThreadsLarge = 1024;  // samples of kRangeLargeSample keys or more
+constexpr int kRangeLargeSample = 16384;
 constexpr int kRangeUnroll = 8;
 
-template <bool FROM_SCORES>
+template <int NTH, bool FROM_SCORES>
 __device__ __forceinline__ void range_load(const float* rp, const int32_t* list, int ns, RowRange rr, int base,
                                            float (&s)[kRangeUnroll], bool (&vis)[kRangeUnroll]) {
   int key[kRangeUnroll];
 #pragma unroll
   for (int u = 0; u < kRangeUnroll; ++u) {
-    const int i = base + u * kRangeThreads + (int)threadIdx.x;
+    const int i = base + u * NTH + (int)threadIdx.x;
     key[u] = i < ns ? list[i] : -1;
   }
 #pragma unroll
   for (int u = 0; u < kRangeUnroll; ++u) {
-    const int i = base + u * kRangeThreads + (int)threadIdx.x;
+    const int i = base + u * NTH + (int)threadIdx.x;
     vis[u] = key[u] >= rr.s && key[u] < rr.e;
     s[u] = vis[u] ? (FROM_SCORES ? rp[key[u]] : rp[i]) : 0.0f;
   }
 }
 
-template <bool FROM_SCORES>
-__global__ __launch_bounds__(kRangeThreads) void k_range(const float* src, int64_t stride, int nq, int nk,
+template <int NTH, bool FROM_SCORES>
+__global__ __launch_bounds__(NTH) void k_range(const float* src, int64_t stride, int nq, int nk,
                                                          const int32_t* offs, const int32_t* starts,
                                                          const int32_t* list, int ns, int m, int k,
                                                          RowParam* params) {
-  constexpr int NW = kRangeThreads / kWave;
+  constexpr int NW = NTH / kWave;
   __shared__ uint32_t hist[kMaxBins];
   __shared__ float red_mn[NW], red_mx[NW];
   __shared__ uint32_t red_n[NW];
@@ -58,13 +60,13 @@ __global__ __launch_bounds__(kRangeThreads) void k_range(const float* src, int64
   const RowRange rr = row_range(offs, starts, row, nk);
   const float* rp = src + (int64_t)row * stride;
 
-  for (int b = threadIdx.x; b < kMaxBins; b += kRangeThreads) hist[b] = 0u;
+  for (int b = threadIdx.x; b < kMaxBins; b += NTH) hist[b] = 0u;
   float mn = __builtin_inff(), mx = -__builtin_inff();
   uint32_t nvis = 0;
-  for (int base = 0; base < ns; base += kRangeThreads * kRangeUnroll) {
+  for (int base = 0; base < ns; base += NTH * kRangeUnroll) {
     float s[kRangeUnroll];
     bool vis[kRangeUnroll];
-    range_load<FROM_SCORES>(rp, list, ns, rr, base, s, vis);
+    range_load<NTH, FROM_SCORES>(rp, list, ns, rr, base, s, vis);
 #pragma unroll
     for (int u = 0; u < kRangeUnroll; ++u) {
       nvis += vis[u];
@@ -98,10 +100,10 @@ __global__ __launch_bounds__(kRangeThreads) void k_range(const float* src, int64
   if (__builtin_isfinite(mn)) c = -mn * delta;
   if (!__builtin_isfinite(c)) c = 0.0f;
 
-  for (int base = 0; base < ns; base += kRangeThreads * kRangeUnroll) {
+  for (int base = 0; base < ns; base += NTH * kRangeUnroll) {
     float s[kRangeUnroll];
     bool vis[kRangeUnroll];
-    range_load<FROM_SCORES>(rp, list, ns, rr, base, s, vis);
+    range_load<NTH, FROM_SCORES>(rp, list, ns, rr, base, s, vis);
 #pragma unroll
     for (int u = 0; u < kRangeUnroll; ++u) {
       const int b = bin_of(bin_x(s[u], delta, c), m);
@@ -454,12 +456,18 @@ hipError_t launch_range(bool from_scores, const float* src, int64_t stride, int 
                         const int32_t* offs, const int32_t* starts, const int32_t* list, int ns, int m, int k,
                         RowParam* params, hipStream_t st) {
   dim3 grid(nq);
-  if (from_scores)
-    hipLaunchKernelGGL(k_range<true>, grid, dim3(kRangeThreads), 0, st, src, stride, nq, nk, offs, starts, list, ns,
-                       m, k, params);
-  else
-    hipLaunchKernelGGL(k_range<false>, grid, dim3(kRangeThreads), 0, st, src, stride, nq, nk, offs, starts, list, ns,
-                       m, k, params);
+  auto go = [&](auto kernel, int nth) {
+    hipLaunchKernelGGL(kernel, grid, dim3(nth), 0, st, src, stride, nq, nk, offs, starts, list, ns, m, k, params);
+  };
+  // a long sample is read in fewer, wider steps (the kernel waits on loads)
+  const bool large = ns >= kRangeLargeSample;
+  if (from_scores) {
+    if (large) go(k_range<kRangeThreadsLarge, true>, kRangeThreadsLarge);
+    else go(k_range<kRangeThreads, true>, kRangeThreads);
+  } else {
+    if (large) go(k_range<kRangeThreadsLarge, false>, kRangeThreadsLarge);
+    else go(k_range<kRangeThreads, false>, kRangeThreads);
+  }
   return hipGetLastError();
 }
 
