@@ -275,6 +275,7 @@ struct WideFusedSink {
   bool ungated;         // some row of the block has no gate (tau = -1)
   int rq;               // row whose histogram and published bin were read last tile (-1: none)
   int rturn;            // the next of this wave's rows to refresh
+  int fturn;            // the next of this wave's rows to flush
   int rg;               // its published bin as read
   int gv;               // the published bin of query qbase + lane, read with it
   int rcount;           // tiles consumed
@@ -315,6 +316,7 @@ struct WideFusedSink {
     rcount = (int)(threadIdx.x / kWave) % C::REFRESH;
     // wave w refreshes rows w, w + WAVES, ...; blocks start at different ones
     rturn = (int)(threadIdx.x / kWave) + C::WAVES * (int)(blockIdx.x % (C::QT / C::WAVES));
+    fturn = (rturn + C::WAVES * (C::QT / C::WAVES / 2)) & (C::QT - 1);
     update_gates();
   }
 
@@ -348,17 +350,26 @@ struct WideFusedSink {
   // move the block's counts of row qbase + q to the shared histogram (each
   // LDS bin swapped with 0, so counts other waves add meanwhile stay for the
   // next move), then read the shared histogram and the published bin
-  __device__ void start_refresh(int q) {
+  // Counts in bins below the block's current bin of the row are dropped:
+  // that bin never exceeds the final threshold bin, and only bins at or
+  // above the final one are ever read (the refresh walks stop there too).
+  __device__ void flush(int q) {
     uint32_t* hr = hist + (int64_t)(qbase + q) * m;
-    const int l = lane_id();
+    const int l = lane_id(), bt = btau[q];
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
       const int b = 4 * l + j;
-      if (b < m) {
+      if (b < m && b >= bt) {
         const uint32_t v = __hip_atomic_exchange(bh + q * m + b, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
         if (v) __hip_atomic_fetch_add(hr + b, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
       }
     }
+  }
+
+  __device__ void start_refresh(int q) {
+    uint32_t* hr = hist + (int64_t)(qbase + q) * m;
+    const int l = lane_id();
+    flush(q);
     // one device-coherent 16-byte read per lane (bins past m read as 0: the
     // buffer covers the row only)
     const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(hr, 0, m * 4, kBufferFlags);
@@ -448,8 +459,12 @@ struct WideFusedSink {
       const uint32_t items = wave_or(bits);
       if (items) emit(key, bits, items, sc);
     }
-    // 3. every C::REFRESH tiles (the block's waves in turn), begin the
-    //    refresh of this wave's next row
+    // 3. move the counts of one of this wave's rows to the shared histogram
+    //    every tile; every C::REFRESH tiles (the block's waves in turn)
+    //    begin the refresh of another
+    const int qf = fturn;
+    fturn = (fturn + C::WAVES) & (C::QT - 1);
+    if (qbase + qf < nq) flush(qf);
     if (++rcount % C::REFRESH != 0) return;
     const int q = rturn;
     rturn = (rturn + C::WAVES) & (C::QT - 1);
@@ -545,10 +560,10 @@ __global__ __launch_bounds__(C::NTHREADS) void k_wide_fused(ScoreArgs a, const R
   __syncthreads();
   if (threadIdx.x < C::QT && q0 + (int)threadIdx.x < a.nq)
     cnt[(int64_t)(q0 + threadIdx.x) * S + split] = btail[threadIdx.x];
-  // the counts no refresh has moved yet
+  // the counts no flush has moved yet (bins at or above the block's bin)
   for (int i = threadIdx.x; i < C::QT * m; i += C::NTHREADS) {
     const int q = i / m;
-    if (bh[i] != 0u && q0 + q < a.nq)
+    if (bh[i] != 0u && q0 + q < a.nq && i - q * m >= btau[q])
       __hip_atomic_fetch_add(hist + (int64_t)(q0 + q) * m + (i - q * m), bh[i], __ATOMIC_RELAXED,
                              __HIP_MEMORY_SCOPE_AGENT);
   }
