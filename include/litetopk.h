@@ -31,7 +31,9 @@
  *    LT_SORTED_OUTPUT the selected entries come in an unspecified but
  *    deterministic order (the paper's select writes the above-threshold bins
  *    directly, sec. 3.2 "Top-k Selection"); with it they are sorted by the
- *    total order.
+ *    total order. The one-head 768-dimensional shapes always return sorted
+ *    rows (their candidate lists fill in arrival order), and report a zero
+ *    score as +0.0 and a NaN score as the canonical quiet NaN.
  */
 #ifndef LITETOPK_H
 #define LITETOPK_H
@@ -90,12 +92,15 @@ typedef struct lt_options {
                               "Sampling"); 1..LT_MAX_BINS; default 256          */
   int32_t sample_size;     /* k': sampled keys per launch (sec. 3.2: k' = 3k for
                               DSA); negative = default: 3k in DSA mode,
-                              max(3k, min(Nk/64, 65536)) in IP mode (the scores-in
-                              entry uses 3k); 0 disables the gate. With
-                              sample_keys set: the length of that list,
-                              1..LT_SAMPLE_LIST_MAX                            */
+                              max(3k, min(Nk/64, 65536)) in IP mode, max(3k,
+                              65536) for the 768-dimensional IP shape (all
+                              capped at Nk; the scores-in entry uses 3k); 0
+                              disables the gate. With sample_keys set: the
+                              length of that list, 1..LT_SAMPLE_LIST_MAX        */
   int32_t capacity;        /* candidate slots per (row, key split); <= 0 = default
-                              max(12k, 2048) (sec. 4.2: 12k for k = 2048)       */
+                              max(12k, 2048) (sec. 4.2: 12k for k = 2048), and
+                              k + max(1024, k/2) for the 768-dimensional shapes,
+                              whose splits share one threshold                 */
   int32_t key_splits;      /* key-range splits per row; 0 = auto (fused), 1 (scores-in) */
   uint32_t flags;          /* LT_SORTED_OUTPUT | LT_FORCE_FALLBACK               */
   uint64_t seed;           /* seed of the key sample                             */
@@ -153,7 +158,8 @@ size_t lt_indexer_topk_workspace_size(int32_t num_queries, int32_t num_keys, int
              its contents on entry do not matter.
    Supported (dtype, mode, num_heads, head_dim): f32 DSA (4, 64), f32 DSA and IP
    (1, 64); bf16 DSA (64, 128), bf16 DSA (4, 128), bf16 DSA and IP (1, 128);
-   fp8 DSA (64, 128). Anything else returns LT_EUNSUPPORTED. */
+   bf16 DSA and IP (1, 768) (the retrieval shapes of sec. 4.1); fp8 DSA
+   (64, 128). Anything else returns LT_EUNSUPPORTED. */
 int lt_indexer_topk(const void* q, const float* q_scale, const float* w, const void* keys,
                     const float* k_scale, lt_dtype dtype, lt_score_mode mode, int32_t num_queries,
                     int32_t num_keys, int32_t num_heads, int32_t head_dim, int32_t k,
