@@ -49,14 +49,16 @@ from paper_2607_11976_amd import workloads  # noqa: E402
 METRIC = "query-key pairs scored+selected/s at 128K/1M ctx; % MFMA & HBM roofline"
 PEAK_TFLOPS = {"bf16": 2500.0, "fp8": 5000.0, "f32": 157.3}
 HBM_PEAK_GBS = 8000.0
-# FETCH_SIZE / WRITE_SIZE of the fused scan kernel (KiB per dispatch, mean of
-# two dispatches, from `rocprofv3 --pmc FETCH_SIZE` and `--pmc WRITE_SIZE` runs
-# of `bench.py --profile-only <workload> --steps 2`), and what the same two
+# FETCH_SIZE / WRITE_SIZE of the fused scan kernel (k_fused, or k_wide_fused
+# for the 768-d retrieval workload; KiB per dispatch, mean of two dispatches,
+# from `rocprofv3 --pmc FETCH_SIZE` and `--pmc WRITE_SIZE` runs of
+# `bench.py --profile-only <workload> --steps 2`), and what the same two
 # counters read per byte actually moved by a plain 1 GiB device copy
 # (`bench.py --copy-calib 1024 --steps 3`): FETCH_SIZE reads half the bytes,
 # WRITE_SIZE all of them. A kernel change since these were taken makes them
 # stale: set the entry to None until they are taken again.
-TRAFFIC_KIB = {"dsa_bf16_128k": (293450.7, 281896.0), "dsa_fp8_1m": (549479.8, 209533.7)}
+TRAFFIC_KIB = {"dsa_bf16_128k": (293450.7, 281896.0), "dsa_fp8_1m": (549479.8, 209533.7),
+               "retrieval_e7_bf16_5m": (3779755.6, 36603.7)}
 COPY_FACTOR = (0.5000, 1.0000)
 
 
@@ -269,10 +271,12 @@ def retrieval_sweep(steps: int):
     del x, q, keys, qt
     torch.cuda.empty_cache()
     ref = [p for p in points if p["corpus"] == 5000000 and p["k"] == 1024][0]
+    kib = TRAFFIC_KIB.get(cfg.name)
+    traffic = None if kib is None else round(kib[0] * 1024.0 / COPY_FACTOR[0] + kib[1] * 1024.0 / COPY_FACTOR[1])
     return {"workload": cfg.name, "num_queries": cfg.nq, "dim": cfg.d, "dtype": "bf16", "mode": "ip",
             "data": "synthetic unit-normalised Gaussian passages (torch Philox, seeded); queries are corpus passages",
             "roofline": {"bound": "hbm", "achieved": ref["filter_hbm_gbs"], "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                         "frac": ref["filter_hbm_frac"], "traffic": None,
+                         "frac": ref["filter_hbm_frac"], "traffic": traffic,
                          "kernel": "k_wide_fused (score+filter scan), 5M passages, k = 1024",
                          "algorithmic_bytes": 5000000 * cfg.d * 2},
             "points": points}
