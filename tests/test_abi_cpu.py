@@ -73,6 +73,15 @@ def test_workspace_sizes(lib):
     assert lt.lt_indexer_topk_workspace_size(64, 4096, 4, 64, lt.LT_F32, lt.LT_SCORE_DSA, 256, o) == 0
     o.sample_size = 1000
     assert lt.lt_indexer_topk_workspace_size(64, 4096, 4, 64, lt.LT_F32, lt.LT_SCORE_DSA, 256, o) > 0
+    # the 768-d one-head shapes (the wide scan): per-(row, split) lists of
+    # k + max(1024, k/2) slots over 256 splits for a 64-query batch, plus one
+    # shared histogram per row; other long dims are not built
+    for mode in (lt.LT_SCORE_IP, lt.LT_SCORE_DSA):
+        w = lt.lt_indexer_topk_workspace_size(64, 5000000, 1, 768, lt.LT_BF16, mode, 1024)
+        assert w >= 64 * 256 * (1024 + 1024) * 8
+    assert lt.lt_indexer_topk_workspace_size(64, 5000000, 1, 768, lt.LT_F32, lt.LT_SCORE_IP, 1024) == 0
+    assert lt.lt_indexer_topk_workspace_size(64, 5000000, 1, 512, lt.LT_BF16, lt.LT_SCORE_IP, 1024) == 0
+    assert lt.lt_indexer_topk_workspace_size(64, 5000000, 2, 768, lt.LT_BF16, lt.LT_SCORE_IP, 1024) == 0
     # previous-chunk sampler: the per-key counts dominate
     assert lt.lt_sample_from_topk_workspace_size(1 << 20) >= 4 << 20
     assert lt.lt_sample_from_topk_workspace_size(-1) == 0

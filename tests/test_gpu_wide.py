@@ -164,6 +164,38 @@ def test_wide_rows_shorter_than_k_and_empty(lib):
         check_row_tol(gi[t], gs[t], ri[t], rs[t], full[t], int(e[t]), k, RTOL["bf16"])
 
 
+@pytest.mark.parametrize("nk", [0, 5, 31, 33])
+def test_wide_tiny_key_counts(lib, nk):
+    """Fewer keys than one wave tile (or none): every visible key, sorted."""
+    nq, k = 3, 40
+    x = workloads.generate(workloads.scaled(E7, nq=nq, nk=max(nk, 1)), seed=7 + nk)
+    if nk == 0:
+        x["keys"] = x["keys"][:0].contiguous()
+    gi, gs, st = _fused(x, k)
+    if nk == 0:
+        assert np.all(gi == -1) and np.all(np.isneginf(gs))
+        return
+    ri, rs, full = oracle_topk(x, "bf16", k, "ip")
+    for t in range(nq):
+        check_row_tol(gi[t], gs[t], ri[t], rs[t], full[t], nk, k, RTOL["bf16"])
+
+
+def test_wide_all_scores_equal_goes_to_fallback(lib):
+    """Every key identical: every key passes every gate and the threshold bin
+    holds all of them, so every row takes the exact fallback (list overflow or
+    threshold-bin overflow), and equal scores go to the lowest key indices."""
+    nq, nk, k = 66, 20000, 100
+    x = workloads.generate(workloads.scaled(E7, nq=nq, nk=nk), seed=21)
+    x["keys"] = x["keys"][:1].repeat(nk, 1).contiguous()
+    gi, gs, st = _fused(x, k, sorted_output=True)
+    assert np.all((st[:, 2] == 1) | (st[:, 2] == 2)), "expected an overflow: %s" % st[:4]
+    ri, rs, _ = oracle_topk(x, "bf16", k, "ip")
+    np.testing.assert_array_equal(gi, ri)
+    np.testing.assert_array_equal(gi, np.tile(np.arange(k, dtype=np.int32), (nq, 1)))
+    for t in range(nq):
+        assert np.all(np.abs(gs[t].astype(np.float64) - rs[t]) <= 1e-3 * np.abs(rs[t]).max())
+
+
 def _oracle_rows_chunked(q_bits, keys_dev, rows, k, chunk=1 << 19):
     """The oracle's scores and top-k of a few rows over a corpus too large to
     dequantise at once: row_scores over key chunks (each score is one key's
