@@ -322,25 +322,40 @@ __global__ __launch_bounds__(NTH) void k_select(
       uint32_t gpos[PER];
       bool ab[PER], ti[PER];
       uint32_t na = 0, nt = 0;
+      // the PER positions of a thread are consecutive: one binary search for
+      // the list holding the first (the last list whose offset is <= i), a
+      // forward walk for the others; then every load goes out before any is
+      // used, so a step costs one load latency, not PER of them
+      const uint32_t i0 = base + (uint32_t)(tid * PER);
+      int lst[PER];
+      {
+        int lo = 0, hi = ng - 1;
+        const uint32_t i = i0 < gtot ? i0 : gtot - 1;
+        while (lo < hi) {
+          const int mid = (lo + hi + 1) >> 1;
+          if (off[mid] <= i) lo = mid;
+          else hi = mid - 1;
+        }
+#pragma unroll
+        for (int j = 0; j < PER; ++j) {
+          while (lo + 1 < ng && off[lo + 1] <= i0 + (uint32_t)j) ++lo;
+          lst[j] = lo;
+        }
+      }
 #pragma unroll
       for (int j = 0; j < PER; ++j) {
-        const uint32_t i = base + (uint32_t)(tid * PER + j);
-        ab[j] = ti[j] = false;
+        const uint32_t i = i0 + (uint32_t)j;
         ce[j] = make_int2(0, 0);
+        if (i < gtot) ce[j] = cand[((int64_t)row * S + g0 + lst[j]) * cap + (i - off[lst[j]])];
+      }
+#pragma unroll
+      for (int j = 0; j < PER; ++j) {
+        const uint32_t i = i0 + (uint32_t)j;
+        ab[j] = ti[j] = false;
         gpos[j] = 0;
         if (i < gtot) {
-          // the list holding position i: the last one whose offset is <= i
-          int lo = 0, hi = ng - 1;
-          while (lo < hi) {
-            const int mid = (lo + hi + 1) >> 1;
-            if (off[mid] <= i) lo = mid;
-            else hi = mid - 1;
-          }
-          const uint32_t pos = i - off[lo];
-          const int s = g0 + lo;
-          ce[j] = cand[((int64_t)row * S + s) * cap + pos];
           // increases with the key index (keyed: it is the key index)
-          gpos[j] = keyed ? (uint32_t)ce[j].x : (uint32_t)s * (uint32_t)cap + pos;
+          gpos[j] = keyed ? (uint32_t)ce[j].x : (uint32_t)(g0 + lst[j]) * (uint32_t)cap + (i - off[lst[j]]);
           const int b = bin_of(bin_x(__int_as_float(ce[j].y), p.delta, p.c), m);
           ab[j] = b > tau;
           ti[j] = b == tau;
