@@ -48,6 +48,8 @@ LAWS = [
     ("dsa_fp8", "dsa_fp8_1m", 17, 30001, 2048),
     ("adversarial_bf16", "adversarial_bf16_256k", 16, 40000, 2048),
     ("retrieval_bf16", "retrieval_bf16_4m", 70, 50000, 100),
+    ("dsa_bf16_kmax", "dsa_bf16_128k", 10, 30000, 8192),     # the largest k (LT_K_MAX)
+    ("dsa_fp8_kmax", "dsa_fp8_1m", 9, 25000, 8192),
 ]
 
 

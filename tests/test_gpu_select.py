@@ -61,6 +61,7 @@ CASES = [
     (5, 300, 300, 1, "ties", "random"),
     (5, 300, 300, 300, "normal", "none"),
     (4, 257, 260, 512, "special", "random"),
+    (6, 40000, 40000, 8192, "ties", "causal"),     # the largest k (LT_K_MAX)
 ]
 
 
