@@ -160,7 +160,6 @@ __device__ __forceinline__ void wide_scan(const ScoreArgs& a, const Src& src, in
   for (int t = wave; t < ntiles; t += C::WAVES) {
     const int tn = t + C::WAVES < ntiles ? t + C::WAVES : t;
     const uint8_t* np = row_of(tn);
-    sink.begin();
     // the A fragments are the same every tile; an opaque offset keeps the
     // compiler from hoisting all of them (KS * MT * 4 VGPRs) out of the loop
     int qoff = l * 16;
@@ -214,8 +213,8 @@ __device__ __forceinline__ void wide_scan(const ScoreArgs& a, const Src& src, in
 }
 
 // ---------------------------------------------------------------------------
-// Sinks. begin() runs before a tile's MFMAs, consume(k0, kend, sc) after them
-// with the lane's scores of positions k0 + lane % 32.
+// Sinks. consume(k0, kend, sc) runs after a tile's MFMAs with the lane's
+// scores of positions k0 + lane % 32.
 // ---------------------------------------------------------------------------
 
 // Every score to out[t * ld + position] (sample and dense scorers).
@@ -224,7 +223,6 @@ struct WideDenseSink {
   float* out;
   int64_t ld;
   int qbase, nq;
-  __device__ void begin() {}
   __device__ void consume(int k0, int kend, const float (&sc)[C::NI]) {
     const int h = lane_id() >> 5, pos = k0 + (lane_id() & 31);
     if (pos >= kend) return;
@@ -241,7 +239,6 @@ template <class C>
 struct WideRowSink {
   float* out;
   int it_t, h_t;
-  __device__ void begin() {}
   __device__ void consume(int k0, int kend, const float (&sc)[C::NI]) {
     const int h = lane_id() >> 5, pos = k0 + (lane_id() & 31);
     float v = 0.0f;
@@ -253,9 +250,6 @@ struct WideRowSink {
 };
 
 __device__ __forceinline__ int wload(const int* p) {
-  return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-}
-__device__ __forceinline__ uint32_t wload(const uint32_t* p) {
   return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
@@ -333,7 +327,6 @@ struct WideFusedSink {
     });
   }
 
-  __device__ void begin() {}
 
   // the threshold bin of row qbase + rq from its histogram read one tile
   // ago: into the block's bins, and published when it beats the published one
