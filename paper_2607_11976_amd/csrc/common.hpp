@@ -7,6 +7,9 @@
 namespace lt {
 
 constexpr int kWave = 64;
+// Word 3 of a raw buffer descriptor on gfx950 (32-bit data, no swizzle, no
+// stride): offsets are byte offsets range-checked against the record count.
+constexpr int kBufferRaw = 0x00020000;
 constexpr int kMaxBins = 256;
 
 // ---------------------------------------------------------------------------

@@ -235,6 +235,67 @@ __device__ __forceinline__ void load_b(const uint8_t* tile, int nt, typename C::
   }
 }
 
+// The same B fragments with the per-lane part of every address held in a
+// register (one per 16-byte piece) and the tile slot and sub-tile folded into
+// the LDS instruction's immediate offset: row nt * 32 + r sits nt * 32 rows
+// after row r with the same swizzle, since 32 / RPL is a multiple of CPK.
+template <class C>
+struct BLane {
+  using M = typename C::M;
+  static constexpr int PIECES = M::FB == 32 ? 2 * C::KS : C::KS;
+  static constexpr bool ENABLED = (M::FB == 16 || M::FB == 32) && PIECES <= 8;
+  uint32_t o[ENABLED ? PIECES : 1];
+  // o[j]: LDS address of piece j of this lane in slot 0, sub-tile 0
+  __device__ void init(const uint8_t* tiles) {
+    if constexpr (ENABLED) {
+      static_assert((32 / C::RPL) % C::CPK == 0, "sub-tile offset must keep the swizzle");
+      const int l = lane_id(), h = l >> 5, r32 = l & 31;
+      const uint32_t base = (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) uint8_t*)tiles;
+#pragma unroll
+      for (int ks = 0; ks < C::KS; ++ks) {
+        const int byte = ks * M::KI * M::ES + h * M::FB;
+        if constexpr (M::FB == 16) {
+          o[ks] = base + (uint32_t)lds_offset<C>(r32, byte);
+        } else {
+          o[2 * ks] = base + (uint32_t)lds_offset<C>(r32, byte);
+          o[2 * ks + 1] = base + (uint32_t)lds_offset<C>(r32, byte + 16);
+        }
+      }
+    }
+  }
+  // new values each tile as far as the compiler knows, so that it folds the
+  // slot offsets into the instructions instead of keeping one register per
+  // (slot, piece)
+  __device__ void opaque() {
+    if constexpr (ENABLED) {
+#pragma unroll
+      for (int j = 0; j < PIECES; ++j) asm volatile("" : "+v"(o[j]));
+    }
+  }
+};
+
+template <class C, int SLOT, int NT>
+__device__ __forceinline__ void load_b_at(const uint8_t* tiles, const BLane<C>& bl,
+                                          typename C::M::Frag (&b)[C::KS]) {
+  using M = typename C::M;
+  typedef __attribute__((address_space(3))) const i32x4_t* lds_v4;
+  constexpr uint32_t off = SLOT * C::TILE_BYTES + NT * 32 * C::ROWB;
+  if constexpr (BLane<C>::ENABLED) {
+#pragma unroll
+    for (int ks = 0; ks < C::KS; ++ks) {
+      if constexpr (M::FB == 16) {
+        b[ks] = __builtin_bit_cast(typename M::Frag, *(lds_v4)(uintptr_t)(bl.o[ks] + off));
+      } else {
+        const i32x4_t lo = *(lds_v4)(uintptr_t)(bl.o[2 * ks] + off);
+        const i32x4_t hi = *(lds_v4)(uintptr_t)(bl.o[2 * ks + 1] + off);
+        b[ks] = typename M::Frag{lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
+      }
+    }
+  } else {
+    load_b<C>(tiles + SLOT * C::TILE_BYTES, NT, b);
+  }
+}
+
 template <class C>
 __device__ __forceinline__ void mma_half(const WaveQ<C>& s, const typename C::M::Frag (&b)[C::KS],
                                          f32x16_t (&acc)[C::MT]) {
@@ -290,14 +351,14 @@ __device__ __forceinline__ void reduce_half(const WaveQ<C>& s, const f32x16_t (&
     for (int mt = 0; mt < C::MT; ++mt)
 #pragma unroll
       for (int j = 0; j < 8; ++j) z[mt][j] = __builtin_elementwise_max(z[mt][j], (i16x2_t){0, 0});
-    float part[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+    float part[1] = {};
 #pragma unroll
     for (int mt = 0; mt < C::MT; ++mt)
 #pragma unroll
       for (int j = 0; j < 8; ++j)
-        part[j & 3] = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2_t, z[mt][j]), s.wp[mt][j],
-                                                      part[j & 3], false);
-    out[0] = (part[0] + part[1]) + (part[2] + part[3]);
+        part[j % 1] = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2_t, z[mt][j]), s.wp[mt][j],
+                                                      part[j % 1], false);
+    out[0] = part[0];
   } else {
 #pragma unroll
     for (int q = 0; q < C::QW; ++q) out[q] = 0.0f;
@@ -361,7 +422,7 @@ __device__ __forceinline__ void schedule_half() {
 
 // Histogram increment in LDS, issued as plain ds_add_u32. Written as an
 // opaque instruction so that the compiler does not make it wait for the key
-// tiles still streaming into LDS (global_load_lds counts on vmcnt, and the
+// tiles still streaming into LDS (loads into LDS count on vmcnt, and the
 // compiler cannot tell the histogram from the tile ring): LDS operations of
 // one wave complete in order, so the wave's later histogram reads still see
 // the increment, and no other wave reads this wave's histogram rows.
@@ -370,10 +431,14 @@ __device__ __forceinline__ void lds_inc(uint32_t* p) {
   asm volatile("ds_add_u32 %0, %1" ::"v"(a), "v"(1u) : "memory");
 }
 
+// Key sources: consecutive positions (kContig, staged through a buffer
+// descriptor per tile) or a list of key indices (gathered per row).
 struct SrcContig {
+  static constexpr bool kContig = true;
   __device__ int key(int i) const { return i; }
 };
 struct SrcList {
+  static constexpr bool kContig = false;
   const int32_t* list;
   __device__ int key(int i) const {
     const int v = list[i];
@@ -382,46 +447,89 @@ struct SrcList {
 };
 
 // The block-wide scan of positions [kbeg, kend) of `src` (key index =
-// src.key(position)). Keys flow HBM -> VGPR -> LDS through a ring of three
-// tiles (global loads two tiles ahead, one barrier per tile). Each tile is
-// processed in two half steps that overlap the matrix cores with the vector
-// ALUs: while the MFMAs of one 32-key sub-tile run, the epilogue of the other
-// sub-tile (and the sink's gate / write-back for the previous tile) executes.
-// B fragments are read from LDS one half step ahead.
+// src.key(position)). Keys flow HBM -> LDS through a ring of four tiles
+// (loads three tiles ahead, one barrier per tile). Each tile is processed in
+// two half steps that overlap the matrix cores with the vector ALUs: while
+// the MFMAs of one 32-key sub-tile run, the epilogue of the other sub-tile
+// (and the sink's gate / write-back for the previous tile) executes. B
+// fragments are read from LDS one half step ahead. The loop is unrolled over
+// the ring, so every LDS address of a B fragment is a per-lane register plus
+// an immediate.
 template <class C, class Src, class Sink>
 __device__ __forceinline__ void wg_scan(const ScoreArgs& a, const Src& src, int kbeg, int kend, uint8_t* tiles,
                                         const WaveQ<C>& wq, Sink& sink) {
   using Frag = typename C::M::Frag;
   const int tid = threadIdx.x, l = lane_id(), h = l >> 5, r32 = l & 31;
   const uint8_t* keys = static_cast<const uint8_t*>(a.keys);
+  // the bounds are the same in every lane; saying so keeps the per-tile
+  // descriptors below in scalar registers
+  kbeg = __builtin_amdgcn_readfirstlane(kbeg);
+  kend = __builtin_amdgcn_readfirstlane(kend);
   const int nsteps = kend > kbeg ? (kend - kbeg + C::KT - 1) / C::KT : 0;
   if (nsteps == 0) return;
-  // Key tiles go straight from HBM to LDS (global_load_lds_dwordx4): each
-  // instruction of a wave fills 64 consecutive 16-byte chunk slots. Rows past
-  // kend are clamped to the last valid row: their scores are never used
-  // (every consumer masks positions >= kend).
+  // Key tiles go straight from HBM to LDS (loads into LDS, 16 bytes per
+  // lane): each instruction of a wave fills 64 consecutive 16-byte chunk
+  // slots. A contiguous source loads through a buffer descriptor based at the
+  // tile's first key and sized to the keys left before kend: each lane's
+  // offset is fixed for the whole scan, and rows past kend fall outside the
+  // descriptor (their slots hold whatever the hardware returns; every
+  // consumer masks positions >= kend). A list source gathers its rows, past
+  // kend clamped to the last valid position.
   const int wave = __builtin_amdgcn_readfirstlane(tid / kWave);
-  auto stage = [&](int slot, int st_abs, int k0) {
-    if constexpr (C::DT == DT_FP8) {
-      // wave 0 copies the tile's key scales (64 lanes x 4 bytes) ahead of its
-      // key chunks, so the key chunks stay the newest loads in flight
-      if (wave == 0) {
-        const int i = min(k0 + l, kend - 1);
-        const float* g = a.k_scale + src.key(i);
-        uint8_t* d = tiles + C::RING * C::TILE_BYTES + (st_abs & (C::SCALE_RING - 1)) * C::KT * 4;
-        __builtin_amdgcn_global_load_lds((const void __attribute__((address_space(1)))*)g,
-                                         (void __attribute__((address_space(3)))*)d, 4, 0, 0);
-      }
-    }
+  uint32_t voff[C::CPT];
 #pragma unroll
-    for (int c = 0; c < C::CPT; ++c) {
-      const int u0 = (c * C::WAVES + wave) * kWave;  // first chunk slot of this instruction
-      const int u = u0 + l, n = u / C::CPK, part = (u ^ C::swz(n)) & (C::CPK - 1);
-      const int i = min(k0 + n, kend - 1);
-      const uint8_t* g = keys + (int64_t)src.key(i) * C::ROWB + part * 16;
-      uint8_t* d = tiles + slot * C::TILE_BYTES + u0 * 16;
-      __builtin_amdgcn_global_load_lds((const void __attribute__((address_space(1)))*)g,
-                                       (void __attribute__((address_space(3)))*)d, 16, 0, 0);
+  for (int c = 0; c < C::CPT; ++c) {
+    const int u = (c * C::WAVES + wave) * kWave + l, n = u / C::CPK, part = (u ^ C::swz(n)) & (C::CPK - 1);
+    voff[c] = (uint32_t)(n * C::ROWB + part * 16);
+  }
+  auto stage = [&](int slot, int st_abs, int k0) {
+    if constexpr (Src::kContig) {
+      // rows of this tile before kend, kept in a scalar register (a vector
+      // clamp would make the descriptor look different per lane)
+      int rows = kend - k0;
+      asm volatile("" : "+s"(rows));
+      rows = rows < 0 ? 0 : rows;
+      asm volatile("" : "+s"(rows));
+      rows = rows > C::KT ? C::KT : rows;
+      if constexpr (C::DT == DT_FP8) {
+        // wave 0 copies the tile's key scales (64 lanes x 4 bytes) ahead of
+        // its key chunks, so the key chunks stay the newest loads in flight
+        if (wave == 0) {
+          uint8_t* d = tiles + C::RING * C::TILE_BYTES + (st_abs & (C::SCALE_RING - 1)) * C::KT * 4;
+          const __amdgpu_buffer_rsrc_t rs =
+              __builtin_amdgcn_make_buffer_rsrc((void*)(a.k_scale + k0), 0, rows * 4, kBufferRaw);
+          __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, (void __attribute__((address_space(3)))*)d, 4,
+                                                   (uint32_t)l * 4u, 0, 0, 0);
+        }
+      }
+      const __amdgpu_buffer_rsrc_t rs =
+          __builtin_amdgcn_make_buffer_rsrc((void*)(keys + (int64_t)k0 * C::ROWB), 0, rows * C::ROWB, kBufferRaw);
+#pragma unroll
+      for (int c = 0; c < C::CPT; ++c) {
+        uint8_t* d = tiles + slot * C::TILE_BYTES + (c * C::WAVES + wave) * kWave * 16;
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, (void __attribute__((address_space(3)))*)d, 16, voff[c], 0, 0,
+                                                 0);
+      }
+    } else {
+      if constexpr (C::DT == DT_FP8) {
+        if (wave == 0) {
+          const int i = min(k0 + l, kend - 1);
+          const float* g = a.k_scale + src.key(i);
+          uint8_t* d = tiles + C::RING * C::TILE_BYTES + (st_abs & (C::SCALE_RING - 1)) * C::KT * 4;
+          __builtin_amdgcn_global_load_lds((const void __attribute__((address_space(1)))*)g,
+                                           (void __attribute__((address_space(3)))*)d, 4, 0, 0);
+        }
+      }
+#pragma unroll
+      for (int c = 0; c < C::CPT; ++c) {
+        const int u0 = (c * C::WAVES + wave) * kWave;  // first chunk slot of this instruction
+        const int u = u0 + l, n = u / C::CPK, part = (u ^ C::swz(n)) & (C::CPK - 1);
+        const int i = min(k0 + n, kend - 1);
+        const uint8_t* g = keys + (int64_t)src.key(i) * C::ROWB + part * 16;
+        uint8_t* d = tiles + slot * C::TILE_BYTES + u0 * 16;
+        __builtin_amdgcn_global_load_lds((const void __attribute__((address_space(1)))*)g,
+                                         (void __attribute__((address_space(3)))*)d, 16, 0, 0);
+      }
     }
   };
   // Wait until at most `n` of this wave's vector-memory operations are in
@@ -460,16 +568,20 @@ __device__ __forceinline__ void wg_scan(const ScoreArgs& a, const Src& src, int 
   float h0[C::NIH], h1[C::NIH];
 #pragma unroll
   for (int j = 0; j < C::NIH; ++j) h0[j] = 0.0f;
-  load_b<C>(tiles, 0, b0);
-  for (int st = 0; st < nsteps; ++st) {
-    const uint8_t* tl = tiles + (st & (C::RING - 1)) * C::TILE_BYTES;
-    const uint8_t* tn = tiles + ((st + 1) & (C::RING - 1)) * C::TILE_BYTES;
+  BLane<C> bl;
+  bl.init(tiles);
+  load_b_at<C, 0, 0>(tiles, bl, b0);
+  // one tile; SLOT = st % RING, a constant in every copy of the body
+  static_assert(C::RING == 4, "the loop is unrolled over the ring");
+  auto body = [&](auto SLOT_, int st) {
+    constexpr int SLOT = decltype(SLOT_)::value;
+    bl.opaque();
     // slot of tile st-1 is free: every wave passed the barrier after reading it
-    stage((st + 3) & (C::RING - 1), st + 3, kbeg + (st + 3) * C::KT);
+    stage((SLOT + 3) & 3, st + 3, kbeg + (st + 3) * C::KT);
     // half step A: MFMA sub-tile 0 of tile st || epilogue of sub-tile 1 of st-1,
     // B fragments of sub-tile 1 read as the slots free up
     mma_half<C>(wq, b0, acc0);
-    load_b<C>(tl, 1, b1);
+    load_b_at<C, SLOT, 1>(tiles, bl, b1);
     reduce_half<C>(wq, acc1, h1);
     float sc[C::NI];
     scores(st - 1, h0, h1, sc);
@@ -477,7 +589,7 @@ __device__ __forceinline__ void wg_scan(const ScoreArgs& a, const Src& src, int 
     // half step B: MFMA sub-tile 1 of tile st || epilogue of sub-tile 0 of st,
     // B fragments of the next tile's sub-tile 0 read as the slots free up
     mma_half<C>(wq, b1, acc1);
-    load_b<C>(tn, 0, b0);
+    load_b_at<C, (SLOT + 1) & 3, 0>(tiles, bl, b0);
     reduce_half<C>(wq, acc0, h0);
     schedule_half<C>();
     // h0 is only read in the next step; without this use the compiler sinks
@@ -487,7 +599,21 @@ __device__ __forceinline__ void wg_scan(const ScoreArgs& a, const Src& src, int 
     // gate + write-back of tile st-1 while the last MFMAs drain
     sink.consume(st - 1, kbeg + (st - 1) * C::KT, kend, sc, st > 0);
     sync_tiles(1);  // tile st+2 landed; tile st+3 may still be in flight
+  };
+  using I0 = std::integral_constant<int, 0>;
+  using I1 = std::integral_constant<int, 1>;
+  using I2 = std::integral_constant<int, 2>;
+  using I3 = std::integral_constant<int, 3>;
+  int st = 0;
+  for (; st + C::RING <= nsteps; st += C::RING) {
+    body(I0{}, st);
+    body(I1{}, st + 1);
+    body(I2{}, st + 2);
+    body(I3{}, st + 3);
   }
+  if (st < nsteps) body(I0{}, st++);
+  if (st < nsteps) body(I1{}, st++);
+  if (st < nsteps) body(I2{}, st++);
   reduce_half<C>(wq, acc1, h1);
   float sc[C::NI];
   scores(nsteps - 1, h0, h1, sc);
@@ -866,7 +992,8 @@ template <class C>
 __global__ __launch_bounds__(C::NTHREADS) void k_sample(ScoreArgs a, const int32_t* list, int ns, float* samp,
                                                         int slice) {
   extern __shared__ __align__(16) uint8_t lds[];
-  const int q0 = blockIdx.x * C::QT, wave = threadIdx.x / kWave, qbase = q0 + wave * C::QW;
+  const int q0 = blockIdx.x * C::QT, wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave),
+            qbase = q0 + wave * C::QW;
   const int kb = blockIdx.y * slice, ke = min(kb + slice, ns);
   WaveQ<C> wq;
   load_q<C>(wq, a, qbase);
@@ -877,7 +1004,8 @@ __global__ __launch_bounds__(C::NTHREADS) void k_sample(ScoreArgs a, const int32
 template <class C>
 __global__ __launch_bounds__(C::NTHREADS) void k_dense(ScoreArgs a, float* out, int64_t ld, int slice) {
   extern __shared__ __align__(16) uint8_t lds[];
-  const int q0 = blockIdx.x * C::QT, wave = threadIdx.x / kWave, qbase = q0 + wave * C::QW;
+  const int q0 = blockIdx.x * C::QT, wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave),
+            qbase = q0 + wave * C::QW;
   const int kb = blockIdx.y * slice, ke = min(kb + slice, a.nk);
   WaveQ<C> wq;
   load_q<C>(wq, a, qbase);
@@ -894,7 +1022,8 @@ __global__ __launch_bounds__(C::NTHREADS) void k_fused(ScoreArgs a, const RowPar
   int* emax = reinterpret_cast<int*>(hist + C::QT * m);
   int* smin = emax + 1;
   const int tile = blockIdx.x / S, split = blockIdx.x - tile * S;
-  const int q0 = tile * C::QT, wave = threadIdx.x / kWave, qbase = q0 + wave * C::QW;
+  const int q0 = tile * C::QT, wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave),
+            qbase = q0 + wave * C::QW;
   for (int i = threadIdx.x; i < C::QT * m; i += C::NTHREADS) hist[i] = 0u;
   if (threadIdx.x == 0) {
     *emax = 0;
@@ -935,7 +1064,7 @@ __global__ __launch_bounds__(C::NTHREADS) void k_fused_fallback(ScoreArgs a, int
                                                                 float* scratch, int32_t* out_i, float* out_s) {
   extern __shared__ __align__(16) uint8_t lds[];
   const uint32_t n = qctl[0];
-  const int wave = threadIdx.x / kWave;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
   for (uint32_t r = blockIdx.x; r < n; r += gridDim.x) {
     const int row = queue[r];
     const int q0 = (row / C::QT) * C::QT, qbase = q0 + wave * C::QW;

@@ -51,9 +51,7 @@ typedef __attribute__((address_space(3))) uint32_t lds_u32_t;
 typedef __attribute__((address_space(3))) int lds_i32_t;
 typedef uint32_t wu32x4_t __attribute__((ext_vector_type(4)));
 
-// Raw buffer descriptor word 3 for gfx950 (32-bit data, no swizzle), and the
-// cache policy of a device-coherent load (sc1, as for agent-scope atomics).
-constexpr int kBufferFlags = 0x00020000;
+// Cache policy of a device-coherent load (sc1, as for agent-scope atomics).
 constexpr int kCoherent = 0x10;
 typedef float wf32x16_t __attribute__((ext_vector_type(16)));
 typedef int wi32x4_t __attribute__((ext_vector_type(4)));
@@ -365,7 +363,7 @@ struct WideFusedSink {
     flush(q);
     // one device-coherent 16-byte read per lane (bins past m read as 0: the
     // buffer covers the row only)
-    const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(hr, 0, m * 4, kBufferFlags);
+    const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(hr, 0, m * 4, kBufferRaw);
     const wu32x4_t v = __builtin_amdgcn_raw_buffer_load_b128(rs, l * 16, 0, kCoherent);
 #pragma unroll
     for (int j = 0; j < 4; ++j) rh[j] = 4 * l + j < m ? v[j] : 0u;
