@@ -79,7 +79,19 @@ def timed_steps(fn, steps, warmup):
     return (time.perf_counter() - t0) * 1e3 / steps
 
 
-def measure(name: str, steps: int, warmup: int, unfused: bool):
+def step_summary(res) -> dict:
+    """Per-call device times of the timed calls (warm caches) and of calls
+    after a cache flush (cold), in milliseconds."""
+    out = {"warm_mean": round(float(np.mean(res["call_ms"])), 4),
+           "warm_median": round(float(np.median(res["call_ms"])), 4),
+           "warm_min": round(float(np.min(res["call_ms"])), 4)}
+    if res["cold_ms"]:
+        out.update({"cold_calls": len(res["cold_ms"]), "cold_median": round(float(np.median(res["cold_ms"])), 4),
+                    "cold_min": round(float(np.min(res["cold_ms"])), 4)})
+    return out
+
+
+def measure(name: str, steps: int, warmup: int, unfused: bool, cold: int = 5):
     cfg = workloads.CONFIGS[name]
     x = workloads.generate(cfg, seed=workloads.CONFIG_SEEDS[name])
     dev = torch.device("cuda")
@@ -102,24 +114,45 @@ def measure(name: str, steps: int, warmup: int, unfused: bool):
 
     for _ in range(warmup):
         step(0)
+    # device time of every timed call (events on the stream the library runs on)
+    marks = [torch.cuda.Event(enable_timing=True) for _ in range(steps + 1)]
     torch.cuda.synchronize()
     t0 = time.perf_counter()
+    marks[0].record()
     for i in range(steps):
         step(i)
+        marks[i + 1].record()
     torch.cuda.synchronize()
     ms = (time.perf_counter() - t0) * 1e3 / steps
+    call_ms = [marks[i].elapsed_time(marks[i + 1]) for i in range(steps)]
     stages = {s: 0.0 for s in lt.STAGES}
     for e in evs:
         for s, v in e.stage_ms().items():
             stages[s] += v / steps
         e.close()
 
+    # cold caches: before each call, overwrite a 512 MiB buffer so that the
+    # inputs are no longer in the L2s or the 256 MB Infinity Cache
+    flush = torch.empty(512 << 20, dtype=torch.uint8, device=dev)
+    cold_ms = []
+    opt_plain = lt.make_options()
+    for i in range(cold):
+        flush.fill_(i & 0xFF)
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        lt.indexer_topk(q, w, keys, k, offs, qs, ks, mode=cfg.mode, options=opt_plain, out=out, workspace=ws)
+        e1.record()
+        torch.cuda.synchronize()
+        cold_ms.append(e0.elapsed_time(e1))
+    del flush
+
     # survivors and fallback rows (untimed call with row statistics)
     stats = torch.zeros((nq, 4), dtype=torch.int32, device=dev)
     lt.indexer_topk(q, w, keys, k, offs, qs, ks, mode=cfg.mode, options=lt.make_options(row_stats=stats),
                     out=out, workspace=ws)
     st = stats.cpu().numpy()
-    res = dict(ms=ms, pairs=pairs, stages=stages, survivors_mean=float(st[:, 0].mean()),
+    res = dict(ms=ms, pairs=pairs, stages=stages, call_ms=call_ms, cold_ms=cold_ms,
+               survivors_mean=float(st[:, 0].mean()),
                survivors_max=int(st[:, 0].max()), fallback_rows=int((st[:, 2] != 0).sum()),
                tie_bin_mean=float(st[:, 3].mean()))
 
@@ -414,6 +447,7 @@ def main():
                    "parallelism": "single GPU"},
         "roofline": roofline(cfg, res),
         "stages_ms": {k: round(v, 4) for k, v in res["stages"].items()},
+        "call_ms": step_summary(res),
         "survivors_per_row": {"mean": round(res["survivors_mean"], 1), "max": res["survivors_max"],
                               "threshold_bin_mean": round(res["tie_bin_mean"], 1)},
         "fallback_rows": res["fallback_rows"],
@@ -433,6 +467,7 @@ def main():
         m = {"workload": "dsa_fp8_1m", "dtype": "fp8", "ms_per_step": round(res2["ms"], 4),
              "value": res2["pairs"] / (res2["ms"] * 1e-3), "unit": "pairs/s", "visible_pairs": res2["pairs"],
              "roofline": roofline(cfg2, res2), "stages_ms": {k: round(v, 4) for k, v in res2["stages"].items()},
+             "call_ms": step_summary(res2),
              "survivors_per_row_mean": round(res2["survivors_mean"], 1), "fallback_rows": res2["fallback_rows"]}
         if "unfused_ms" in res2:
             m["unfused_ms_per_step"] = round(res2["unfused_ms"], 4)
