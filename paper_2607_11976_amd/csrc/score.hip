@@ -129,9 +129,14 @@ struct Cfg {
   static constexpr int NI = GROUPED ? NT * MT * 4 * GPQ : NT * QW / 2;  // scores per lane per tile
   static constexpr int NIH = GROUPED ? MT * 4 * GPQ : QW;              // per-lane results of one sub-tile
   // epilogue VALU ops of one sub-tile (ReLU + FMA per accumulator element)
-  // spread over the MFMAs of the other sub-tile
+  // spread over the MFMAs of the other sub-tile. The 64-head values leave
+  // room for the combine and gate work of the half step too (measured best
+  // on MI355X: 5 for bf16, 17 for fp8, against 4 and 13 for the epilogue
+  // alone).
   static constexpr int VALU_PER_MFMA =
-      ((DT == DT_FP8 && H >= 8 && RELU && QW == 1 ? 26 : 32) * MT + KS * MT - 1) / (KS * MT);
+      H == 64 && QW == 1 && DT == DT_BF16  ? 5
+      : H == 64 && QW == 1 && DT == DT_FP8 ? 17
+      : ((DT == DT_FP8 && H >= 8 && RELU && QW == 1 ? 26 : 32) * MT + KS * MT - 1) / (KS * MT);
   static_assert((QW * H) % 32 == 0, "a wave must fill whole M tiles");
   static_assert(NT == 2, "the scan pipelines the two 32-key halves of a tile");
   static_assert(CHUNKS % NTHREADS == 0 && CPT < 16, "tile staging assumes whole instructions per thread");
