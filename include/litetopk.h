@@ -100,7 +100,9 @@ typedef struct lt_options {
   int32_t capacity;        /* candidate slots per (row, key split); <= 0 = default
                               max(12k, 2048) (sec. 4.2: 12k for k = 2048), and
                               k + max(1024, k/2) for the 768-dimensional shapes,
-                              whose splits share one threshold                 */
+                              whose splits share one threshold (for those shapes
+                              rounded up to a multiple of 16: their lists are
+                              stored in chunks of 16 entries)                  */
   int32_t key_splits;      /* key-range splits per row; 0 = auto (fused), 1 (scores-in) */
   uint32_t flags;          /* LT_SORTED_OUTPUT | LT_FORCE_FALLBACK               */
   uint64_t seed;           /* seed of the key sample                             */

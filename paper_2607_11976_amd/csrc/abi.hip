@@ -122,6 +122,8 @@ Resolved resolve_fused(const lt_options* o, int nq, int nk, int k, int mode, con
     // refreshes; k more keeps a row whose whole top-k lies in one split
     r.cap = k + std::max(1024, k / 2);
   }
+  // the shared scan's lists are stored in chunks of 16 entries
+  if (r.shared) r.cap = (r.cap + 15) & ~15;
   r.ns = resolve_sample(o, r, nk, k, mode, true);
   const int steps = (nk + sh.keys_per_step - 1) / sh.keys_per_step;
   const int tiles = (nq + sh.queries_per_block - 1) / sh.queries_per_block;

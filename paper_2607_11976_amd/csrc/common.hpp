@@ -12,6 +12,15 @@ constexpr int kWave = 64;
 constexpr int kBufferRaw = 0x00020000;
 constexpr int kMaxBins = 256;
 
+// Candidate lists of the shared-threshold (768-d) scan: `nlists` lists of
+// `cap` entries (cap a multiple of 16) stored in 128-byte chunks of 16
+// entries, chunk c of every list before chunk c + 1 of any. The lists grow
+// a few entries at a time in every block, so the chunks being appended to sit
+// together in a few megabytes instead of one page per list.
+__host__ __device__ constexpr int64_t ilv_index(int64_t list, uint32_t pos, int64_t nlists) {
+  return (int64_t)(pos >> 4) * nlists * 16 + list * 16 + (pos & 15u);
+}
+
 // ---------------------------------------------------------------------------
 // Total order on float32 scores (selection, Eq. 2 with ties made unique):
 // higher first, -0 == +0, NaN below -inf. ord_key maps a score to an unsigned

@@ -346,7 +346,11 @@ __global__ __launch_bounds__(NTH) void k_select(
       for (int j = 0; j < PER; ++j) {
         const uint32_t i = i0 + (uint32_t)j;
         ce[j] = make_int2(0, 0);
-        if (i < gtot) ce[j] = cand[((int64_t)row * S + g0 + lst[j]) * cap + (i - off[lst[j]])];
+        if (i < gtot) {
+          const int64_t li = (int64_t)row * S + g0 + lst[j];
+          const uint32_t pos = i - off[lst[j]];
+          ce[j] = cand[keyed ? ilv_index(li, pos, (int64_t)nq * S) : li * cap + pos];
+        }
       }
 #pragma unroll
       for (int j = 0; j < PER; ++j) {

@@ -413,7 +413,7 @@ struct WideFusedSink {
         const float s = scv[it];
         const uint32_t pos = h ? bb + mbcnt64(m2) - lo : ba + mbcnt64(m2);
         const int64_t t = qbase + (h ? qb : qa);
-        if (pos < (uint32_t)cap) cand[(t * S + split) * cap + pos] = make_int2(key, __float_as_int(s));
+        if (pos < (uint32_t)cap) cand[ilv_index(t * S + split, pos, (int64_t)nq * S)] = make_int2(key, __float_as_int(s));
         const float x = fmaf(s, h ? db : da, h ? cb : ca);
         if (x >= 0.0f)
           __hip_atomic_fetch_add(bh + (h ? qb : qa) * m + min(__float2int_rz(x), m - 1), 1u, __ATOMIC_RELAXED,
