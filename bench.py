@@ -57,8 +57,8 @@ HBM_PEAK_GBS = 8000.0
 # (`bench.py --copy-calib 1024 --steps 3`): FETCH_SIZE reads half the bytes,
 # WRITE_SIZE all of them. A kernel change since these were taken makes them
 # stale: set the entry to None until they are taken again.
-TRAFFIC_KIB = {"dsa_bf16_128k": (293570.3, 281898.2), "dsa_fp8_1m": (549560.0, 209530.9),
-               "retrieval_e7_bf16_5m": (3779755.6, 36603.7)}
+TRAFFIC_KIB = {"dsa_bf16_128k": (293568.2, 281895.8), "dsa_fp8_1m": (549560.8, 209531.3),
+               "retrieval_e7_bf16_5m": (3779409.1, 35678.8)}
 COPY_FACTOR = (0.5000, 1.0000)
 
 
