@@ -442,14 +442,18 @@ struct SrcContig {
   static constexpr bool kContig = true;
   __device__ int key(int i) const { return i; }
 };
-struct SrcList {
+template <bool FAR>
+struct SrcListT {
   static constexpr bool kContig = false;
+  static constexpr bool kFar = FAR;  // keys beyond 4 GiB: per-lane global addresses
   const int32_t* list;
-  __device__ int key(int i) const {
-    const int v = list[i];
-    return v < 0 ? 0 : v;
-  }
+  __device__ int raw(int i) const { return list[i]; }
+  // a list entry as a key index (hole markers -1 read key 0; never used)
+  __device__ static int clamp(int v) { return v < 0 ? 0 : v; }
+  __device__ int key(int i) const { return clamp(raw(i)); }
 };
+using SrcList = SrcListT<false>;
+using SrcListFar = SrcListT<true>;
 
 // The block-wide scan of positions [kbeg, kend) of `src` (key index =
 // src.key(position)). Keys flow HBM -> LDS through a ring of four tiles
@@ -487,6 +491,21 @@ __device__ __forceinline__ void wg_scan(const ScoreArgs& a, const Src& src, int 
     const int u = (c * C::WAVES + wave) * kWave + l, n = u / C::CPK, part = (u ^ C::swz(n)) & (C::CPK - 1);
     voff[c] = (uint32_t)(n * C::ROWB + part * 16);
   }
+  // A list source's key indices for the next tile to stage, read one tile
+  // ahead: a list read that the stage itself waited on would also wait for
+  // every tile load in flight (vector-memory loads complete in issue order).
+  int lk[C::CPT], lks = 0;
+  auto list_keys = [&](int k0) {
+    if constexpr (!Src::kContig) {
+#pragma unroll
+      for (int c = 0; c < C::CPT; ++c) {
+        const int u = (c * C::WAVES + wave) * kWave + l, n = u / C::CPK;
+        lk[c] = src.raw(min(k0 + n, kend - 1));
+      }
+      if constexpr (C::DT == DT_FP8) lks = src.raw(min(k0 + l, kend - 1));
+    }
+  };
+  list_keys(kbeg);
   auto stage = [&](int slot, int st_abs, int k0) {
     if constexpr (Src::kContig) {
       // rows of this tile before kend, kept in a scalar register (a vector
@@ -516,24 +535,53 @@ __device__ __forceinline__ void wg_scan(const ScoreArgs& a, const Src& src, int 
                                                  0);
       }
     } else {
-      if constexpr (C::DT == DT_FP8) {
-        if (wave == 0) {
-          const int i = min(k0 + l, kend - 1);
-          const float* g = a.k_scale + src.key(i);
-          uint8_t* d = tiles + C::RING * C::TILE_BYTES + (st_abs & (C::SCALE_RING - 1)) * C::KT * 4;
-          __builtin_amdgcn_global_load_lds((const void __attribute__((address_space(1)))*)g,
-                                           (void __attribute__((address_space(3)))*)d, 4, 0, 0);
-        }
-      }
+      // addresses from the keys read one tile ago; then the next tile's keys,
+      // issued ahead of this tile's loads so that the tile wait covers them
+      const uint32_t soff = (uint32_t)Src::clamp(lks);
+      const float* gs = a.k_scale + soff;
+      const uint8_t* g[C::CPT];
 #pragma unroll
       for (int c = 0; c < C::CPT; ++c) {
-        const int u0 = (c * C::WAVES + wave) * kWave;  // first chunk slot of this instruction
-        const int u = u0 + l, n = u / C::CPK, part = (u ^ C::swz(n)) & (C::CPK - 1);
-        const int i = min(k0 + n, kend - 1);
-        const uint8_t* g = keys + (int64_t)src.key(i) * C::ROWB + part * 16;
-        uint8_t* d = tiles + slot * C::TILE_BYTES + u0 * 16;
-        __builtin_amdgcn_global_load_lds((const void __attribute__((address_space(1)))*)g,
-                                         (void __attribute__((address_space(3)))*)d, 16, 0, 0);
+        const int u = (c * C::WAVES + wave) * kWave + l, n = u / C::CPK, part = (u ^ C::swz(n)) & (C::CPK - 1);
+        g[c] = keys + (int64_t)Src::clamp(lk[c]) * C::ROWB + part * 16;
+      }
+      list_keys(k0 + C::KT);
+      asm volatile("" ::: "memory");
+      if constexpr (!Src::kFar) {
+        // keys within 4 GiB: byte offsets from the array's start through a
+        // buffer descriptor (loads into LDS through a descriptor keep the
+        // compiler's LDS waits exact; see the contiguous case)
+        if constexpr (C::DT == DT_FP8) {
+          if (wave == 0) {
+            uint8_t* d = tiles + C::RING * C::TILE_BYTES + (st_abs & (C::SCALE_RING - 1)) * C::KT * 4;
+            const __amdgpu_buffer_rsrc_t rs =
+                __builtin_amdgcn_make_buffer_rsrc((void*)a.k_scale, 0, a.nk * 4, kBufferRaw);
+            __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, (void __attribute__((address_space(3)))*)d, 4,
+                                                     soff * 4u, 0, 0, 0);
+          }
+        }
+        const __amdgpu_buffer_rsrc_t rs =
+            __builtin_amdgcn_make_buffer_rsrc((void*)keys, 0, (int)((uint32_t)a.nk * (uint32_t)C::ROWB), kBufferRaw);
+#pragma unroll
+        for (int c = 0; c < C::CPT; ++c) {
+          uint8_t* d = tiles + slot * C::TILE_BYTES + (c * C::WAVES + wave) * kWave * 16;
+          __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, (void __attribute__((address_space(3)))*)d, 16,
+                                                   (uint32_t)(g[c] - keys), 0, 0, 0);
+        }
+      } else {
+        if constexpr (C::DT == DT_FP8) {
+          if (wave == 0) {
+            uint8_t* d = tiles + C::RING * C::TILE_BYTES + (st_abs & (C::SCALE_RING - 1)) * C::KT * 4;
+            __builtin_amdgcn_global_load_lds((const void __attribute__((address_space(1)))*)gs,
+                                             (void __attribute__((address_space(3)))*)d, 4, 0, 0);
+          }
+        }
+#pragma unroll
+        for (int c = 0; c < C::CPT; ++c) {
+          uint8_t* d = tiles + slot * C::TILE_BYTES + (c * C::WAVES + wave) * kWave * 16;
+          __builtin_amdgcn_global_load_lds((const void __attribute__((address_space(1)))*)g[c],
+                                           (void __attribute__((address_space(3)))*)d, 16, 0, 0);
+        }
       }
     }
   };
@@ -993,7 +1041,7 @@ struct GroupedSink {
 // ---------------------------------------------------------------------------
 // Kernels
 // ---------------------------------------------------------------------------
-template <class C>
+template <class C, bool FAR>
 __global__ __launch_bounds__(C::NTHREADS) void k_sample(ScoreArgs a, const int32_t* list, int ns, float* samp,
                                                         int slice) {
   extern __shared__ __align__(16) uint8_t lds[];
@@ -1003,7 +1051,7 @@ __global__ __launch_bounds__(C::NTHREADS) void k_sample(ScoreArgs a, const int32
   WaveQ<C> wq;
   load_q<C>(wq, a, qbase);
   DenseSink<C> sink{samp, ns, qbase, a.nq};
-  wg_scan<C>(a, SrcList{list}, kb, ke, lds, wq, sink);
+  wg_scan<C>(a, SrcListT<FAR>{list}, kb, ke, lds, wq, sink);
 }
 
 template <class C>
@@ -1145,7 +1193,12 @@ hipError_t launch_sample_scores(const ScoreArgs& a, const int32_t* list, int ns,
       err = hipSuccess;
       return;
     }
-    hipLaunchKernelGGL(k_sample<C>, grid, dim3(C::NTHREADS), C::SCAN_LDS, st, a, list, ns, samp, slice);
+    // a buffer descriptor reaches 4 GiB of keys; larger key arrays gather
+    // through per-lane global addresses
+    if ((uint64_t)a.nk * C::ROWB < (1ull << 32))
+      hipLaunchKernelGGL((k_sample<C, false>), grid, dim3(C::NTHREADS), C::SCAN_LDS, st, a, list, ns, samp, slice);
+    else
+      hipLaunchKernelGGL((k_sample<C, true>), grid, dim3(C::NTHREADS), C::SCAN_LDS, st, a, list, ns, samp, slice);
     err = hipGetLastError();
   });
   return err;

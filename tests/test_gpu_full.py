@@ -103,3 +103,43 @@ def test_full_size_retrieval(lib):
     fi_h, fs_h = fi.cpu().numpy(), fs.cpu().numpy()
     for j, t in enumerate(rows):
         check_row_tol(fi_h[t], fs_h[t], oi[j], os_[j], full[j], nk, k, RTOL[cfg.dtype])
+
+
+@pytest.mark.parametrize("over", [False, True])
+@pytest.mark.parametrize("dtype,h,mode", [("bf16", 64, "dsa"), ("bf16", 1, "ip"), ("fp8", 64, "dsa")])
+def test_sample_scan_around_4gib_of_keys(lib, dtype, h, mode, over):
+    """Key arrays just under and just over 4 GiB: the sample scorer gathers
+    its rows through one buffer descriptor (byte offsets up to 4 GiB) below
+    that size, through per-lane global addresses above it. The fused result
+    must equal radix selection over the dense scores, with no row taking the
+    fallback (a wrong sample threshold would send rows there)."""
+    d, nq, k = 128, 8, 64
+    row_bytes = d * (2 if dtype == "bf16" else 1)
+    nk = (1 << 32) // row_bytes + (4096 if over else -64)
+    g = torch.Generator(device="cuda").manual_seed(7)
+    if dtype == "bf16":
+        keys = (torch.randn((nk, d), device="cuda", generator=g) * 0.1).to(torch.bfloat16)
+        q = (torch.randn((nq, h, d), device="cuda", generator=g) * 0.1).to(torch.bfloat16)
+        qs = ks = None
+    else:
+        # E4M3FN bytes without the two NaN encodings (0x7F, 0xFF)
+        keys = torch.randint(0, 0x7F, (nk, d), device="cuda", generator=g, dtype=torch.int32)
+        keys = (keys | (torch.randint(0, 2, (nk, d), device="cuda", generator=g, dtype=torch.int32) << 7)).to(torch.uint8)
+        q = torch.randint(0, 0x7F, (nq, h, d), device="cuda", generator=g, dtype=torch.int32).to(torch.uint8)
+        qs = torch.rand((nq, h), device="cuda", generator=g) * 1e-2 + 1e-3
+        ks = torch.rand((nk,), device="cuda", generator=g) * 1e-2 + 1e-3
+    w = torch.rand((nq, h), device="cuda", generator=g) if mode == "dsa" else None
+    stats = torch.zeros((nq, 4), dtype=torch.int32, device="cuda")
+    # a sample large enough for the range estimate to hold the top-k of 2^25
+    # keys (the default 3k keys would put every top-k key in the clamped top
+    # bin and send the rows to the fallback by design)
+    opts = lt.make_options(row_stats=stats, sample_size=65536)
+    fi, fs = lt.indexer_topk(q, w, keys, k, None, qs, ks, mode=mode, options=opts)
+    dense = lt.indexer_scores(q, w, keys, qs, ks, mode=mode)
+    ri, rs = lt.topk_radix(dense, k, sorted_output=True)
+    torch.cuda.synchronize()
+    del dense, keys
+    gi, gs = _sorted_pairs(fi, fs)
+    np.testing.assert_array_equal(gi, ri.cpu().numpy())
+    np.testing.assert_array_equal(gs.view(np.uint32), rs.cpu().numpy().view(np.uint32))
+    assert int((stats[:, 2] != 0).sum()) == 0, "rows took the fallback"
