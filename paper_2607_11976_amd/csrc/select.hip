@@ -26,7 +26,7 @@ __global__ void k_init(uint32_t* qctl) {
 // kRangeUnroll loads in flight: the kernel is bound by load latency.
 // ---------------------------------------------------------------------------
 constexpr int kRangeThreads = 256;
-constexpr int kRangeThreadsLarge = 1024;  // samples of kRangeLargeSample keys or more
+constexpr int kRangeThreadsLarge = 1024;  // samples of kRangeLargeSample keys or more, or few rows
 constexpr int kRangeLargeSample = 16384;
 constexpr int kRangeUnroll = 8;
 
@@ -479,8 +479,10 @@ hipError_t launch_range(bool from_scores, const float* src, int64_t stride, int 
   auto go = [&](auto kernel, int nth) {
     hipLaunchKernelGGL(kernel, grid, dim3(nth), 0, st, src, stride, nq, nk, offs, starts, list, ns, m, k, params);
   };
-  // a long sample is read in fewer, wider steps (the kernel waits on loads)
-  const bool large = ns >= kRangeLargeSample;
+  // a long sample is read in fewer, wider steps (the kernel waits on loads);
+  // so are the rows of a launch of few rows, which otherwise leaves most of
+  // the GPU idle
+  const bool large = ns >= kRangeLargeSample || nq <= kSelFewRows;
   if (from_scores) {
     if (large) go(k_range<kRangeThreadsLarge, true>, kRangeThreadsLarge);
     else go(k_range<kRangeThreads, true>, kRangeThreads);
