@@ -66,7 +66,7 @@ struct ScoreShape {
   int queries_per_block;  // queries one block owns
   int keys_per_step;      // keys per LDS tile
   int threads;            // block size
-  size_t scan_lds;        // LDS bytes of the scan (tiles), excluding histograms
+  size_t scan_lds;        // LDS bytes of the fused scan (tiles, per-query state), excluding histograms
   int shared_rows;        // 1: all key splits of a row share one histogram,
                           // threshold and candidate list (the wide scan)
 };

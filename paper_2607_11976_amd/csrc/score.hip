@@ -431,9 +431,25 @@ __device__ __forceinline__ void schedule_half() {
 // compiler cannot tell the histogram from the tile ring): LDS operations of
 // one wave complete in order, so the wave's later histogram reads still see
 // the increment, and no other wave reads this wave's histogram rows.
-__device__ __forceinline__ void lds_inc(uint32_t* p) {
+__device__ __forceinline__ void lds_add(uint32_t* p, uint32_t v) {
   const uint32_t a = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) uint32_t*)p;
-  asm volatile("ds_add_u32 %0, %1" ::"v"(a), "v"(1u) : "memory");
+  asm volatile("ds_add_u32 %0, %1" ::"v"(a), "v"(v) : "memory");
+}
+__device__ __forceinline__ void lds_inc(uint32_t* p) { lds_add(p, 1u); }
+
+// The first 16 bytes of a per-query LDS record and a slot from the query's
+// LDS counter (ds_add_rtn_u32 of 1), issued together under one wait. Opaque
+// for the same reason as lds_inc.
+typedef float f32x4_t __attribute__((ext_vector_type(4)));
+__device__ __forceinline__ uint32_t lds_state_slot(const void* rec, uint32_t* ctr, f32x4_t& f) {
+  const uint32_t a = (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) void*)rec;
+  const uint32_t b = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) uint32_t*)ctr;
+  uint32_t r;
+  asm volatile("ds_read_b128 %0, %2\n\tds_add_rtn_u32 %1, %3, %4\n\ts_waitcnt lgkmcnt(0)"
+               : "=&v"(f), "=&v"(r)
+               : "v"(a), "v"(b), "v"(1u)
+               : "memory");
+  return r;
 }
 
 // Key sources: consecutive positions (kContig, staged through a buffer
@@ -848,10 +864,11 @@ struct FusedSink {
 
 // The fused filter for layouts where a lane holds whole scores of many queries
 // (H <= 4: up to 32 queries per wave, 32 scores per lane per tile, e.g. the
-// one-head inner-product retrieval scorer). The per-query state lives one
-// query per lane (lane q holds query q's range, bin map, threshold, list
-// tail and count above the threshold), read with readlane and written by a
-// lane select, so it costs a handful of registers instead of QW of each.
+// one-head inner-product retrieval scorer). The per-query state (visible
+// range, bin map, threshold, list length, count above the threshold) lives in
+// LDS, one 32-byte record per query plus two counters, so that a lane reaches
+// the state of whichever query its score belongs to with one gather, and list
+// slots and counts are taken with LDS atomics by every passing lane at once.
 // Gate in the score domain: bin(fma(I, delta, c)) >= tau holds for every
 // I >= (tau - c) / delta (real division; fma rounding is monotone and tau is
 // a float), so the lane compares each score with T, that quotient lowered by
@@ -860,26 +877,41 @@ struct FusedSink {
 // edge is written and counted in its true (lower) bin, which changes neither
 // the refresh (it only reads bins above tau) nor the final select (it keeps
 // bins >= the final threshold, whose counts stay complete). Scores that pass
-// the compare are re-checked against the causal end of their row before they
-// are written. NaN passes the compare (as in the bin gate) and is never
-// counted.
+// the compare are re-checked against the visible range of their row before
+// they are written. NaN passes the compare (as in the bin gate) and is never
+// counted. The order of a list's entries depends on the order in which the
+// atomics are served; the final select orders candidates by (score, key)
+// alone, so no result depends on it.
 template <class C>
 struct GroupedSink {
   static_assert(C::GROUPED && C::QW <= kWave, "one query per lane");
-  // lane q: state of query qbase + q
-  float delta_v, c_v, t_v;
-  int tau_v, e_v, s_v;
-  uint32_t tail_v, above_v;
+  // LDS record of one query: the first 16 bytes are what a passing score
+  // needs (bin map and the bin above the threshold), the rest what the
+  // refresh and the range check read
+  struct alignas(16) QState {
+    float delta, c;  // bin-space value x = fma(I, delta, c)
+    float up;        // (float)(tau + 1): x >= up is a count above tau; +inf at the top bin
+    float gate;      // T, the score-domain gate (+inf for rows past the end)
+    int s, e;        // visible keys [s, e) within this split
+    int tau;         // threshold bin, -1 = no gate
+    int pad;
+  };
+  static constexpr int kLdsPerWave = C::QW * (int)sizeof(QState) + 2 * C::QW * 4;
+  QState* qs;         // LDS [QW]
+  uint32_t* tail;     // LDS [QW]: candidates passed (the list length; may exceed cap)
+  uint32_t* above;    // LDS [QW]: counted candidates in bins above tau
   float tq[C::NIH];   // T of the query of item j (items j and j + NIH share it)
   bool ungated;       // some row of the wave has no gate (tau = -1)
+  int vis_s, vis_e;   // every row of the wave sees [vis_s, vis_e)
   uint32_t* hist;     // LDS, [QW][m] for this wave
   int2* cand;
+  int64_t lbase, lstride;  // list of query q: cand + lbase + q * lstride
   int qbase, nq, S, split, cap, m, k;
 
-  // value `val` into lane q of a per-lane register
-  template <typename T>
-  __device__ static T set_lane(T v, int q, T val) {
-    return lane_id() == q ? val : v;
+  __device__ void bind(uint8_t* lds) {
+    qs = reinterpret_cast<QState*>(lds);
+    tail = reinterpret_cast<uint32_t*>(lds + C::QW * sizeof(QState));
+    above = tail + C::QW;
   }
 
   __device__ static float gate_floor(float delta, float c, int tau) {
@@ -889,60 +921,70 @@ struct GroupedSink {
     return i0 - err;
   }
 
-  __device__ void refresh_items() {
-    const int h = lane_id() >> 5;
+  // lane q (< QW): threshold bin t of its query -> the record's derived fields
+  __device__ void set_tau(QState& r, int t) const {
+    r.tau = t;
+    r.up = t < m - 1 ? (float)(t + 1) : __builtin_inff();
+  }
+
+  // the per-item copies of T, and the ungated flag
+  __device__ void update_gates() {
+    const int l = lane_id(), h = l >> 5;
+    __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "wavefront");
     static_for<C::NIH>([&](auto J) {
       constexpr int j = decltype(J)::value;
       constexpr int qa = C::item_q(j, 0), qb = C::item_q(j, 1);
-      const float a = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, t_v), qa));
-      const float b = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, t_v), qb));
-      tq[j] = h ? b : a;
+      tq[j] = qs[h ? qb : qa].gate;
     });
+    const bool valid = l < C::QW && qbase + l < nq;
+    ungated = __ballot(valid && qs[l < C::QW ? l : 0].tau < 0) != 0;
   }
 
   __device__ void init(const ScoreArgs& a, const RowParam* params, int kend) {
     const int l = lane_id(), t = qbase + l;
+    const bool valid = l < C::QW && t < nq;
     RowRange rr{0, 0};
     float dl = 1.0f, c = 0.0f;
     int t0 = -1;
-    if (l < C::QW && t < nq) {
+    if (valid) {
       rr = row_range(a.offs, a.starts, t, a.nk);
       const RowParam p = params[t];
       dl = p.delta;
       c = p.c;
       t0 = p.tau0;
     }
-    e_v = rr.e < kend ? rr.e : kend;
-    s_v = rr.s;
-    delta_v = dl;
-    c_v = c;
-    tau_v = t0;
-    tail_v = 0;
-    above_v = 0;
+    const int e = rr.e < kend ? rr.e : kend;
+    // the wave's common range (empty rows past the end do not narrow it)
+    int cs = valid ? rr.s : 0, ce = valid ? e : INT_MAX;
+#pragma unroll
+    for (int o = 1; o < kWave; o <<= 1) {
+      cs = max(cs, __shfl_xor(cs, o));
+      ce = min(ce, __shfl_xor(ce, o));
+    }
+    vis_s = __builtin_amdgcn_readfirstlane(cs);
+    vis_e = __builtin_amdgcn_readfirstlane(ce);
+    lstride = (int64_t)S * cap;
+    lbase = ((int64_t)qbase * S + split) * cap;
+    if (l < C::QW) {
+      QState r;
+      r.delta = dl;
+      r.c = c;
+      r.s = rr.s;
+      r.e = e;
+      r.pad = 0;
+      set_tau(r, valid ? t0 : m - 1);
+      r.gate = valid ? gate_floor(dl, c, t0) : __builtin_inff();
+      qs[l] = r;
+      tail[l] = 0u;
+      above[l] = 0u;
+    }
     update_gates();
-  }
-
-  // T of every row (+inf for rows past the end: they never pass), the
-  // ungated flag, and the per-item copies
-  __device__ void update_gates() {
-    const int l = lane_id();
-    const bool valid = l < C::QW && qbase + l < nq;
-    t_v = valid ? gate_floor(delta_v, c_v, tau_v) : __builtin_inff();
-    ungated = __ballot(valid && tau_v < 0) != 0;
-    refresh_items();
-  }
-
-  // Query of item it in lane half h, with a run-time item index.
-  __device__ static int item_query(int it, int h) {
-    const int s = it % C::GPQ, g = it / C::GPQ, i = g % 4, mt = (g / 4) % C::MT;
-    return (32 * mt + 8 * i + 4 * h + s * C::H) / C::H;
   }
 
   __device__ void consume(int, int k0, int, const float (&sc)[C::NI], bool live) {
     if (!live) return;
     static_assert(C::NI <= 32, "one bit per item");
     typedef float fNI __attribute__((ext_vector_type(C::NI)));
-    typedef float fNIH __attribute__((ext_vector_type(C::NIH)));
     const int l = lane_id(), h = l >> 5, r32 = l & 31;
     // fast path, vector ALU only (a chain of per-item ballots would stall on
     // every scalar read of a compare result): the largest margin score - T
@@ -955,74 +997,65 @@ struct GroupedSink {
       for (int it = 0; it < C::NI; ++it) mx = fmaxf(mx, sc[it] - tq[it % C::NIH]);
       if (__ballot(mx >= 0.0f) == 0) return;  // wave-uniform: nothing passes
     }
-    // bit it of `items` = some lane's score of item it passed
+    // bit it of `bits`: this lane's score of item it passed the compare
     uint32_t bits = 0;
 #pragma unroll
     for (int it = 0; it < C::NI; ++it) bits |= !(sc[it] < tq[it % C::NIH]) ? (1u << it) : 0u;
     const uint32_t items = wave_or(bits);
     if (items == 0) return;
-    // slow path, one item at a time (a run-time loop keeps the code small)
+    // the tile lies inside the visible range of every row of the wave
+    const bool inside = k0 >= vis_s && k0 + C::KT <= vis_e;
     fNI scv;
-    fNIH tqv;
 #pragma unroll
     for (int it = 0; it < C::NI; ++it) scv[it] = sc[it];
-#pragma unroll
-    for (int j = 0; j < C::NIH; ++j) tqv[j] = tq[j];
+    // one item at a time (a run-time loop keeps the code small); within an
+    // item every passing lane takes its slot and counts at once
     for (uint32_t rem = items; rem; rem &= rem - 1) {
       const int it = __builtin_ctz(rem);
+      if (!((bits >> it) & 1u)) continue;
       const int j = it % C::NIH, nt = it / C::NIH;
-      const int qa = item_query(j, 0), qb = item_query(j, 1);
-      const float s_it = scv[it];
+      const int q = item_query(j, h);
       const int key = k0 + nt * 32 + r32;
-      const int ea = __builtin_amdgcn_readlane(e_v, qa), eb = __builtin_amdgcn_readlane(e_v, qb);
-      const int sa = __builtin_amdgcn_readlane(s_v, qa), sb = __builtin_amdgcn_readlane(s_v, qb);
-      const bool pass = !(s_it < tqv[j]) && key < (h ? eb : ea) && key >= (h ? sb : sa);
-      const uint64_t m2 = __ballot(pass);
-      if (m2 == 0) continue;
-      const uint32_t lo = (uint32_t)__popcll(m2 & 0xFFFFFFFFull), hi = (uint32_t)__popcll(m2) - lo;
-      const uint32_t ta = (uint32_t)__builtin_amdgcn_readlane((int)tail_v, qa);
-      const uint32_t tb = (uint32_t)__builtin_amdgcn_readlane((int)tail_v, qb);
-      const int q = h ? qb : qa;
-      // (readlane takes a wave-uniform lane: read both queries, then select)
-      const float da = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, delta_v), qa));
-      const float db = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, delta_v), qb));
-      const float ca = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, c_v), qa));
-      const float cb = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, c_v), qb));
-      const int ua = __builtin_amdgcn_readlane(tau_v, qa), ub = __builtin_amdgcn_readlane(tau_v, qb);
-      const float x = fmaf(s_it, h ? db : da, h ? cb : ca);
-      if (pass) {
-        const uint32_t pos = h ? tb + mbcnt64(m2) - lo : ta + mbcnt64(m2);
-        if (pos < (uint32_t)cap)
-          cand[((int64_t)(qbase + q) * S + split) * cap + pos] = make_int2(key, __float_as_int(s_it));
-        if (x >= 0.0f) lds_inc(&hist[q * m + min(__float2int_rz(x), m - 1)]);
+      if (!inside) {
+        const QState& r = qs[q];
+        if (key < r.s || key >= r.e) continue;
       }
-      // counted candidates strictly above the query's threshold bin
-      const uint64_t up = __ballot(pass && x >= (float)((h ? ub : ua) + 1));
-      const uint32_t ulo = (uint32_t)__popcll(up & 0xFFFFFFFFull), uhi = (uint32_t)__popcll(up) - ulo;
-      tail_v = set_lane(tail_v, qa, ta + lo);
-      tail_v = set_lane(tail_v, qb, tb + hi);
-      const uint32_t aa = (uint32_t)__builtin_amdgcn_readlane((int)above_v, qa);
-      const uint32_t ab = (uint32_t)__builtin_amdgcn_readlane((int)above_v, qb);
-      above_v = set_lane(above_v, qa, aa + ulo);
-      above_v = set_lane(above_v, qb, ab + uhi);
+      const float s_it = scv[it];
+      f32x4_t f;
+      const uint32_t pos = lds_state_slot(&qs[q], &tail[q], f);
+      const float x = fmaf(s_it, f[0], f[1]);
+      // counted only when x >= 0 (not NaN, not below the range): the add is
+      // issued either way, of 0 for the others, so that no branch is taken
+      const int b = min(max(__float2int_rz(x), 0), m - 1);
+      lds_add(&hist[q * m + b], x >= 0.0f ? 1u : 0u);
+      lds_add(&above[q], x >= f[2] ? 1u : 0u);
+      if (pos < (uint32_t)cap) cand[lbase + q * lstride + pos] = make_int2(key, __float_as_int(s_it));
     }
-    // threshold refresh of every query whose count above tau reached k
-    uint64_t adv = __ballot(l < C::QW && above_v >= (uint32_t)k && tau_v < m - 1);
-    if (adv == 0) return;
+    // threshold refresh: each lane walks its own query's histogram
     __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "wavefront");
-    while (adv) {
-      const int q = __builtin_ctzll(adv);
-      adv &= adv - 1;
-      int t = __builtin_amdgcn_readlane(tau_v, q);
-      uint32_t ab = (uint32_t)__builtin_amdgcn_readlane((int)above_v, q);
+    const bool mine = l < C::QW;
+    const int lq = mine ? l : 0;
+    uint32_t ab = above[lq];
+    int t = qs[lq].tau;
+    const bool adv = mine && ab >= (uint32_t)k && t < m - 1;
+    if (__ballot(adv) == 0) return;
+    if (adv) {
       while (ab >= (uint32_t)k && t < m - 1) {
         ++t;
-        ab -= hist[q * m + t];
+        ab -= hist[lq * m + t];
       }
-      tau_v = set_lane(tau_v, q, t);
-      above_v = set_lane(above_v, q, ab);
+      above[lq] = ab;
+      QState& r = qs[lq];
+      set_tau(r, t);
+      r.gate = gate_floor(r.delta, r.c, t);
     }
     update_gates();
+  }
+
+  // Query of item it in lane half h, with a run-time item index.
+  __device__ static int item_query(int it, int h) {
+    const int s = it % C::GPQ, g = it / C::GPQ, i = g % 4, mt = (g / 4) % C::MT;
+    return (32 * mt + 8 * i + 4 * h + s * C::H) / C::H;
   }
 
   __device__ void finish(uint32_t* cnt, uint32_t* hist_out) {
@@ -1034,7 +1067,7 @@ struct GroupedSink {
       const int64_t u = (int64_t)t * S + split;
       for (int b = l; b < m; b += kWave) hist_out[u * m + b] = hist[q * m + b];
     }
-    if (l < C::QW && qbase + l < nq) cnt[(int64_t)(qbase + l) * S + split] = tail_v;
+    if (l < C::QW && qbase + l < nq) cnt[(int64_t)(qbase + l) * S + split] = tail[l];
   }
 };
 
@@ -1066,12 +1099,20 @@ __global__ __launch_bounds__(C::NTHREADS) void k_dense(ScoreArgs a, float* out, 
   wg_scan<C>(a, SrcContig{}, kb, ke, lds, wq, sink);
 }
 
+// LDS of the fused scan besides the tile ring and the histograms: the
+// per-query records of the grouped filter
+template <class C>
+constexpr int fused_sink_lds() {
+  if constexpr (C::GROUPED) return C::WAVES * GroupedSink<C>::kLdsPerWave;
+  else return 0;
+}
+
 template <class C>
 __global__ __launch_bounds__(C::NTHREADS) void k_fused(ScoreArgs a, const RowParam* params, int S, int L, int cap,
                                                        int m, int k, uint32_t* cnt,
                                                        uint32_t* hist_out, int2* cand) {
   extern __shared__ __align__(16) uint8_t lds[];
-  uint32_t* hist = reinterpret_cast<uint32_t*>(lds + C::SCAN_LDS);
+  uint32_t* hist = reinterpret_cast<uint32_t*>(lds + C::SCAN_LDS + fused_sink_lds<C>());
   int* emax = reinterpret_cast<int*>(hist + C::QT * m);
   int* smin = emax + 1;
   const int tile = blockIdx.x / S, split = blockIdx.x - tile * S;
@@ -1098,6 +1139,7 @@ __global__ __launch_bounds__(C::NTHREADS) void k_fused(ScoreArgs a, const RowPar
   load_q<C>(wq, a, qbase);
   std::conditional_t<C::GROUPED, GroupedSink<C>, FusedSink<C>> sink;
   sink.hist = hist + wave * C::QW * m;
+  if constexpr (C::GROUPED) sink.bind(lds + C::SCAN_LDS + wave * GroupedSink<C>::kLdsPerWave);
   sink.cand = cand;
   sink.qbase = qbase;
   sink.nq = a.nq;
@@ -1169,7 +1211,7 @@ ScoreShape score_shape(int dtype, int mode, int h, int d) {
     s.queries_per_block = C::QT;
     s.keys_per_step = C::KT;
     s.threads = C::NTHREADS;
-    s.scan_lds = C::SCAN_LDS;
+    s.scan_lds = C::SCAN_LDS + fused_sink_lds<C>();
   });
   return found ? s : wide_shape(dtype, mode, h, d);
 }
@@ -1228,7 +1270,7 @@ hipError_t launch_fused_scan(const ScoreArgs& a, const RowParam* params, int S, 
       err = hipSuccess;
       return;
     }
-    const size_t lds = C::SCAN_LDS + (size_t)C::QT * m * 4 + 16;
+    const size_t lds = C::SCAN_LDS + fused_sink_lds<C>() + (size_t)C::QT * m * 4 + 16;
     if (lds > 65536)
       (void)hipFuncSetAttribute((const void*)k_fused<C>, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
     hipLaunchKernelGGL(k_fused<C>, dim3(tiles * S), dim3(C::NTHREADS), lds, st, a, params, S, L, cap, m, k,
