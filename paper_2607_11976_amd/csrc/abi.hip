@@ -58,7 +58,7 @@ Layout carve(int nq, int nk, const Resolved& r, bool fused) {
   L.cnt = take((size_t)nq * r.S * 4);
   L.hist = take((size_t)nq * r.HS * r.m * 4);
   L.cand = take((size_t)nq * r.S * r.cap * 8);
-  L.gate = r.shared ? take((size_t)nq * 4) : 0;
+  L.gate = fused ? take((size_t)nq * 8) : 0;  // published bins: [nq] ints (wide), [nq][8] bytes
   L.scratch = fused ? take((size_t)kFallbackGridFused * nk * 4) : 0;
   L.total = off;
   return L;
@@ -279,7 +279,7 @@ int lt_indexer_topk(const void* q, const float* q_scale, const float* w, const v
     return hip_status(e);
   record(r, LT_STAGE_FILTER, st);
   e = r.shared ? launch_wide_fused(a, params, r.S, r.L, r.cap, r.m, k, gate, cnt, hist, cand, st)
-               : launch_fused_scan(a, params, r.S, r.L, r.cap, r.m, k, cnt, hist, cand, st);
+               : launch_fused_scan(a, params, r.S, r.L, r.cap, r.m, k, gate, cnt, hist, cand, st);
   if (e != hipSuccess) return hip_status(e);
   record(r, LT_STAGE_SELECT, st);
   if ((e = launch_select(params, cnt, hist, cand, nq, r.S, r.HS, r.cap, r.m, k, r.E,

@@ -76,9 +76,11 @@ ScoreShape score_shape(int dtype, int mode, int h, int d);
 hipError_t launch_sample_scores(const ScoreArgs& a, const int32_t* list, int ns, float* samp, hipStream_t st);
 // Dense scores: out[t * ld + s] = I(t, s) for every key.
 hipError_t launch_dense_scores(const ScoreArgs& a, float* out, int64_t ld, hipStream_t st);
-// Fused score + gate + write-back scan over S key splits of L keys each.
+// Fused score + gate + write-back scan over S key splits of L keys each;
+// pub [nq * 8 bytes] holds the bins the splits of each row publish where they
+// share thresholds (initialised here).
 hipError_t launch_fused_scan(const ScoreArgs& a, const RowParam* params, int S, int L, int cap, int m,
-                             int k, uint32_t* cnt, uint32_t* hist, int2* cand, hipStream_t st);
+                             int k, int* pub, uint32_t* cnt, uint32_t* hist, int2* cand, hipStream_t st);
 // Exact fallback for queued rows: dense re-score into scratch [grid, nk], then radix select.
 hipError_t launch_fused_fallback(const ScoreArgs& a, int k, uint32_t flags, const uint32_t* qctl,
                                  const int32_t* queue, float* scratch, int grid, int32_t* out_i,

@@ -437,6 +437,15 @@ __device__ __forceinline__ void lds_add(uint32_t* p, uint32_t v) {
 }
 __device__ __forceinline__ void lds_inc(uint32_t* p) { lds_add(p, 1u); }
 
+// The lane index, computed where it is used: paths taken on few tiles derive
+// their per-lane addresses from it instead of keeping them live across the
+// scan.
+__device__ __forceinline__ int lane_here() {
+  int l;
+  asm volatile("v_mbcnt_lo_u32_b32 %0, -1, 0\n\tv_mbcnt_hi_u32_b32 %0, -1, %0" : "=v"(l));
+  return l;
+}
+
 // The first 16 bytes of a per-query LDS record and a slot from the query's
 // LDS counter (ds_add_rtn_u32 of 1), issued together under one wait. Opaque
 // for the same reason as lds_inc.
@@ -450,6 +459,37 @@ __device__ __forceinline__ uint32_t lds_state_slot(const void* rec, uint32_t* ct
                : "v"(a), "v"(b), "v"(1u)
                : "memory");
   return r;
+}
+
+// A slot from an LDS counter (ds_add_rtn_u32 of 1, the old value), an
+// 8-byte LDS write, an 8-byte LDS read and a 32-byte per-query record read
+// (as two 16-byte halves). Opaque for the same reason as lds_inc; the reads
+// wait for their data.
+__device__ __forceinline__ uint32_t lds_slot(uint32_t* ctr) {
+  const uint32_t b = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) uint32_t*)ctr;
+  uint32_t r;
+  asm volatile("ds_add_rtn_u32 %0, %1, %2\n\ts_waitcnt lgkmcnt(0)" : "=v"(r) : "v"(b), "v"(1u) : "memory");
+  return r;
+}
+typedef uint32_t u32x2_t __attribute__((ext_vector_type(2)));
+__device__ __forceinline__ void lds_put2(uint32_t* p, uint32_t x, uint32_t y) {
+  const uint32_t a = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) uint32_t*)p;
+  const u32x2_t v = {x, y};
+  asm volatile("ds_write_b64 %0, %1" ::"v"(a), "v"(v) : "memory");
+}
+__device__ __forceinline__ void lds_get2(const uint32_t* p, uint32_t (&out)[2]) {
+  const uint32_t a = (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) uint32_t*)p;
+  u32x2_t v;
+  asm volatile("ds_read_b64 %0, %1\n\ts_waitcnt lgkmcnt(0)" : "=v"(v) : "v"(a) : "memory");
+  out[0] = v[0];
+  out[1] = v[1];
+}
+__device__ __forceinline__ void lds_get_rec(const void* rec, f32x4_t& f, i32x4_t& g) {
+  const uint32_t a = (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) void*)rec;
+  asm volatile("ds_read_b128 %0, %2\n\tds_read_b128 %1, %2 offset:16\n\ts_waitcnt lgkmcnt(0)"
+               : "=&v"(f), "=&v"(g)
+               : "v"(a)
+               : "memory");
 }
 
 // Key sources: consecutive positions (kContig, staged through a buffer
@@ -645,6 +685,9 @@ __device__ __forceinline__ void wg_scan(const ScoreArgs& a, const Src& src, int 
   auto body = [&](auto SLOT_, int st) {
     constexpr int SLOT = decltype(SLOT_)::value;
     bl.opaque();
+    // the sink's loads for this step go ahead of the tile loads, so that the
+    // step's tile wait covers them
+    if constexpr (requires { sink.pre(); }) sink.pre();
     // slot of tile st-1 is free: every wave passed the barrier after reading it
     stage((SLOT + 3) & 3, st + 3, kbeg + (st + 3) * C::KT);
     // half step A: MFMA sub-tile 0 of tile st || epilogue of sub-tile 1 of st-1,
@@ -865,10 +908,11 @@ struct FusedSink {
 // The fused filter for layouts where a lane holds whole scores of many queries
 // (H <= 4: up to 32 queries per wave, 32 scores per lane per tile, e.g. the
 // one-head inner-product retrieval scorer). The per-query state (visible
-// range, bin map, threshold, list length, count above the threshold) lives in
-// LDS, one 32-byte record per query plus two counters, so that a lane reaches
-// the state of whichever query its score belongs to with one gather, and list
-// slots and counts are taken with LDS atomics by every passing lane at once.
+// range, bin map, thresholds, list length, counts above the thresholds) lives
+// in LDS, one 32-byte record per query plus three counters, so that a lane
+// reaches the state of whichever query its score belongs to with one gather,
+// and list slots and counts are taken with LDS atomics by every passing lane
+// at once.
 // Gate in the score domain: bin(fma(I, delta, c)) >= tau holds for every
 // I >= (tau - c) / delta (real division; fma rounding is monotone and tau is
 // a float), so the lane compares each score with T, that quotient lowered by
@@ -882,27 +926,60 @@ struct FusedSink {
 // counted. The order of a list's entries depends on the order in which the
 // atomics are served; the final select orders candidates by (score, key)
 // alone, so no result depends on it.
+// Passing scores are not written out in the tile that finds them: each wave
+// appends them to its LDS queue (a ballot and one LDS write per item, no
+// round trip), and every kDrainEvery tiles all waves drain their queues at
+// once, one entry per lane, re-checking each against the row's current gate.
+// Handled where found, the per-item work of one wave held up the other waves
+// of its block at the tile barrier on most tiles; drained together, no wave
+// waits for another, and the counting's LDS round trips serve 64 entries at a
+// time. The thresholds then move up to kDrainEvery tiles later, which only
+// lets a few more keys through. A tile with more passing scores than the
+// queue holds (a row without a gate) is handled in place.
+// Key splits of one row share a threshold (S > 1). Besides its own bin tau
+// (the largest bin with at least k of the split's candidates at or above
+// it), each split tracks tau_s, the same walk for ks = ceil(k / S), and
+// publishes it in its byte of the row's entry in `pub`. The smallest bin g
+// the S splits of a row have published has at least ks candidates of every
+// split at or above it, S * ks >= k keys of the row in all, so g never
+// exceeds the row's final threshold bin over all splits; every split raises
+// its own bin to g. (Sharing the largest own bin instead would keep each
+// split at its own top k; the smallest of the ks walks follows the top k of
+// all splits together.) A raised gate drops only keys below the final bin,
+// and the counts at and above that bin stay complete in every histogram.
 template <class C>
 struct GroupedSink {
   static_assert(C::GROUPED && C::QW <= kWave, "one query per lane");
   // LDS record of one query: the first 16 bytes are what a passing score
-  // needs (bin map and the bin above the threshold), the rest what the
-  // refresh and the range check read
+  // needs (bin map and the bins above the two thresholds), the rest what the
+  // threshold updates and the range check read
   struct alignas(16) QState {
     float delta, c;  // bin-space value x = fma(I, delta, c)
     float up;        // (float)(tau + 1): x >= up is a count above tau; +inf at the top bin
+    float ups;       // the same for tau_s
     float gate;      // T, the score-domain gate (+inf for rows past the end)
     int s, e;        // visible keys [s, e) within this split
-    int tau;         // threshold bin, -1 = no gate
     int pad;
   };
-  static constexpr int kLdsPerWave = C::QW * (int)sizeof(QState) + 2 * C::QW * 4;
+  static constexpr int kQueue = 128;      // entries of a wave's queue of passing scores
+  static constexpr int kDrainEvery = 16;  // tiles between queue drains
+  static constexpr int kShareEvery = 2;   // tiles between reads of the published bins
+  static constexpr int kLdsPerWave = C::QW * (int)sizeof(QState) + 3 * C::QW * 4 + kQueue * 8;
   QState* qs;         // LDS [QW]
   uint32_t* tail;     // LDS [QW]: candidates passed (the list length; may exceed cap)
   uint32_t* above;    // LDS [QW]: counted candidates in bins above tau
+  uint32_t* above_s;  // LDS [QW]: the same above tau_s
+  uint32_t* queue;    // LDS [kQueue][2]: (score bits, (key - kq0) << 8 | query)
+  int qlen;           // entries in the queue
+  int kq0;            // first key of the split
+  bool use_queue;     // keys of the split are told apart by 24 bits
   float tq[C::NIH];   // T of the query of item j (items j and j + NIH share it)
   bool ungated;       // some row of the wave has no gate (tau = -1)
   int vis_s, vis_e;   // every row of the wave sees [vis_s, vis_e)
+  uint8_t* pub;       // [nq][8] published bins + 1 of the row's splits (S > 1), or NULL
+  int tau_v, taus_v;  // lane q: tau and tau_s of query qbase + q
+  uint64_t gw;        // lane q: its row's published bytes, as read
+  int ks, steps, ntile;
   uint32_t* hist;     // LDS, [QW][m] for this wave
   int2* cand;
   int64_t lbase, lstride;  // list of query q: cand + lbase + q * lstride
@@ -912,6 +989,8 @@ struct GroupedSink {
     qs = reinterpret_cast<QState*>(lds);
     tail = reinterpret_cast<uint32_t*>(lds + C::QW * sizeof(QState));
     above = tail + C::QW;
+    above_s = above + C::QW;
+    queue = above_s + C::QW;
   }
 
   __device__ static float gate_floor(float delta, float c, int tau) {
@@ -921,23 +1000,21 @@ struct GroupedSink {
     return i0 - err;
   }
 
-  // lane q (< QW): threshold bin t of its query -> the record's derived fields
-  __device__ void set_tau(QState& r, int t) const {
-    r.tau = t;
-    r.up = t < m - 1 ? (float)(t + 1) : __builtin_inff();
-  }
+  __device__ float up_of(int t) const { return t < m - 1 ? (float)(t + 1) : __builtin_inff(); }
 
-  // the per-item copies of T, and the ungated flag
+  // the per-item copies of T, and the ungated flag (the query of item j in
+  // lane half h is item_q(j, 0) + h * 4 / H)
   __device__ void update_gates() {
-    const int l = lane_id(), h = l >> 5;
+    const int l = lane_here();
     __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "wavefront");
+    const QState* qh = qs + (l >> 5) * (4 / C::H);
     static_for<C::NIH>([&](auto J) {
       constexpr int j = decltype(J)::value;
-      constexpr int qa = C::item_q(j, 0), qb = C::item_q(j, 1);
-      tq[j] = qs[h ? qb : qa].gate;
+      static_assert(C::item_q(j, 1) - C::item_q(j, 0) == 4 / C::H, "query of an item in the upper half");
+      tq[j] = qh[C::item_q(j, 0)].gate;
     });
     const bool valid = l < C::QW && qbase + l < nq;
-    ungated = __ballot(valid && qs[l < C::QW ? l : 0].tau < 0) != 0;
+    ungated = __ballot(valid && tau_v < 0) != 0;
   }
 
   __device__ void init(const ScoreArgs& a, const RowParam* params, int kend) {
@@ -965,20 +1042,50 @@ struct GroupedSink {
     vis_e = __builtin_amdgcn_readfirstlane(ce);
     lstride = (int64_t)S * cap;
     lbase = ((int64_t)qbase * S + split) * cap;
+    ks = (k + S - 1) / S;
+    steps = 0;
+    ntile = 0;
+    qlen = 0;
+    use_queue = kend - kq0 < (1 << 24);
+    tau_v = valid ? t0 : m - 1;
+    taus_v = tau_v;
+    gw = 0;
     if (l < C::QW) {
       QState r;
       r.delta = dl;
       r.c = c;
+      r.up = up_of(tau_v);
+      r.ups = r.up;
+      r.gate = valid ? gate_floor(dl, c, t0) : __builtin_inff();
       r.s = rr.s;
       r.e = e;
       r.pad = 0;
-      set_tau(r, valid ? t0 : m - 1);
-      r.gate = valid ? gate_floor(dl, c, t0) : __builtin_inff();
       qs[l] = r;
       tail[l] = 0u;
       above[l] = 0u;
+      above_s[l] = 0u;
     }
     update_gates();
+  }
+
+  // every kShareEvery steps: read the rows' published bins (lands by the
+  // step's tile wait)
+  __device__ void pre() {
+    if (!pub) return;
+    if (steps++ % kShareEvery != 0) return;
+    const int l = lane_id();
+    if (l < C::QW && qbase + l < nq)
+      gw = __hip_atomic_load(reinterpret_cast<uint64_t*>(pub) + qbase + l, __ATOMIC_RELAXED,
+                             __HIP_MEMORY_SCOPE_AGENT);
+  }
+
+  // lane lq: its query's bin moves to t (above already adjusted)
+  __device__ void move_tau(int lq, int t, uint32_t ab) {
+    above[lq] = ab;
+    QState& r = qs[lq];
+    r.up = up_of(t);
+    r.gate = gate_floor(r.delta, r.c, t);
+    tau_v = t;
   }
 
   __device__ void consume(int, int k0, int, const float (&sc)[C::NI], bool live) {
@@ -986,6 +1093,28 @@ struct GroupedSink {
     static_assert(C::NI <= 32, "one bit per item");
     typedef float fNI __attribute__((ext_vector_type(C::NI)));
     const int l = lane_id(), h = l >> 5, r32 = l & 31;
+    // raise each row's bin to the smallest bin its splits have published
+    if (pub && (steps - 1) % kShareEvery == 0) {
+      int g = 255;
+      for (int j = 0; j < S; ++j) g = min(g, (int)((gw >> (8 * j)) & 0xFFu));
+      g -= 1;
+      const bool raise = l < C::QW && qbase + l < nq && g > tau_v;
+      if (__ballot(raise) != 0) {
+        __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "wavefront");
+        if (raise) {
+          const int lq = lane_here();
+          uint32_t ab = above[lq];
+          for (int t = tau_v + 1; t <= g; ++t) ab -= hist[lq * m + t];
+          move_tau(lq, g, ab);
+        }
+        update_gates();
+      }
+    }
+    // the periodic drain, at the same tile in every wave
+    if (use_queue && ++ntile % kDrainEvery == 0 && qlen != 0) {
+      drain();
+      refresh();
+    }
     // fast path, vector ALU only (a chain of per-item ballots would stall on
     // every scalar read of a compare result): the largest margin score - T
     // over the lane's items; T - T' < 0 for every non-NaN score below its T.
@@ -1003,13 +1132,36 @@ struct GroupedSink {
     for (int it = 0; it < C::NI; ++it) bits |= !(sc[it] < tq[it % C::NIH]) ? (1u << it) : 0u;
     const uint32_t items = wave_or(bits);
     if (items == 0) return;
-    // the tile lies inside the visible range of every row of the wave
-    const bool inside = k0 >= vis_s && k0 + C::KT <= vis_e;
     fNI scv;
 #pragma unroll
     for (int it = 0; it < C::NI; ++it) scv[it] = sc[it];
-    // one item at a time (a run-time loop keeps the code small); within an
-    // item every passing lane takes its slot and counts at once
+    if (use_queue) {
+      const int n = __builtin_amdgcn_readlane((int)wave_prefix_sum((uint32_t)__builtin_popcount(bits)), kWave - 1);
+      if (qlen + n > kQueue) {
+        drain();
+        refresh();
+      }
+      if (n <= kQueue) {
+        // append: one ballot and one LDS write per item
+        const uint32_t hq = (uint32_t)(h * (4 / C::H));
+        for (uint32_t rem = items; rem; rem &= rem - 1) {
+          const int it = __builtin_ctz(rem);
+          const bool pass = (bits >> it) & 1u;
+          const uint64_t mask = __ballot(pass);
+          if (pass) {
+            const int j = it % C::NIH, nt = it / C::NIH;
+            const uint32_t q = (uint32_t)item_query(j, 0) + hq;
+            const uint32_t rel = (uint32_t)(k0 - kq0 + nt * 32 + r32);
+            lds_put2(queue + 2 * (qlen + (int)mbcnt64(mask)), __float_as_uint(scv[it]), rel << 8 | q);
+          }
+          qlen += __popcll(mask);
+        }
+        return;
+      }
+    }
+    // in place, one item at a time: every passing lane takes its slot and
+    // counts at once
+    const bool inside = k0 >= vis_s && k0 + C::KT <= vis_e;
     for (uint32_t rem = items; rem; rem &= rem - 1) {
       const int it = __builtin_ctz(rem);
       if (!((bits >> it) & 1u)) continue;
@@ -1023,31 +1175,82 @@ struct GroupedSink {
       const float s_it = scv[it];
       f32x4_t f;
       const uint32_t pos = lds_state_slot(&qs[q], &tail[q], f);
-      const float x = fmaf(s_it, f[0], f[1]);
-      // counted only when x >= 0 (not NaN, not below the range): the add is
-      // issued either way, of 0 for the others, so that no branch is taken
-      const int b = min(max(__float2int_rz(x), 0), m - 1);
-      lds_add(&hist[q * m + b], x >= 0.0f ? 1u : 0u);
-      lds_add(&above[q], x >= f[2] ? 1u : 0u);
+      count(q, s_it, f);
       if (pos < (uint32_t)cap) cand[lbase + q * lstride + pos] = make_int2(key, __float_as_int(s_it));
     }
-    // threshold refresh: each lane walks its own query's histogram
+    refresh();
+  }
+
+  // counts of a written candidate of query q: its bin, and above tau / tau_s
+  // (only when x >= 0: not NaN, not below the range; the adds are issued
+  // either way, of 0 for the others, so that no branch is taken)
+  __device__ void count(int q, float s, const f32x4_t& f) {
+    const float x = fmaf(s, f[0], f[1]);
+    const int b = min(max(__float2int_rz(x), 0), m - 1);
+    lds_add(&hist[q * m + b], x >= 0.0f ? 1u : 0u);
+    lds_add(&above[q], x >= f[2] ? 1u : 0u);
+    lds_add(&above_s[q], x >= f[3] ? 1u : 0u);
+  }
+
+  // the queue, one entry per lane: entries still at or above their row's
+  // gate and inside its visible range take a slot, are written and counted
+  __device__ void drain() {
+    const int l = lane_here();
+    for (int b0 = 0; b0 < qlen; b0 += kWave) {
+      const int i = b0 + l;
+      if (i < qlen) {
+        uint32_t ent[2];
+        lds_get2(queue + 2 * i, ent);
+        const float s = __uint_as_float(ent[0]);
+        const int q = (int)(ent[1] & 0xFFu), key = kq0 + (int)(ent[1] >> 8);
+        f32x4_t f;
+        i32x4_t g;
+        lds_get_rec(&qs[q], f, g);  // g: gate bits, s, e
+        if (!(s < __int_as_float(g[0])) && key >= g[1] && key < g[2]) {
+          const uint32_t pos = lds_slot(&tail[q]);
+          count(q, s, f);
+          if (pos < (uint32_t)cap) cand[lbase + q * lstride + pos] = make_int2(key, __float_as_int(s));
+        }
+      }
+    }
+    qlen = 0;
+  }
+
+  // threshold refresh: each lane walks its own query's histogram, for tau
+  // (k) and, where the splits share, for tau_s (ks)
+  __device__ void refresh() {
+    const int l = lane_id();
     __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "wavefront");
     const bool mine = l < C::QW;
-    const int lq = mine ? l : 0;
-    uint32_t ab = above[lq];
-    int t = qs[lq].tau;
-    const bool adv = mine && ab >= (uint32_t)k && t < m - 1;
-    if (__ballot(adv) == 0) return;
-    if (adv) {
-      while (ab >= (uint32_t)k && t < m - 1) {
-        ++t;
-        ab -= hist[lq * m + t];
+    const uint32_t ab0 = above[mine ? l : 0];
+    const uint32_t as0 = pub ? above_s[mine ? l : 0] : 0u;
+    const bool adv = mine && ab0 >= (uint32_t)k && tau_v < m - 1;
+    const bool advs = mine && as0 >= (uint32_t)ks && taus_v < m - 1;
+    if (__ballot(adv || advs) == 0) return;
+    if (adv || advs) {
+      const int lq = lane_here();
+      if (adv) {
+        uint32_t ab = ab0;
+        int t = tau_v;
+        while (ab >= (uint32_t)k && t < m - 1) {
+          ++t;
+          ab -= hist[lq * m + t];
+        }
+        move_tau(lq, t, ab);
       }
-      above[lq] = ab;
-      QState& r = qs[lq];
-      set_tau(r, t);
-      r.gate = gate_floor(r.delta, r.c, t);
+      if (advs) {
+        uint32_t ab = as0;
+        int t = taus_v;
+        while (ab >= (uint32_t)ks && t < m - 1) {
+          ++t;
+          ab -= hist[lq * m + t];
+        }
+        above_s[lq] = ab;
+        qs[lq].ups = up_of(t);
+        taus_v = t;
+        __hip_atomic_store(pub + (int64_t)(qbase + lq) * 8 + split, (uint8_t)(t + 1), __ATOMIC_RELAXED,
+                           __HIP_MEMORY_SCOPE_AGENT);
+      }
     }
     update_gates();
   }
@@ -1059,6 +1262,7 @@ struct GroupedSink {
   }
 
   __device__ void finish(uint32_t* cnt, uint32_t* hist_out) {
+    if (qlen != 0) drain();
     __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "wavefront");
     const int l = lane_id();
     for (int q = 0; q < C::QW; ++q) {
@@ -1109,7 +1313,7 @@ constexpr int fused_sink_lds() {
 
 template <class C>
 __global__ __launch_bounds__(C::NTHREADS) void k_fused(ScoreArgs a, const RowParam* params, int S, int L, int cap,
-                                                       int m, int k, uint32_t* cnt,
+                                                       int m, int k, uint8_t* pub, uint32_t* cnt,
                                                        uint32_t* hist_out, int2* cand) {
   extern __shared__ __align__(16) uint8_t lds[];
   uint32_t* hist = reinterpret_cast<uint32_t*>(lds + C::SCAN_LDS + fused_sink_lds<C>());
@@ -1139,7 +1343,13 @@ __global__ __launch_bounds__(C::NTHREADS) void k_fused(ScoreArgs a, const RowPar
   load_q<C>(wq, a, qbase);
   std::conditional_t<C::GROUPED, GroupedSink<C>, FusedSink<C>> sink;
   sink.hist = hist + wave * C::QW * m;
-  if constexpr (C::GROUPED) sink.bind(lds + C::SCAN_LDS + wave * GroupedSink<C>::kLdsPerWave);
+  if constexpr (C::GROUPED) {
+    sink.bind(lds + C::SCAN_LDS + wave * GroupedSink<C>::kLdsPerWave);
+    sink.kq0 = kb;
+    // splits share thresholds through one byte per (row, split): up to 8
+    // splits, bins + 1 below 256
+    sink.pub = S > 1 && S <= 8 && m <= 255 ? pub : nullptr;
+  }
   sink.cand = cand;
   sink.qbase = qbase;
   sink.nq = a.nq;
@@ -1261,8 +1471,14 @@ hipError_t launch_dense_scores(const ScoreArgs& a, float* out, int64_t ld, hipSt
   return err;
 }
 
+// Published bins of the rows' splits start at the sample's (stored + 1).
+__global__ void k_pub_init(const RowParam* params, int nq, uint64_t* pub) {
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < nq; i += (int64_t)gridDim.x * blockDim.x)
+    pub[i] = 0x0101010101010101ull * (uint64_t)(uint8_t)(params[i].tau0 + 1);
+}
+
 hipError_t launch_fused_scan(const ScoreArgs& a, const RowParam* params, int S, int L, int cap, int m, int k,
-                             uint32_t* cnt, uint32_t* hist, int2* cand, hipStream_t st) {
+                             int* pub, uint32_t* cnt, uint32_t* hist, int2* cand, hipStream_t st) {
   hipError_t err = hipErrorInvalidValue;
   with_cfg(a.dtype, a.mode, a.h, a.d, [&]<class C>() {
     const int tiles = (a.nq + C::QT - 1) / C::QT;
@@ -1270,11 +1486,16 @@ hipError_t launch_fused_scan(const ScoreArgs& a, const RowParam* params, int S, 
       err = hipSuccess;
       return;
     }
+    if (C::GROUPED && S > 1 && S <= 8 && m <= 255) {
+      hipLaunchKernelGGL(k_pub_init, dim3((a.nq + 255) / 256), dim3(256), 0, st, params, a.nq,
+                         reinterpret_cast<uint64_t*>(pub));
+      if ((err = hipGetLastError()) != hipSuccess) return;
+    }
     const size_t lds = C::SCAN_LDS + fused_sink_lds<C>() + (size_t)C::QT * m * 4 + 16;
     if (lds > 65536)
       (void)hipFuncSetAttribute((const void*)k_fused<C>, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
     hipLaunchKernelGGL(k_fused<C>, dim3(tiles * S), dim3(C::NTHREADS), lds, st, a, params, S, L, cap, m, k,
-                       cnt, hist, cand);
+                       reinterpret_cast<uint8_t*>(pub), cnt, hist, cand);
     err = hipGetLastError();
   });
   return err;
