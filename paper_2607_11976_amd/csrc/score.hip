@@ -492,6 +492,14 @@ __device__ __forceinline__ void lds_get_rec(const void* rec, f32x4_t& f, i32x4_t
                : "memory");
 }
 
+// (v << 1) | !(a < b): the compare writes VCC, the add with carry doubles v
+// and adds the carry.
+__device__ __forceinline__ uint32_t shift_in_nlt(uint32_t v, float a, float b) {
+  uint32_t r;
+  asm("v_cmp_nlt_f32 vcc, %1, %2\n\tv_addc_co_u32 %0, vcc, %3, %3, vcc" : "=v"(r) : "v"(a), "v"(b), "v"(v) : "vcc");
+  return r;
+}
+
 // Key sources: consecutive positions (kContig, staged through a buffer
 // descriptor per tile) or a list of key indices (gathered per row).
 struct SrcContig {
@@ -1120,16 +1128,18 @@ struct GroupedSink {
     // over the lane's items; T - T' < 0 for every non-NaN score below its T.
     // A NaN score only matters to an ungated row, and then the fast path is
     // skipped.
+    static_assert(C::NI == 2 * C::NIH, "items j and j + NIH share their query");
     if (!ungated) {
       float mx = -__builtin_inff();
 #pragma unroll
-      for (int it = 0; it < C::NI; ++it) mx = fmaxf(mx, sc[it] - tq[it % C::NIH]);
+      for (int j = 0; j < C::NIH; ++j) mx = fmaxf(mx, fmaxf(sc[j], sc[j + C::NIH]) - tq[j]);
       if (__ballot(mx >= 0.0f) == 0) return;  // wave-uniform: nothing passes
     }
     // bit it of `bits`: this lane's score of item it passed the compare
+    // (built from the top item down: a compare and a shift-add of its result)
     uint32_t bits = 0;
 #pragma unroll
-    for (int it = 0; it < C::NI; ++it) bits |= !(sc[it] < tq[it % C::NIH]) ? (1u << it) : 0u;
+    for (int it = C::NI - 1; it >= 0; --it) bits = shift_in_nlt(bits, sc[it], tq[it % C::NIH]);
     const uint32_t items = wave_or(bits);
     if (items == 0) return;
     fNI scv;
