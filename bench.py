@@ -20,6 +20,10 @@ fallback, inputs resident in HBM. Prints ONE JSON line with
                  chunked-prefill protocol), with a random sample per chunk and
                  with the sample taken from the previous chunk's top-k
                  (sec. 3.2 "Sampling"), total time over all chunks.
+  other_configs  the remaining synthetic workloads, one short measurement
+                 each: the 64 x 4096 fp32 case, the 10000 x 4M one-head
+                 inner-product retrieval (k = 100) and the 1024 x 256K
+                 adversarial DSA case (outliers and duplicate keys, k = 2048).
   retrieval_e7   the retrieval sweep of sec. 4.1 ("Large-Scale Retrieval
                  Benchmark"): 64 queries x corpora of 1M, 2M, 4M, 5M passages
                  of 768-dimensional bf16 embeddings, k = 128, 1024, 4096,
@@ -95,10 +99,11 @@ def measure(name: str, steps: int, warmup: int, unfused: bool, cold: int = 5):
     cfg = workloads.CONFIGS[name]
     x = workloads.generate(cfg, seed=workloads.CONFIG_SEEDS[name])
     dev = torch.device("cuda")
-    q, w, keys = x["q"].to(dev), x["w"].to(dev), x["keys"].to(dev)
+    q, keys = x["q"].to(dev), x["keys"].to(dev)
+    w = None if x["w"] is None else x["w"].to(dev)
     qs = None if x["q_scale"] is None else x["q_scale"].to(dev)
     ks = None if x["k_scale"] is None else x["k_scale"].to(dev)
-    offs = x["offsets"].to(dev)
+    offs = None if x["offsets"] is None else x["offsets"].to(dev)
     del x
     nq, nk, k = cfg.nq, cfg.nk, cfg.k
     pairs = visible_pairs(cfg)
@@ -329,6 +334,23 @@ def roofline(cfg, res):
             "kernel_ms": round(filt_ms, 4), "algorithmic_flops": flops}
 
 
+def other_config(name: str, unfused: bool):
+    """One short measurement of a workload besides the headline ones (the
+    unfused baseline only where its dense score matrix fits: not for the 4M
+    retrieval, whose matrix would take 160 GB)."""
+    cfg, res = measure(name, 5, 2, unfused, cold=2)
+    out = {"workload": name, "dtype": cfg.dtype, "mode": cfg.mode, "num_queries": cfg.nq, "num_keys": cfg.nk,
+           "heads": cfg.h, "head_dim": cfg.d, "k": cfg.k, "ms_per_step": round(res["ms"], 4),
+           "value": res["pairs"] / (res["ms"] * 1e-3), "unit": "pairs/s", "visible_pairs": res["pairs"],
+           "roofline": roofline(cfg, res), "stages_ms": {k: round(v, 4) for k, v in res["stages"].items()},
+           "survivors_per_row_mean": round(res["survivors_mean"], 1), "fallback_rows": res["fallback_rows"]}
+    if "unfused_ms" in res:
+        out["unfused_ms_per_step"] = round(res["unfused_ms"], 4)
+        out["unfused_same_sets"] = res["unfused_same_sets"]
+    print("[bench] %s: %.3f ms/step" % (name, res["ms"]), file=sys.stderr, flush=True)
+    return out
+
+
 def cpu_oracle_rate(name: str, budget_s: float):
     from oracle import litetopk_oracle as orc
     try:
@@ -382,6 +404,7 @@ def main():
     ap.add_argument("--no-unfused", action="store_true", help="skip the unfused baseline")
     ap.add_argument("--no-chunked", action="store_true", help="skip the chunked-prefill measurement")
     ap.add_argument("--no-retrieval", action="store_true", help="skip the 768-d retrieval sweep")
+    ap.add_argument("--no-others", action="store_true", help="skip the other synthetic workloads")
     ap.add_argument("--retrieval-only", action="store_true", help="run only the 768-d retrieval sweep")
     ap.add_argument("--cpu-budget", type=float, default=15.0)
     ap.add_argument("--profile-only", default=None, metavar="WORKLOAD",
@@ -473,6 +496,11 @@ def main():
             m["unfused_ms_per_step"] = round(res2["unfused_ms"], 4)
             m["unfused_same_sets"] = res2["unfused_same_sets"]
         line["ctx_1m"] = m
+    if not args.no_others:
+        line["other_configs"] = [other_config(n, unf and not args.no_unfused)
+                                 for n, unf in (("tiny_fp32", True), ("retrieval_bf16_4m", False),
+                                                ("adversarial_bf16_256k", True))]
+        print("[bench] other workloads done", file=sys.stderr, flush=True)
     if not args.no_chunked:
         line["chunked_prefill"] = [chunked_prefill("dsa_bf16_128k", c, 3) for c in (256, 1024)]
         print("[bench] chunked prefill done", file=sys.stderr, flush=True)

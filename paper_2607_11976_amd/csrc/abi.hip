@@ -15,7 +15,7 @@ constexpr int kDefaultBins = 256;
 constexpr int kFallbackGridFused = 64;      // rows re-scored concurrently (scratch rows)
 constexpr int kFallbackGridScores = 256;
 constexpr int kTargetBlocks = 256;          // one block per CU before key splitting stops
-constexpr int kMinSplitKeys = 4096;         // shortest key split the automatic choice makes
+constexpr int kMinSplitKeys = 512;          // shortest key split the automatic choice makes
 constexpr int kMaxAutoSplits = 64;
 constexpr size_t kHistLdsBudget = 96 * 1024;
 constexpr size_t kLdsPerBlock = 160 * 1024;   // gfx950 LDS per workgroup

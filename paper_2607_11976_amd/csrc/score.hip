@@ -1258,7 +1258,8 @@ struct GroupedSink {
         above_s[lq] = ab;
         qs[lq].ups = up_of(t);
         taus_v = t;
-        __hip_atomic_store(pub + (int64_t)(qbase + lq) * 8 + split, (uint8_t)(t + 1), __ATOMIC_RELAXED,
+        // (bins above 254 publish as 254: a lower bin is still a lower bound)
+        __hip_atomic_store(pub + (int64_t)(qbase + lq) * 8 + split, (uint8_t)(min(t, 254) + 1), __ATOMIC_RELAXED,
                            __HIP_MEMORY_SCOPE_AGENT);
       }
     }
@@ -1356,9 +1357,8 @@ __global__ __launch_bounds__(C::NTHREADS) void k_fused(ScoreArgs a, const RowPar
   if constexpr (C::GROUPED) {
     sink.bind(lds + C::SCAN_LDS + wave * GroupedSink<C>::kLdsPerWave);
     sink.kq0 = kb;
-    // splits share thresholds through one byte per (row, split): up to 8
-    // splits, bins + 1 below 256
-    sink.pub = S > 1 && S <= 8 && m <= 255 ? pub : nullptr;
+    // splits share thresholds through one byte per (row, split): up to 8 splits
+    sink.pub = S > 1 && S <= 8 ? pub : nullptr;
   }
   sink.cand = cand;
   sink.qbase = qbase;
@@ -1484,7 +1484,7 @@ hipError_t launch_dense_scores(const ScoreArgs& a, float* out, int64_t ld, hipSt
 // Published bins of the rows' splits start at the sample's (stored + 1).
 __global__ void k_pub_init(const RowParam* params, int nq, uint64_t* pub) {
   for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < nq; i += (int64_t)gridDim.x * blockDim.x)
-    pub[i] = 0x0101010101010101ull * (uint64_t)(uint8_t)(params[i].tau0 + 1);
+    pub[i] = 0x0101010101010101ull * (uint64_t)(uint8_t)(min(params[i].tau0, 254) + 1);
 }
 
 hipError_t launch_fused_scan(const ScoreArgs& a, const RowParam* params, int S, int L, int cap, int m, int k,
@@ -1496,7 +1496,7 @@ hipError_t launch_fused_scan(const ScoreArgs& a, const RowParam* params, int S, 
       err = hipSuccess;
       return;
     }
-    if (C::GROUPED && S > 1 && S <= 8 && m <= 255) {
+    if (C::GROUPED && S > 1 && S <= 8) {
       hipLaunchKernelGGL(k_pub_init, dim3((a.nq + 255) / 256), dim3(256), 0, st, params, a.nq,
                          reinterpret_cast<uint64_t*>(pub));
       if ((err = hipGetLastError()) != hipSuccess) return;
