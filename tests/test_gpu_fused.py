@@ -136,3 +136,40 @@ def test_fused_deterministic(lib):
     np.testing.assert_array_equal(a[0], b[0])
     np.testing.assert_array_equal(a[1].view(np.uint32), b[1].view(np.uint32))
     np.testing.assert_array_equal(a[2], b[2])
+
+
+# The grouped filter (H <= 4: many queries per wave): key splits that share a
+# threshold (up to 8) and splits that do not, bins past what a published byte
+# holds, rows without a gate (every score passes: the in-place path), tiny
+# lists (overflow and fallback), and the forced fallback -- every result the
+# same, bit for bit, and within tolerance of the oracle.
+GROUPED = [
+    # id, base config, nq, nk, k, mode
+    ("ip_bf16_h1", "retrieval_bf16_4m", 300, 50001, 100, "ip"),
+    ("dsa_f32_h4", "tiny_fp32", 40, 9001, 256, "dsa"),
+]
+
+
+@pytest.mark.parametrize("opt", [
+    dict(key_splits=2),
+    dict(key_splits=5),
+    dict(key_splits=8),
+    dict(key_splits=12),
+    dict(key_splits=6, num_bins=300),
+    dict(sample_size=0),
+    dict(key_splits=3, sample_size=0),
+    dict(capacity=48),
+    dict(force_fallback=True),
+], ids=lambda o: ",".join(f"{a}={b}" for a, b in o.items()))
+@pytest.mark.parametrize("law", GROUPED, ids=[g[0] for g in GROUPED])
+def test_grouped_forced_paths_are_exact(lib, law, opt):
+    name, base, nq, nk, k, mode = law
+    cfg = workloads.scaled(workloads.CONFIGS[base], nq=nq, nk=nk)
+    x = workloads.generate(cfg, seed=12)
+    ref = _fused(x, k, mode, sorted_output=True)
+    got = _fused(x, k, mode, sorted_output=True, **opt)
+    np.testing.assert_array_equal(got[0], ref[0])
+    np.testing.assert_array_equal(got[1].view(np.uint32), ref[1].view(np.uint32))
+    _check_tol(x, cfg.dtype, k, mode, got[0], got[1])
+    if opt.get("force_fallback"):
+        assert np.all(got[2][:, 2] == 3)
