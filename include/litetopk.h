@@ -92,7 +92,7 @@ typedef struct lt_options {
                               "Sampling"); 1..LT_MAX_BINS; default 256          */
   int32_t sample_size;     /* k': sampled keys per launch (sec. 3.2: k' = 3k for
                               DSA); negative = default: 3k in DSA mode,
-                              max(3k, min(Nk/64, 65536)) in IP mode, max(3k,
+                              max(3k, min(Nk/128, 65536)) in IP mode, max(3k,
                               65536) for the 768-dimensional IP shape (all
                               capped at Nk; the scores-in entry uses 3k); 0
                               disables the gate. With sample_keys set: the

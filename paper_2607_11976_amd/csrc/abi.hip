@@ -95,10 +95,13 @@ int resolve_sample(const lt_options* o, const Resolved& r, int nk, int k, int mo
   if (ns < 0) {
     ns = 3 * k;  // sec. 3.2: k' = 3k
     if (fused && mode == LT_SCORE_IP) {
-      // a random sample's k-th score sits at rank k * nk / ns of the corpus;
-      // with splits sharing their thresholds, the first tiles of every split
-      // run at that rank, so the wide scan samples kSharedSample keys
-      ns = std::max(ns, r.shared ? kSharedSample : std::min(nk / 64, 65536));
+      // a random sample's k-th score sits at rank k * nk / ns of the corpus,
+      // and the first tiles of every split run at that rank: the wide scan
+      // samples kSharedSample keys, the grouped one nk / 128 (the 10000 x 4M
+      // retrieval: nk / 64 took 15.9 ms a call, nk / 128 15.2, nk / 256 15.4;
+      // its scoring and range stages grow with the sample, its survivors
+      // shrink)
+      ns = std::max(ns, r.shared ? kSharedSample : std::min(nk / 128, 65536));
     }
   }
   return sample_count(ns, nk);
