@@ -1054,6 +1054,7 @@ struct GroupedSink {
     steps = 0;
     ntile = 0;
     qlen = 0;
+    // tiles start at kq0 + 64 j, so the last one ends below kq0 + 2^24
     use_queue = kend - kq0 < (1 << 24);
     tau_v = valid ? t0 : m - 1;
     taus_v = tau_v;
