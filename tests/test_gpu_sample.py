@@ -67,12 +67,13 @@ def test_sample_from_topk_dsa_shaped(lib):
     np.testing.assert_array_equal(got.cpu().numpy(), orc.sample_from_topk(prev, cfg.nk, 3 * cfg.k))
 
 
+@pytest.mark.parametrize("nk", [70000, 300000])
 @pytest.mark.parametrize("big", [1500, 2_200_000])
-def test_sample_from_topk_large_counts(lib, big):
+def test_sample_from_topk_large_counts(lib, big, nk):
     """Counts above 2^10 and 2^21 exercise the upper digits of the radix pick;
-    ties between keys with equal large counts must still go to the lower key."""
+    ties between keys with equal large counts must still go to the lower key.
+    70000 keys are counted in LDS, 300000 with global atomics."""
     rng = np.random.default_rng(big)
-    nk = 70000
     heavy = np.array([5, 60000, 123, 777, 69999, 40000], dtype=np.int32)
     reps = np.array([big, big, big - 1, big + 3, 2, big], dtype=np.int64)
     body = np.repeat(heavy, reps)
@@ -83,6 +84,18 @@ def test_sample_from_topk_large_counts(lib, big):
     flat = np.concatenate([flat, np.full((-flat.size) % cols, -1, np.int32)])
     prev = flat.reshape(-1, cols)
     for ns in (1, 2, 4, 5, 300):
+        np.testing.assert_array_equal(_gpu_sample(prev, nk, ns), orc.sample_from_topk(prev, nk, ns))
+
+
+@pytest.mark.parametrize("nk", [262144, 262145, 500000])
+def test_sample_from_topk_around_the_lds_count_limit(lib, nk):
+    """Key arrays at, just past and well past the largest one counted in LDS,
+    with the clamped single histogram pass (few entries) and the digit passes
+    (a sample larger than entries / 2047 allows)."""
+    rng = np.random.default_rng(nk)
+    prev = np.minimum(rng.zipf(1.3, size=(96, 2048)) * 7 + rng.integers(0, 7, size=(96, 2048)), nk + 3) - 2
+    prev = prev.astype(np.int32)
+    for ns in (1, 97, 6144):
         np.testing.assert_array_equal(_gpu_sample(prev, nk, ns), orc.sample_from_topk(prev, nk, ns))
 
 
