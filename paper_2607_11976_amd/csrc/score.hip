@@ -461,28 +461,50 @@ __device__ __forceinline__ uint32_t lds_state_slot(const void* rec, uint32_t* ct
   return r;
 }
 
-// A slot from an LDS counter (ds_add_rtn_u32 of 1, the old value), an
-// 8-byte LDS write, an 8-byte LDS read and a 32-byte per-query record read
-// (as two 16-byte halves). Opaque for the same reason as lds_inc; the reads
-// wait for their data.
+// A slot from an LDS counter (ds_add_rtn_u32 of 1, the old value), LDS
+// writes and reads, and a 32-byte per-query record read (as two 16-byte
+// halves). Opaque for the same reason as lds_inc; the reads wait for their
+// data.
 __device__ __forceinline__ uint32_t lds_slot(uint32_t* ctr) {
   const uint32_t b = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) uint32_t*)ctr;
   uint32_t r;
   asm volatile("ds_add_rtn_u32 %0, %1, %2\n\ts_waitcnt lgkmcnt(0)" : "=v"(r) : "v"(b), "v"(1u) : "memory");
   return r;
 }
-typedef uint32_t u32x2_t __attribute__((ext_vector_type(2)));
-__device__ __forceinline__ void lds_put2(uint32_t* p, uint32_t x, uint32_t y) {
-  const uint32_t a = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) uint32_t*)p;
-  const u32x2_t v = {x, y};
-  asm volatile("ds_write_b64 %0, %1" ::"v"(a), "v"(v) : "memory");
+__device__ __forceinline__ void lds_put4(float* p, f32x4_t v) {
+  const uint32_t a = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) float*)p;
+  asm volatile("ds_write_b128 %0, %1" ::"v"(a), "v"(v) : "memory");
 }
-__device__ __forceinline__ void lds_get2(const uint32_t* p, uint32_t (&out)[2]) {
+__device__ __forceinline__ void lds_put1(uint32_t* p, uint32_t v) {
+  const uint32_t a = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) uint32_t*)p;
+  asm volatile("ds_write_b32 %0, %1" ::"v"(a), "v"(v) : "memory");
+}
+__device__ __forceinline__ uint32_t lds_get1(const uint32_t* p) {
   const uint32_t a = (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) uint32_t*)p;
-  u32x2_t v;
-  asm volatile("ds_read_b64 %0, %1\n\ts_waitcnt lgkmcnt(0)" : "=v"(v) : "v"(a) : "memory");
-  out[0] = v[0];
-  out[1] = v[1];
+  uint32_t r;
+  asm volatile("ds_read_b32 %0, %1\n\ts_waitcnt lgkmcnt(0)" : "=v"(r) : "v"(a) : "memory");
+  return r;
+}
+// N (2 or 8) consecutive 16-byte LDS reads under one wait
+template <int N>
+__device__ __forceinline__ void lds_get_n(const float* p, f32x4_t (&o)[N]) {
+  static_assert(N == 2 || N == 8, "record sizes of the grouped layouts");
+  const uint32_t a = (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) float*)p;
+  if constexpr (N == 2) {
+    asm volatile("ds_read_b128 %0, %2\n\tds_read_b128 %1, %2 offset:16\n\ts_waitcnt lgkmcnt(0)"
+                 : "=&v"(o[0]), "=&v"(o[1])
+                 : "v"(a)
+                 : "memory");
+  } else {
+    asm volatile(
+        "ds_read_b128 %0, %8\n\tds_read_b128 %1, %8 offset:16\n\t"
+        "ds_read_b128 %2, %8 offset:32\n\tds_read_b128 %3, %8 offset:48\n\t"
+        "ds_read_b128 %4, %8 offset:64\n\tds_read_b128 %5, %8 offset:80\n\t"
+        "ds_read_b128 %6, %8 offset:96\n\tds_read_b128 %7, %8 offset:112\n\ts_waitcnt lgkmcnt(0)"
+        : "=&v"(o[0]), "=&v"(o[1]), "=&v"(o[2]), "=&v"(o[3]), "=&v"(o[4]), "=&v"(o[5]), "=&v"(o[6]), "=&v"(o[7])
+        : "v"(a)
+        : "memory");
+  }
 }
 __device__ __forceinline__ void lds_get_rec(const void* rec, f32x4_t& f, i32x4_t& g) {
   const uint32_t a = (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) void*)rec;
@@ -934,15 +956,16 @@ struct FusedSink {
 // counted. The order of a list's entries depends on the order in which the
 // atomics are served; the final select orders candidates by (score, key)
 // alone, so no result depends on it.
-// Passing scores are not written out in the tile that finds them: each wave
-// appends them to its LDS queue (a ballot and one LDS write per item, no
-// round trip), and every kDrainEvery tiles all waves drain their queues at
-// once, one entry per lane, re-checking each against the row's current gate.
+// Passing scores are not written out in the tile that finds them: every
+// lane with one appends a record of its tile scores to the wave's LDS queue
+// (a ballot, mbcnt for the slot, a few LDS writes, no round trip), and every
+// kDrainEvery tiles all waves drain their queues at once, one record per
+// lane, re-checking each score against its row's current gate.
 // Handled where found, the per-item work of one wave held up the other waves
 // of its block at the tile barrier on most tiles; drained together, no wave
-// waits for another, and the counting's LDS round trips serve 64 entries at a
-// time. The thresholds then move up to kDrainEvery tiles later, which only
-// lets a few more keys through. A tile with more passing scores than the
+// waits for another, and the counting's LDS round trips serve many records
+// at a time. The thresholds then move up to kDrainEvery tiles later, which
+// only lets a few more keys through. A tile with more passing lanes than the
 // queue holds (a row without a gate) is handled in place.
 // Key splits of one row share a threshold (S > 1). Besides its own bin tau
 // (the largest bin with at least k of the split's candidates at or above
@@ -969,16 +992,19 @@ struct GroupedSink {
     int s, e;        // visible keys [s, e) within this split
     int pad;
   };
-  static constexpr int kQueue = 128;      // entries of a wave's queue of passing scores
+  static constexpr int kRecs = 8;         // records of a wave's queue: a lane's scores of one tile
   static constexpr int kDrainEvery = 16;  // tiles between queue drains
   static constexpr int kShareEvery = 2;   // tiles between reads of the published bins
-  static constexpr int kLdsPerWave = C::QW * (int)sizeof(QState) + 3 * C::QW * 4 + kQueue * 8;
+  static constexpr int kLdsPerWave =
+      C::QW * (int)sizeof(QState) + 3 * C::QW * 4 + kRecs * C::NI * 4 + ((kRecs * 4 + 15) & ~15);
+  static_assert(C::NI % 4 == 0 && (C::QW * 12) % 16 == 0, "16-byte aligned records");
   QState* qs;         // LDS [QW]
   uint32_t* tail;     // LDS [QW]: candidates passed (the list length; may exceed cap)
   uint32_t* above;    // LDS [QW]: counted candidates in bins above tau
   uint32_t* above_s;  // LDS [QW]: the same above tau_s
-  uint32_t* queue;    // LDS [kQueue][2]: (score bits, (key - kq0) << 8 | query)
-  int qlen;           // entries in the queue
+  float* rec;         // LDS [kRecs][NI]: a lane's scores of one tile
+  uint32_t* rhdr;     // LDS [kRecs]: (tile's first key - kq0) << 8 | lane
+  int qlen;           // records in the queue
   int kq0;            // first key of the split
   bool use_queue;     // keys of the split are told apart by 24 bits
   float tq[C::NIH];   // T of the query of item j (items j and j + NIH share it)
@@ -998,7 +1024,8 @@ struct GroupedSink {
     tail = reinterpret_cast<uint32_t*>(lds + C::QW * sizeof(QState));
     above = tail + C::QW;
     above_s = above + C::QW;
-    queue = above_s + C::QW;
+    rec = reinterpret_cast<float*>(above_s + C::QW);
+    rhdr = reinterpret_cast<uint32_t*>(rec + kRecs * C::NI);
   }
 
   __device__ static float gate_floor(float delta, float c, int tau) {
@@ -1134,7 +1161,29 @@ struct GroupedSink {
       float mx = -__builtin_inff();
 #pragma unroll
       for (int j = 0; j < C::NIH; ++j) mx = fmaxf(mx, fmaxf(sc[j], sc[j + C::NIH]) - tq[j]);
-      if (__ballot(mx >= 0.0f) == 0) return;  // wave-uniform: nothing passes
+      const bool lp = mx >= 0.0f;  // some score of this lane passes
+      const uint64_t lm = __ballot(lp);
+      if (lm == 0) return;  // wave-uniform: nothing passes
+      if (use_queue) {
+        // append a record of every such lane: its scores and where they are
+        const int nrec = __popcll(lm);
+        if (qlen + nrec > kRecs) {
+          drain();
+          refresh();
+        }
+        if (nrec <= kRecs) {
+          if (lp) {
+            const int slot = qlen + (int)mbcnt64(lm);
+            float* rp = rec + slot * C::NI;
+#pragma unroll
+            for (int v = 0; v < C::NI / 4; ++v)
+              lds_put4(rp + 4 * v, f32x4_t{sc[4 * v], sc[4 * v + 1], sc[4 * v + 2], sc[4 * v + 3]});
+            lds_put1(rhdr + slot, (uint32_t)(k0 - kq0) << 8 | (uint32_t)l);
+          }
+          qlen += nrec;
+          return;
+        }
+      }
     }
     // bit it of `bits`: this lane's score of item it passed the compare
     // (built from the top item down: a compare and a shift-add of its result)
@@ -1146,30 +1195,6 @@ struct GroupedSink {
     fNI scv;
 #pragma unroll
     for (int it = 0; it < C::NI; ++it) scv[it] = sc[it];
-    if (use_queue) {
-      const int n = __builtin_amdgcn_readlane((int)wave_prefix_sum((uint32_t)__builtin_popcount(bits)), kWave - 1);
-      if (qlen + n > kQueue) {
-        drain();
-        refresh();
-      }
-      if (n <= kQueue) {
-        // append: one ballot and one LDS write per item
-        const uint32_t hq = (uint32_t)(h * (4 / C::H));
-        for (uint32_t rem = items; rem; rem &= rem - 1) {
-          const int it = __builtin_ctz(rem);
-          const bool pass = (bits >> it) & 1u;
-          const uint64_t mask = __ballot(pass);
-          if (pass) {
-            const int j = it % C::NIH, nt = it / C::NIH;
-            const uint32_t q = (uint32_t)item_query(j, 0) + hq;
-            const uint32_t rel = (uint32_t)(k0 - kq0 + nt * 32 + r32);
-            lds_put2(queue + 2 * (qlen + (int)mbcnt64(mask)), __float_as_uint(scv[it]), rel << 8 | q);
-          }
-          qlen += __popcll(mask);
-        }
-        return;
-      }
-    }
     // in place, one item at a time: every passing lane takes its slot and
     // counts at once
     const bool inside = k0 >= vis_s && k0 + C::KT <= vis_e;
@@ -1203,21 +1228,36 @@ struct GroupedSink {
     lds_add(&above_s[q], x >= f[3] ? 1u : 0u);
   }
 
-  // the queue, one entry per lane: entries still at or above their row's
-  // gate and inside its visible range take a slot, are written and counted
+  // the queue, one record per lane: the record's scores still at or above
+  // their row's gate and inside its visible range take a slot, are written
+  // and counted
   __device__ void drain() {
+    static_assert(kRecs <= kWave, "one record per lane");
     const int l = lane_here();
-    for (int b0 = 0; b0 < qlen; b0 += kWave) {
-      const int i = b0 + l;
-      if (i < qlen) {
-        uint32_t ent[2];
-        lds_get2(queue + 2 * i, ent);
-        const float s = __uint_as_float(ent[0]);
-        const int q = (int)(ent[1] & 0xFFu), key = kq0 + (int)(ent[1] >> 8);
+    if (l < qlen) {
+      const float* rp = rec + l * C::NI;
+      f32x4_t sv[C::NI / 4];
+      lds_get_n<C::NI / 4>(rp, sv);
+      const uint32_t hd = lds_get1(rhdr + l);
+      const int src = (int)(hd & 0xFFu), hs = src >> 5, k0 = kq0 + (int)(hd >> 8);
+      const int key0 = k0 + (src & 31);
+      // the record's queries in its lane half: item_q(j, 0) + hs * 4 / H
+      const QState* qh = qs + hs * (4 / C::H);
+      uint32_t bits = 0;
+#pragma unroll
+      for (int it = C::NI - 1; it >= 0; --it)
+        bits = shift_in_nlt(bits, sv[it / 4][it % 4], qh[C::item_q(it % C::NIH, 0)].gate);
+      while (bits) {
+        const int it = __builtin_ctz(bits);
+        bits &= bits - 1;
+        const int j = it % C::NIH, nt = it / C::NIH;
+        const int q = item_query(j, hs);
+        const int key = key0 + nt * 32;
+        const float s = __uint_as_float(lds_get1(reinterpret_cast<const uint32_t*>(rp) + it));
         f32x4_t f;
         i32x4_t g;
         lds_get_rec(&qs[q], f, g);  // g: gate bits, s, e
-        if (!(s < __int_as_float(g[0])) && key >= g[1] && key < g[2]) {
+        if (key >= g[1] && key < g[2]) {
           const uint32_t pos = lds_slot(&tail[q]);
           count(q, s, f);
           if (pos < (uint32_t)cap) cand[lbase + q * lstride + pos] = make_int2(key, __float_as_int(s));
