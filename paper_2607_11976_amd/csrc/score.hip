@@ -992,9 +992,9 @@ struct GroupedSink {
     int s, e;        // visible keys [s, e) within this split
     int pad;
   };
-  static constexpr int kRecs = 8;         // records of a wave's queue: a lane's scores of one tile
+  static constexpr int kRecs = 32;        // records of a wave's queue: a lane's scores of one tile
   static constexpr int kDrainEvery = 16;  // tiles between queue drains
-  static constexpr int kShareEvery = 2;   // tiles between reads of the published bins
+  static constexpr int kShareEvery = 8;   // tiles between reads of the published bins
   static constexpr int kLdsPerWave =
       C::QW * (int)sizeof(QState) + 3 * C::QW * 4 + kRecs * C::NI * 4 + ((kRecs * 4 + 15) & ~15);
   static_assert(C::NI % 4 == 0 && (C::QW * 12) % 16 == 0, "16-byte aligned records");
