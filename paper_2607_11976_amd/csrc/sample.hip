@@ -301,10 +301,10 @@ __global__ __launch_bounds__(kFreqThreads) void k_freq_count_lds(const int32_t* 
   for (int i = threadIdx.x; i < n; i += kFreqThreads) part[(int64_t)ch * nk + lo + i] = c[i];
 }
 
-// counts[key] = sum of the chunks' counts; with `clamp`, the histogram of the
-// counts clamped at kFreqBins - 1 and, in the last block, c*.
+// counts[key] = sum of the chunks' counts; with `clamp`, also the histogram
+// of the counts clamped at kFreqBins - 1.
 __global__ __launch_bounds__(kFreqThreads) void k_freq_merge(const uint32_t* part, int nparts, int nk, bool clamp,
-                                                              uint32_t* counts, FreqState* fs, uint32_t* hist) {
+                                                              uint32_t* counts, uint32_t* hist) {
   __shared__ uint32_t h[kFreqBins];
   for (int i = threadIdx.x; i < kFreqBins; i += kFreqThreads) h[i] = 0u;
   __syncthreads();
@@ -436,8 +436,7 @@ hipError_t launch_sample_from_topk(const int32_t* prev, int64_t ld, int rows, in
     const int mgrid = (nk + kFreqThreads - 1) / kFreqThreads;
     hipLaunchKernelGGL(k_freq_count_lds, dim3(ranges, nparts), dim3(kFreqThreads), 0, st, prev, ld, rows, pk, nk,
                        part, hist, fs, ns);
-    hipLaunchKernelGGL(k_freq_merge, dim3(mgrid), dim3(kFreqThreads), 0, st, part, nparts, nk, clamp, counts, fs,
-                       hist);
+    hipLaunchKernelGGL(k_freq_merge, dim3(mgrid), dim3(kFreqThreads), 0, st, part, nparts, nk, clamp, counts, hist);
     if (clamp) hipLaunchKernelGGL(k_freq_pick, dim3(1), dim3(kWave), 0, st, kFreqClampPass, hist, fs);
   } else {
     hipLaunchKernelGGL(k_freq_zero, dim3(sweep), dim3(kFreqThreads), 0, st, counts, nk, hist, fs, ns);
