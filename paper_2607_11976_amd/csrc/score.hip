@@ -967,7 +967,8 @@ struct FusedSink {
 // at a time. The thresholds then move up to kDrainEvery tiles later, which
 // only lets a few more keys through. A tile with more passing lanes than the
 // queue holds (a row without a gate) is handled in place.
-// Key splits of one row share a threshold (S > 1). Besides its own bin tau
+// Key splits of one row share a threshold (2 to 8 splits; every kShareEvery
+// tiles a wave reads its rows' published bins). Besides its own bin tau
 // (the largest bin with at least k of the split's candidates at or above
 // it), each split tracks tau_s, the same walk for ks = ceil(k / S), and
 // publishes it in its byte of the row's entry in `pub`. The smallest bin g
@@ -1010,7 +1011,7 @@ struct GroupedSink {
   float tq[C::NIH];   // T of the query of item j (items j and j + NIH share it)
   bool ungated;       // some row of the wave has no gate (tau = -1)
   int vis_s, vis_e;   // every row of the wave sees [vis_s, vis_e)
-  uint8_t* pub;       // [nq][8] published bins + 1 of the row's splits (S > 1), or NULL
+  uint8_t* pub;       // [nq][8] published bins + 1 of the row's splits (2 to 8), or NULL
   int tau_v, taus_v;  // lane q: tau and tau_s of query qbase + q
   uint64_t gw;        // lane q: its row's published bytes, as read
   int ks, steps, ntile;
