@@ -277,6 +277,8 @@ struct WideFusedSink {
   lds_u32_t* bh;        // [64, m] LDS: block counts not yet moved to `hist`
   lds_i32_t* btau;      // [64] LDS: the block's threshold bins
   lds_u32_t* btail;     // [64] LDS: slots taken in the block's list of each row
+  float2* bmap;         // [64] LDS: bin map (delta, c) of each row
+  int vis_s, vis_e;     // every row of the block sees [vis_s, vis_e)
   int2* cand;           // [nq, S, cap] (key, score) lists, this block's is `split`
   int qbase, nq, S, split, cap, m, k;
 
@@ -304,6 +306,16 @@ struct WideFusedSink {
     delta_v = dl;
     c_v = c;
     tau_v = t0;
+    // each wave writes the whole map (the same values) before its own reads
+    bmap[l] = make_float2(dl, c);
+    int cs = t < nq ? rr.s : 0, ce = t < nq ? e_v : INT_MAX;
+#pragma unroll
+    for (int o = 1; o < kWave; o <<= 1) {
+      cs = max(cs, __shfl_xor(cs, o));
+      ce = min(ce, __shfl_xor(ce, o));
+    }
+    vis_s = __builtin_amdgcn_readfirstlane(cs);
+    vis_e = __builtin_amdgcn_readfirstlane(ce);
     rq = -1;
     rcount = (int)(threadIdx.x / kWave) % C::REFRESH;
     // wave w refreshes rows w, w + WAVES, ...; blocks start at different ones
@@ -380,44 +392,33 @@ struct WideFusedSink {
   }
 
   // write-back of the items in `items` (wave-uniform bit set of score items
-  // some lane passed; bits = this lane's)
+  // some lane passed; bits = this lane's): every passing lane takes its slot
+  // in the block's list of its row with an LDS atomic and reads the row's bin
+  // map from LDS; the visible range is checked only on tiles that cross some
+  // row's range
   __device__ void emit(int key, uint32_t bits, uint32_t items, const float (&sc)[C::NI]) {
     typedef float fNI __attribute__((ext_vector_type(C::NI)));
     const int l = lane_id(), h = l >> 5;
+    const int k0 = key - (l & 31);
+    const bool inside = k0 >= vis_s && k0 + C::KT <= vis_e;
     fNI scv;
 #pragma unroll
     for (int it = 0; it < C::NI; ++it) scv[it] = sc[it];
-    // passes per query (a query is one item of one lane half)
-    uint32_t cnt_v = 0;
     for (uint32_t rem = items; rem; rem &= rem - 1) {
       const int it = __builtin_ctz(rem), qa = wq_of(it, 0), qb = qa + 4;
-      const uint64_t m2 = __ballot(lane_pass(it, key, bits, qa, qb));
-      const uint32_t lo = (uint32_t)__popcll(m2 & 0xFFFFFFFFull), hi = (uint32_t)__popcll(m2 >> 32);
-      cnt_v = l == qa ? lo : (l == qb ? hi : cnt_v);
-    }
-    // one slot reservation per query with passes, in the block's list
-    uint32_t base_v = 0;
-    if (cnt_v != 0) base_v = __hip_atomic_fetch_add(btail + l, cnt_v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
-    for (uint32_t rem = items; rem; rem &= rem - 1) {
-      const int it = __builtin_ctz(rem), qa = wq_of(it, 0), qb = qa + 4;
-      const bool pass = lane_pass(it, key, bits, qa, qb);
-      const uint64_t m2 = __ballot(pass);
-      const uint32_t lo = (uint32_t)__popcll(m2 & 0xFFFFFFFFull);
-      const uint32_t ba = (uint32_t)__builtin_amdgcn_readlane((int)base_v, qa);
-      const uint32_t bb = (uint32_t)__builtin_amdgcn_readlane((int)base_v, qb);
-      const float da = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, delta_v), qa));
-      const float db = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, delta_v), qb));
-      const float ca = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, c_v), qa));
-      const float cb = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, c_v), qb));
+      const bool pass = inside ? ((bits >> it) & 1u) != 0u : lane_pass(it, key, bits, qa, qb);
       if (pass) {
+        const int q = h ? qb : qa;
+        const uint32_t pos = __hip_atomic_fetch_add(btail + q, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+        const float2 mp = bmap[q];
         const float s = scv[it];
-        const uint32_t pos = h ? bb + mbcnt64(m2) - lo : ba + mbcnt64(m2);
-        const int64_t t = qbase + (h ? qb : qa);
+        const int64_t t = qbase + q;
         if (pos < (uint32_t)cap) cand[ilv_index(t * S + split, pos, (int64_t)nq * S)] = make_int2(key, __float_as_int(s));
-        const float x = fmaf(s, h ? db : da, h ? cb : ca);
-        if (x >= 0.0f)
-          __hip_atomic_fetch_add(bh + (h ? qb : qa) * m + min(__float2int_rz(x), m - 1), 1u, __ATOMIC_RELAXED,
-                                 __HIP_MEMORY_SCOPE_WORKGROUP);
+        // counted only when x >= 0 (not NaN, not below the range): the add is
+        // issued either way, of 0 for the others
+        const float x = fmaf(s, mp.x, mp.y);
+        const int b = min(max(__float2int_rz(x), 0), m - 1);
+        __hip_atomic_fetch_add(bh + q * m + b, x >= 0.0f ? 1u : 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
       }
     }
   }
@@ -505,9 +506,10 @@ __global__ __launch_bounds__(C::NTHREADS) void k_wide_fused(ScoreArgs a, const R
                                                             int2* cand) {
   extern __shared__ __align__(16) uint8_t lds[];
   int* rng = reinterpret_cast<int*>(lds + C::Q_LDS);  // [0] largest end, [1] smallest start
-  uint32_t* btail = reinterpret_cast<uint32_t*>(lds + C::Q_LDS + 16);           // [QT]
-  int* btau = reinterpret_cast<int*>(lds + C::Q_LDS + 16 + C::QT * 4);          // [QT]
-  uint32_t* bh = reinterpret_cast<uint32_t*>(lds + C::Q_LDS + 16 + C::QT * 8);  // [QT, m]
+  uint32_t* btail = reinterpret_cast<uint32_t*>(lds + C::Q_LDS + 16);            // [QT]
+  int* btau = reinterpret_cast<int*>(lds + C::Q_LDS + 16 + C::QT * 4);           // [QT]
+  float2* bmap = reinterpret_cast<float2*>(lds + C::Q_LDS + 16 + C::QT * 8);     // [QT]
+  uint32_t* bh = reinterpret_cast<uint32_t*>(lds + C::Q_LDS + 16 + C::QT * 16);  // [QT, m]
   const int tile = blockIdx.x / S, split = blockIdx.x - tile * S, q0 = tile * C::QT;
   if (threadIdx.x == 0) {
     rng[0] = 0;
@@ -538,6 +540,7 @@ __global__ __launch_bounds__(C::NTHREADS) void k_wide_fused(ScoreArgs a, const R
   sink.bh = (lds_u32_t*)bh;
   sink.btau = (lds_i32_t*)btau;
   sink.btail = (lds_u32_t*)btail;
+  sink.bmap = bmap;
   sink.cand = cand;
   sink.qbase = q0;
   sink.nq = a.nq;
@@ -620,7 +623,7 @@ ScoreShape wide_shape(int dtype, int mode, int h, int d) {
     s.queries_per_block = C::QT;
     s.keys_per_step = C::STEP;
     s.threads = C::NTHREADS;
-    s.scan_lds = C::Q_LDS + 16 + C::QT * 8;  // queries, key range, list tails, bins
+    s.scan_lds = C::Q_LDS + 16 + C::QT * 16;  // queries, key range, list tails, bins, bin maps
     s.shared_rows = 1;
   });
   return s;
@@ -677,7 +680,7 @@ hipError_t launch_wide_fused(const ScoreArgs& a, const RowParam* params, int S, 
     const int ib = (int)std::min<int64_t>((n + 255) / 256, 1024);
     hipLaunchKernelGGL(k_wide_init, dim3(ib < 1 ? 1 : ib), dim3(256), 0, st, params, a.nq, m, gate, hist);
     if ((err = hipGetLastError()) != hipSuccess) return;
-    const size_t lds = C::Q_LDS + 16 + C::QT * 8 + (size_t)C::QT * m * 4;
+    const size_t lds = C::Q_LDS + 16 + C::QT * 16 + (size_t)C::QT * m * 4;
     allow_lds(k_wide_fused<C>, lds);
     hipLaunchKernelGGL(k_wide_fused<C>, dim3(tiles * S), dim3(C::NTHREADS), lds, st, a, params, S, L, cap, m, k,
                        gate, cnt, hist, cand);
