@@ -153,7 +153,7 @@ def measure(name: str, steps: int, warmup: int, unfused: bool, cold: int = 5):
     del flush
 
     # survivors and fallback rows (untimed call with row statistics)
-    stats = torch.zeros((nq, 4), dtype=torch.int32, device=dev)
+    stats = torch.zeros((nq, lt.LT_ROW_STATS), dtype=torch.int32, device=dev)
     lt.indexer_topk(q, w, keys, k, offs, qs, ks, mode=cfg.mode, options=lt.make_options(row_stats=stats),
                     out=out, workspace=ws)
     st = stats.cpu().numpy()
@@ -234,7 +234,7 @@ def chunked_prefill(name: str, chunk: int, reps: int):
     res = {"workload": name, "chunk": chunk, "chunks": len(parts), "sample_size": ns}
     for mode in ("random", "previous"):
         res[mode + "_ms"] = round(timed_steps(lambda: run(mode == "previous"), reps, 1), 4)
-        st = [torch.zeros((p["q"].shape[0], 4), dtype=torch.int32, device=dev) for p in parts]
+        st = [torch.zeros((p["q"].shape[0], lt.LT_ROW_STATS), dtype=torch.int32, device=dev) for p in parts]
         run(mode == "previous", st)
         sv = torch.cat(st).cpu().numpy()
         res[mode + "_survivors_per_row"] = round(float(sv[:, 0].mean()), 1)
@@ -278,7 +278,7 @@ def retrieval_sweep(steps: int):
                 for s_, v in e.stage_ms().items():
                     stg[s_] += v / steps
                 e.close()
-            stats = torch.zeros((cfg.nq, 4), dtype=torch.int32, device=dev)
+            stats = torch.zeros((cfg.nq, lt.LT_ROW_STATS), dtype=torch.int32, device=dev)
             lt.indexer_topk(q, None, kv, k, None, mode="ip", options=lt.make_options(row_stats=stats), out=out,
                             workspace=ws)
             st = stats.cpu().numpy()

@@ -31,9 +31,11 @@
  *    LT_SORTED_OUTPUT the selected entries come in an unspecified but
  *    deterministic order (the paper's select writes the above-threshold bins
  *    directly, sec. 3.2 "Top-k Selection"); with it they are sorted by the
- *    total order. The one-head 768-dimensional shapes always return sorted
- *    rows (their candidate lists fill in arrival order), and report a zero
- *    score as +0.0 and a NaN score as the canonical quiet NaN.
+ *    total order. Shapes with at most four heads (the one-head retrieval and
+ *    768-dimensional shapes, the four-head float32 and bf16 shapes) always
+ *    return sorted rows (their candidate lists fill in arrival order, so
+ *    equal scores are told apart by the key itself), and report a zero score
+ *    as +0.0 and a NaN score as the canonical quiet NaN.
  */
 #ifndef LITETOPK_H
 #define LITETOPK_H
@@ -56,6 +58,7 @@ extern "C" {
 #define LT_MAX_BINS 256
 #define LT_SAMPLE_LIST_MAX 32768  /* longest caller-supplied sample list */
 #define LT_UNION_MAX 32768        /* largest group * k for lt_dsa_union */
+#define LT_ROW_STATS 12           /* int32 fields per row of lt_options.row_stats */
 
 /* ---- enums --------------------------------------------------------------- */
 typedef enum {
@@ -107,11 +110,35 @@ typedef struct lt_options {
   uint32_t flags;          /* LT_SORTED_OUTPUT | LT_FORCE_FALLBACK               */
   uint64_t seed;           /* seed of the key sample                             */
   void** stage_events;     /* NULL, or LT_NUM_STAGE_EVENTS hipEvent_t handles     */
-  int32_t* row_stats;      /* NULL, or a DEVICE int32 [num_queries, 4] receiving per
-                              row: {candidates written (summed over splits),
-                              final threshold bin, fallback reason (0 none,
-                              1 buffer overflow, 2 threshold-bin overflow,
-                              3 forced), candidates in the threshold bin}       */
+  int32_t* row_stats;      /* NULL, or a DEVICE int32 [num_queries, LT_ROW_STATS]
+                              receiving per row (the internal invariants of
+                              sec. 3.2, for tests and tuning):
+                              [0] candidates written (summed over splits);
+                              [1] final threshold bin tau_f (-2 if the row was
+                                  queued before it was found);
+                              [2] fallback reason: 0 none, 1 candidate buffer
+                                  overflow, 2 threshold bin too large to sort,
+                                  3 forced, 4 candidate count disagrees with
+                                  the histogram, 5 tau_f below the sample's
+                                  initial bin (sample and scan scores
+                                  disagree; sec. 3.2 "Sampling" guarantees
+                                  tau_f >= tau0 otherwise);
+                              [3] candidates in bin tau_f;
+                              [4] the sample's initial bin tau0 (-1 = no gate);
+                              [5] bits of the float32 k-th largest visible
+                                  sample score under the total order (-inf if
+                                  fewer than k sample keys are visible);
+                              [6], [7] bits of the float32 bin map (delta, c):
+                                  a score I falls in bin
+                                  floor(fmaf(I, delta, c)), clamped to
+                                  m - 1 (below 0: not counted);
+                              [8] m, the bins in use (num_bins, lowered where
+                                  the shape's histograms would not fit in LDS);
+                              [9] sample keys visible to the row;
+                              [10], [11] 0.
+                              Fields 4-11 are written for every row, 0-3 by
+                              the final select or when the row is queued.
+                              Collecting them adds passes over the sample.  */
   const int32_t* sample_keys; /* NULL = a random stratified sample drawn with
                               `seed`; else a DEVICE int32 [sample_size] list of
                               key indices to score as the sample instead. Sec. 3.2

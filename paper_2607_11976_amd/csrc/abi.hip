@@ -278,19 +278,23 @@ int lt_indexer_topk(const void* q, const float* q_scale, const float* w, const v
   if ((e = make_list(r, nk, 1, list, st)) != hipSuccess) return hip_status(e);
   if (r.ns > 0 && (e = launch_sample_scores(a, list, r.ns, samp, st)) != hipSuccess) return hip_status(e);
   record(r, LT_STAGE_RANGE, st);
-  if ((e = launch_range(false, samp, r.ns, nq, nk, offs, r.starts, list, r.ns, r.m, k, params, st)) != hipSuccess)
+  if ((e = launch_range(false, samp, r.ns, nq, nk, offs, r.starts, list, r.ns, r.m, k, params, r.stats, st)) !=
+      hipSuccess)
     return hip_status(e);
   record(r, LT_STAGE_FILTER, st);
   e = r.shared ? launch_wide_fused(a, params, r.S, r.L, r.cap, r.m, k, gate, cnt, hist, cand, st)
                : launch_fused_scan(a, params, r.S, r.L, r.cap, r.m, k, gate, cnt, hist, cand, st);
   if (e != hipSuccess) return hip_status(e);
   record(r, LT_STAGE_SELECT, st);
-  if ((e = launch_select(params, cnt, hist, cand, nq, r.S, r.HS, r.cap, r.m, k, r.E,
-                         r.flags | (r.shared ? kSelKeyed : 0u), out_idx, out_scores, qctl, queue, r.stats, st)) !=
-      hipSuccess)
+  // lists in arrival order: ties by key, every row sorted (also the rows the
+  // fallback completes)
+  const uint32_t sel_flags = r.flags | (sh.arrival_order ? kSelKeyed : 0u) | (r.shared ? kSelIlv : 0u);
+  const uint32_t fb_flags = r.flags | (sh.arrival_order ? LT_SORTED_OUTPUT : 0u);
+  if ((e = launch_select(params, cnt, hist, cand, nq, r.S, r.HS, r.cap, r.m, k, r.E, sel_flags, out_idx, out_scores,
+                         qctl, queue, r.stats, st)) != hipSuccess)
     return hip_status(e);
   record(r, LT_STAGE_FALLBACK, st);
-  if ((e = launch_fused_fallback(a, k, r.flags, qctl, queue, scratch, kFallbackGridFused, out_idx, out_scores,
+  if ((e = launch_fused_fallback(a, k, fb_flags, qctl, queue, scratch, kFallbackGridFused, out_idx, out_scores,
                                  st)) != hipSuccess)
     return hip_status(e);
   record(r, LT_NUM_STAGE_EVENTS - 1, st);
@@ -350,7 +354,7 @@ int lt_topk_select(const float* scores, int64_t stride, int32_t nq, int32_t nk, 
   if ((e = launch_init(qctl, st)) != hipSuccess) return hip_status(e);
   if ((e = make_list(r, nk, kSampleBlockScores, list, st)) != hipSuccess) return hip_status(e);
   record(r, LT_STAGE_RANGE, st);
-  if ((e = launch_range(true, scores, stride, nq, nk, offs, r.starts, list, r.ns, r.m, k, params, st)) !=
+  if ((e = launch_range(true, scores, stride, nq, nk, offs, r.starts, list, r.ns, r.m, k, params, r.stats, st)) !=
       hipSuccess)
     return hip_status(e);
   record(r, LT_STAGE_FILTER, st);

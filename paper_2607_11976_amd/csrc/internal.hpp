@@ -14,9 +14,11 @@ namespace lt {
 hipError_t launch_init(uint32_t* qctl, hipStream_t st);
 // Visibility: row t sees keys [s_t, e_t) (row_range); `offs` holds the ends
 // (NULL = num_keys) and `starts` the starts (NULL = 0).
+// With stats non-NULL, also writes row_stats fields 4..11 (the sample's
+// initial bin and k-th score, the bin map, the bins in use).
 hipError_t launch_range(bool from_scores, const float* src, int64_t stride, int nq, int nk,
                         const int32_t* offs, const int32_t* starts, const int32_t* list, int ns, int m, int k,
-                        RowParam* params, hipStream_t st);
+                        RowParam* params, int32_t* stats, hipStream_t st);
 hipError_t launch_filter(const float* scores, int64_t stride, int nq, int nk, const int32_t* offs,
                          const int32_t* starts, const RowParam* params, int S, int L, int cap, int m, int k,
                          uint32_t* cnt, uint32_t* hist, int2* cand, hipStream_t st);
@@ -69,6 +71,8 @@ struct ScoreShape {
   size_t scan_lds;        // LDS bytes of the fused scan (tiles, per-query state), excluding histograms
   int shared_rows;        // 1: all key splits of a row share one histogram,
                           // threshold and candidate list (the wide scan)
+  int arrival_order;      // 1: candidate lists fill in arrival order, not key
+                          // order (the grouped and wide scans)
 };
 ScoreShape score_shape(int dtype, int mode, int h, int d);
 
@@ -101,9 +105,13 @@ hipError_t launch_wide_fallback(const ScoreArgs& a, int k, uint32_t flags, const
                                 const int32_t* queue, float* scratch, int grid, int32_t* out_i, float* out_s,
                                 hipStream_t st);
 
-// k_select flag (internal): candidate lists are not in key order (the wide
-// scan's lists fill in arrival order), so equal scores are ordered by the key
-// itself and every row is output sorted.
+// k_select flags (internal).
+// kSelKeyed: candidate lists are not in key order (the grouped and wide scans
+// fill them in arrival order), so equal scores are ordered by the key itself,
+// every row is output sorted and its scores are rebuilt from the sort keys.
+// kSelIlv: the lists are stored interleaved in chunks of 16 (ilv_index, the
+// wide scan); rows are few and long, so the select runs 1024-thread blocks.
 constexpr uint32_t kSelKeyed = 1u << 30;
+constexpr uint32_t kSelIlv = 1u << 29;
 
 }  // namespace lt

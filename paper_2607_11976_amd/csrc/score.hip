@@ -120,23 +120,19 @@ struct Cfg {
   // GROUPED: H <= 4, a 4-row accumulator group holds whole queries, no
   // cross-lane step. Otherwise H % 8 == 0 and the halves are combined.
   static constexpr bool GROUPED = H <= 4;
-  // fp8 DSA with H >= 8: ReLU and head weighting on packed bf16 pairs
-  // (convert, integer max with 0, bf16 dot product accumulating in fp32):
-  // three instructions per two heads instead of four. Relative error of a
-  // score below 2^-8 for non-negative weights, inside the fp8 tolerance.
-  static constexpr bool PACKED_EPI = DT == DT_FP8 && !GROUPED && RELU && QW == 1;
   static constexpr int GPQ = GROUPED ? 4 / H : 1;      // queries per 4-row group
   static constexpr int NI = GROUPED ? NT * MT * 4 * GPQ : NT * QW / 2;  // scores per lane per tile
   static constexpr int NIH = GROUPED ? MT * 4 * GPQ : QW;              // per-lane results of one sub-tile
   // epilogue VALU ops of one sub-tile (ReLU + FMA per accumulator element)
   // spread over the MFMAs of the other sub-tile. The 64-head values leave
   // room for the combine and gate work of the half step too (measured best
-  // on MI355X: 5 for bf16, 17 for fp8, against 4 and 13 for the epilogue
-  // alone).
-  static constexpr int VALU_PER_MFMA =
-      H == 64 && QW == 1 && DT == DT_BF16  ? 5
-      : H == 64 && QW == 1 && DT == DT_FP8 ? 17
-      : ((DT == DT_FP8 && H >= 8 && RELU && QW == 1 ? 26 : 32) * MT + KS * MT - 1) / (KS * MT);
+  // on MI355X: 5 for bf16, against 4 for the epilogue alone).
+#ifndef LT_FP8_VALU_PER_MFMA
+#define LT_FP8_VALU_PER_MFMA 20
+#endif
+  static constexpr int VALU_PER_MFMA = H == 64 && QW == 1 && DT == DT_BF16  ? 5
+                                       : H == 64 && QW == 1 && DT == DT_FP8 ? LT_FP8_VALU_PER_MFMA
+                                                                            : (32 * MT + KS * MT - 1) / (KS * MT);
   static_assert((QW * H) % 32 == 0, "a wave must fill whole M tiles");
   static_assert(NT == 2, "the scan pipelines the two 32-key halves of a tile");
   static_assert(CHUNKS % NTHREADS == 0 && CPT < 16, "tile staging assumes whole instructions per thread");
@@ -163,15 +159,11 @@ struct Cfg {
 
 // Per-wave stationary operands: the A fragments of the wave's queries and the
 // head weight of every accumulator row the lane holds.
-typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
-typedef float f32x2_t __attribute__((ext_vector_type(2)));
-typedef short i16x2_t __attribute__((ext_vector_type(2)));
 
 template <class C>
 struct WaveQ {
   typename C::M::Frag qa[C::MT][C::KS];
   float wv[C::MT][16];
-  bf16x2_t wp[C::MT][8];  // PACKED_EPI: weights of accumulator rows (2i, 2i+1)
 };
 
 template <class C>
@@ -203,11 +195,6 @@ __device__ __forceinline__ void load_q(WaveQ<C>& s, const ScoreArgs& a, int qbas
         if constexpr (C::DT == DT_FP8) wt *= a.q_scale[(int64_t)t * C::H + j];
       }
       s.wv[mt][v] = wt;
-    }
-    if constexpr (C::PACKED_EPI) {
-#pragma unroll
-      for (int i = 0; i < 8; ++i)
-        s.wp[mt][i] = __builtin_convertvector((f32x2_t){s.wv[mt][2 * i], s.wv[mt][2 * i + 1]}, bf16x2_t);
     }
   }
 }
@@ -342,28 +329,6 @@ __device__ __forceinline__ void reduce_half(const WaveQ<C>& s, const f32x16_t (&
           }
           out[(mt * 4 + i) * C::GPQ + sq] = sum;
         }
-  } else if constexpr (C::PACKED_EPI) {
-    // all conversions, then all maxima, then the dot products into four
-    // partial sums: no instruction waits on the one just before it
-    i16x2_t z[C::MT][8];
-#pragma unroll
-    for (int mt = 0; mt < C::MT; ++mt)
-#pragma unroll
-      for (int j = 0; j < 8; ++j)
-        z[mt][j] = __builtin_bit_cast(
-            i16x2_t, __builtin_convertvector((f32x2_t){acc[mt][2 * j], acc[mt][2 * j + 1]}, bf16x2_t));
-#pragma unroll
-    for (int mt = 0; mt < C::MT; ++mt)
-#pragma unroll
-      for (int j = 0; j < 8; ++j) z[mt][j] = __builtin_elementwise_max(z[mt][j], (i16x2_t){0, 0});
-    float part[1] = {};
-#pragma unroll
-    for (int mt = 0; mt < C::MT; ++mt)
-#pragma unroll
-      for (int j = 0; j < 8; ++j)
-        part[j % 1] = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2_t, z[mt][j]), s.wp[mt][j],
-                                                      part[j % 1], false);
-    out[0] = part[0];
   } else {
 #pragma unroll
     for (int q = 0; q < C::QW; ++q) out[q] = 0.0f;
@@ -1467,9 +1432,10 @@ static bool with_cfg(int dt, int mode, int h, int d, F&& f) {
 }
 
 ScoreShape score_shape(int dtype, int mode, int h, int d) {
-  ScoreShape s{0, 0, 0, 0, 0, 0};
+  ScoreShape s{0, 0, 0, 0, 0, 0, 0};
   const bool found = with_cfg(dtype, mode, h, d, [&]<class C>() {
     s.supported = 1;
+    s.arrival_order = C::GROUPED ? 1 : 0;
     s.queries_per_block = C::QT;
     s.keys_per_step = C::KT;
     s.threads = C::NTHREADS;

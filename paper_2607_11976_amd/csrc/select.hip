@@ -51,11 +51,12 @@ template <int NTH, bool FROM_SCORES>
 __global__ __launch_bounds__(NTH) void k_range(const float* src, int64_t stride, int nq, int nk,
                                                          const int32_t* offs, const int32_t* starts,
                                                          const int32_t* list, int ns, int m, int k,
-                                                         RowParam* params) {
+                                                         RowParam* params, int32_t* stats) {
   constexpr int NW = NTH / kWave;
   __shared__ uint32_t hist[kMaxBins];
   __shared__ float red_mn[NW], red_mx[NW];
   __shared__ uint32_t red_n[NW];
+  __shared__ uint32_t sel[2];
   const int row = blockIdx.x, wave = threadIdx.x / kWave, l = lane_id();
   const RowRange rr = row_range(offs, starts, row, nk);
   const float* rp = src + (int64_t)row * stride;
@@ -114,7 +115,55 @@ __global__ __launch_bounds__(NTH) void k_range(const float* src, int64_t stride,
   if (wave == 0) {
     const int tau0 = wave_threshold(hist, m, (uint32_t)k, nullptr);
     if (l == 0) params[row] = RowParam{delta, c, tau0, (int)nvis};
+    if (stats && l == 0) {
+      int32_t* sr = stats + (int64_t)row * LT_ROW_STATS;
+      sr[4] = tau0;
+      sr[6] = (int32_t)__float_as_uint(delta);
+      sr[7] = (int32_t)__float_as_uint(c);
+      sr[8] = m;
+      sr[9] = (int32_t)nvis;
+      sr[10] = 0;
+      sr[11] = 0;
+    }
   }
+  if (!stats) return;
+  // The sample's k-th score under the total order (for the invariant
+  // kth(sample) <= kth(row) of sec. 3.2 "Sampling"): most-significant-digit
+  // radix selection over the order keys of the visible sample scores, four
+  // 8-bit digits, the bins reused as the digit histogram.
+  uint32_t prefix = 0, pmask = 0, want = (uint32_t)k;
+  for (int shift = 24; shift >= 0 && nvis >= (uint32_t)k; shift -= 8) {
+    __syncthreads();
+    for (int b = threadIdx.x; b < kMaxBins; b += NTH) hist[b] = 0u;
+    __syncthreads();
+    for (int base = 0; base < ns; base += NTH * kRangeUnroll) {
+      float sv[kRangeUnroll];
+      bool vis[kRangeUnroll];
+      range_load<NTH, FROM_SCORES>(rp, list, ns, rr, base, sv, vis);
+#pragma unroll
+      for (int u = 0; u < kRangeUnroll; ++u) {
+        const uint32_t o = ord_key(sv[u]);
+        if (vis[u] && (o & pmask) == prefix) atomicAdd(&hist[(o >> shift) & 0xFFu], 1u);
+      }
+    }
+    __syncthreads();
+    if (wave == 0) {
+      uint32_t above = 0;
+      const int dg = wave_threshold(hist, kMaxBins, want, &above);
+      if (l == 0) {
+        sel[0] = (uint32_t)dg;
+        sel[1] = above;
+      }
+    }
+    __syncthreads();
+    const uint32_t dg = sel[0], above = sel[1];
+    prefix |= dg << shift;
+    pmask |= 0xFFu << shift;
+    want -= above;
+  }
+  if (threadIdx.x == 0)
+    stats[(int64_t)row * LT_ROW_STATS + 5] =
+        nvis >= (uint32_t)k ? (int32_t)__float_as_uint(ord_inv(prefix)) : (int32_t)0xFF800000u;
 }
 
 // ---------------------------------------------------------------------------
@@ -220,8 +269,10 @@ __global__ __launch_bounds__(kFilterWaves * kWave) void k_filter(
 // short lists cost no more than one long one. Keyed rows (few rows with
 // hundreds of thousands of candidates each) run 1024 threads with 8 entries
 // per thread; the others 256 threads with 4.
-// Rows whose buffer overflowed, whose threshold bin does not fit in LDS, or
-// that are forced, are queued for the exact fallback instead.
+// Rows whose buffer overflowed, whose threshold bin does not fit in LDS,
+// whose counts disagree with their lists, whose final bin lies below the
+// sample's initial bin, or that are forced, are queued for the exact fallback
+// instead.
 // ---------------------------------------------------------------------------
 constexpr int kSelThreads = 256;
 constexpr int kSelPer = 4;         // list entries per thread per step
@@ -247,6 +298,7 @@ __global__ __launch_bounds__(NTH) void k_select(
   // key itself, the output is rebuilt from the sort entries, and every row
   // is sorted (the order of arrival would make it vary between calls)
   const bool keyed = flags & kSelKeyed;
+  const bool ilv = flags & kSelIlv;
   const bool sorted = (flags & LT_SORTED_OUTPUT) || keyed;
   int32_t* oi = out_i + (int64_t)row * k;
   float* os = out_s + (int64_t)row * k;
@@ -270,7 +322,7 @@ __global__ __launch_bounds__(NTH) void k_select(
       uint32_t slot = atomicAdd(&qctl[0], 1u);
       queue[slot] = row;
       if (stats) {
-        int32_t* st = stats + (int64_t)row * 4;
+        int32_t* st = stats + (int64_t)row * LT_ROW_STATS;
         st[0] = (int32_t)total_c;
         st[1] = tau;
         st[2] = why;
@@ -304,6 +356,14 @@ __global__ __launch_bounds__(NTH) void k_select(
   const uint32_t c_above = tmp[25];
   __syncthreads();
   const RowParam p = params[row];
+  // Every visible sample key in a bin >= tau0 passes the gate or is
+  // outranked by k counted keys, so an exact scan ends with tau >= tau0. A
+  // lower bin means the sample's scores and the scan's disagree; the bins
+  // between were gated and are incomplete, so the row is recomputed.
+  if (p.tau0 >= 0 && tau < p.tau0) {
+    enqueue(5, tau, 0);
+    return;
+  }
 
   // ---- 2./3. one ordered pass over the candidates ----
   uint32_t run_above = 0, run_tie = 0;
@@ -350,7 +410,7 @@ __global__ __launch_bounds__(NTH) void k_select(
         if (i < gtot) {
           const int64_t li = (int64_t)row * S + g0 + lst[j];
           const uint32_t pos = i - off[lst[j]];
-          ce[j] = cand[keyed ? ilv_index(li, pos, (int64_t)nq * S) : li * cap + pos];
+          ce[j] = cand[ilv ? ilv_index(li, pos, (int64_t)nq * S) : li * cap + pos];
         }
       }
 #pragma unroll
@@ -424,7 +484,7 @@ __global__ __launch_bounds__(NTH) void k_select(
     os[i] = -__builtin_inff();
   }
   if (stats && tid == 0) {
-    int32_t* st = stats + (int64_t)row * 4;
+    int32_t* st = stats + (int64_t)row * LT_ROW_STATS;
     st[0] = (int32_t)total_c;
     st[1] = tau;
     st[2] = 0;
@@ -474,10 +534,11 @@ hipError_t launch_init(uint32_t* qctl, hipStream_t st) {
 
 hipError_t launch_range(bool from_scores, const float* src, int64_t stride, int nq, int nk,
                         const int32_t* offs, const int32_t* starts, const int32_t* list, int ns, int m, int k,
-                        RowParam* params, hipStream_t st) {
+                        RowParam* params, int32_t* stats, hipStream_t st) {
   dim3 grid(nq);
   auto go = [&](auto kernel, int nth) {
-    hipLaunchKernelGGL(kernel, grid, dim3(nth), 0, st, src, stride, nq, nk, offs, starts, list, ns, m, k, params);
+    hipLaunchKernelGGL(kernel, grid, dim3(nth), 0, st, src, stride, nq, nk, offs, starts, list, ns, m, k, params,
+                       stats);
   };
   // a long sample is read in fewer, wider steps (the kernel waits on loads);
   // so are the rows of a launch of few rows, which otherwise leaves most of
@@ -520,7 +581,7 @@ hipError_t launch_select(const RowParam* params, const uint32_t* cnt, const uint
   // over the lists; many rows fill it with narrow ones (measured on MI355X:
   // 256 rows, 33 K candidates each, 1.57 -> 0.79 ms; 4096 rows with 8.7 K,
   // 0.16 ms at 256 threads against 0.37 ms at 1024)
-  if ((flags & kSelKeyed) || nq <= kSelFewRows) go(k_select<kSelThreadsWide, kSelPerWide>, kSelThreadsWide);
+  if ((flags & kSelIlv) || nq <= kSelFewRows) go(k_select<kSelThreadsWide, kSelPerWide>, kSelThreadsWide);
   else go(k_select<kSelThreads, kSelPer>, kSelThreads);
   return hipGetLastError();
 }

@@ -617,7 +617,7 @@ static void allow_lds(K kernel, size_t bytes) {
 }
 
 ScoreShape wide_shape(int dtype, int mode, int h, int d) {
-  ScoreShape s{0, 0, 0, 0, 0, 0};
+  ScoreShape s{0, 0, 0, 0, 0, 0, 0};
   with_wide(dtype, mode, h, d, [&]<class C>() {
     s.supported = 1;
     s.queries_per_block = C::QT;
@@ -625,6 +625,7 @@ ScoreShape wide_shape(int dtype, int mode, int h, int d) {
     s.threads = C::NTHREADS;
     s.scan_lds = C::Q_LDS + 16 + C::QT * 16;  // queries, key range, list tails, bins, bin maps
     s.shared_rows = 1;
+    s.arrival_order = 1;
   });
   return s;
 }

@@ -30,6 +30,7 @@ LT_SORTED_OUTPUT, LT_FORCE_FALLBACK = 1, 2
 LT_K_MAX = 8192
 LT_SAMPLE_LIST_MAX = 32768
 LT_UNION_MAX = 32768
+LT_ROW_STATS = 12
 LT_NUM_STAGE_EVENTS = 6
 STAGES = ("sample", "range", "filter", "select", "fallback")
 
@@ -234,7 +235,11 @@ def make_options(num_bins=None, sample_size=None, capacity=None, key_splits=None
     if stage_events is not None:
         o.stage_events = ctypes.cast(stage_events.array, ctypes.c_void_p)
     if row_stats is not None:
+        _on_gpu(row_stats)
+        _need(row_stats.dtype == torch.int32 and row_stats.dim() == 2 and row_stats.shape[1] == LT_ROW_STATS,
+              "row_stats must be an int32 [Nq, LT_ROW_STATS] GPU tensor")
         o.row_stats = row_stats.data_ptr()
+        o.row_stats_rows = row_stats.shape[0]
     if sample_keys is not None:
         _on_gpu(sample_keys)
         _need(sample_keys.dtype == torch.int32 and sample_keys.dim() == 1, "sample_keys must be int32 [n]")
@@ -276,6 +281,32 @@ class StageEvents:
                 self.array[i] = None
 
 
+def _check_rows(nq: int, causal_offsets: Optional[torch.Tensor], options: Optional[LtOptions]):
+    """Per-row arguments: causal_offsets int32 [Nq] on the GPU; the options'
+    row_stats (checked in make_options for its shape) must cover Nq rows."""
+    if causal_offsets is not None:
+        _on_gpu(causal_offsets)
+        _need(causal_offsets.dtype == torch.int32 and causal_offsets.numel() == nq,
+              "causal_offsets must be int32 [Nq]")
+    if options is not None and options.row_stats:
+        n = getattr(options, "row_stats_rows", None)
+        _need(n is not None and n >= nq, "row_stats must hold LT_ROW_STATS fields for each of the Nq rows "
+              "(pass it through make_options)")
+
+
+def _check_score_inputs(q, w, keys, causal_offsets, q_scale, k_scale, options):
+    nq, h, _ = q.shape
+    nk = keys.shape[0]
+    if w is not None:
+        _need(w.dtype == torch.float32 and tuple(w.shape) == (nq, h), "w must be float32 [Nq, H]")
+    if _dtype_code(q) == LT_FP8_E4M3FN:
+        _need(q_scale is not None and q_scale.dtype == torch.float32 and tuple(q_scale.shape) == (nq, h),
+              "fp8: q_scale must be float32 [Nq, H]")
+        _need(k_scale is not None and k_scale.dtype == torch.float32 and tuple(k_scale.shape) == (nk,),
+              "fp8: k_scale must be float32 [Nk]")
+    _check_rows(nq, causal_offsets, options)
+
+
 def _mode_code(mode: str) -> int:
     if mode == "dsa":
         return LT_SCORE_DSA
@@ -306,10 +337,7 @@ def indexer_topk(q: torch.Tensor, w: Optional[torch.Tensor], keys: torch.Tensor,
     _need(_dtype_code(keys) == dt, "q and keys must share a dtype")
     nq, h, d = q.shape
     nk = keys.shape[0]
-    if w is not None:
-        _need(w.dtype == torch.float32 and tuple(w.shape) == (nq, h), "w must be float32 [Nq, H]")
-    if causal_offsets is not None:
-        _need(causal_offsets.dtype == torch.int32 and causal_offsets.numel() == nq, "causal_offsets int32 [Nq]")
+    _check_score_inputs(q, w, keys, causal_offsets, q_scale, k_scale, options)
     if out is None:
         out = (torch.empty((nq, k), dtype=torch.int32, device=q.device),
                torch.empty((nq, k), dtype=torch.float32, device=q.device))
@@ -327,7 +355,10 @@ def indexer_scores(q: torch.Tensor, w: Optional[torch.Tensor], keys: torch.Tenso
                    mode: str = "dsa", out: Optional[torch.Tensor] = None, stream=None) -> torch.Tensor:
     """Dense float32 index scores [Nq, Nk] (the materialising baseline)."""
     _on_gpu(q, w, keys, q_scale, k_scale)
+    _need(q.dim() == 3 and keys.dim() == 2 and q.shape[2] == keys.shape[1], "q [Nq,H,d] and keys [Nk,d] required")
     dt = _dtype_code(q)
+    _need(_dtype_code(keys) == dt, "q and keys must share a dtype")
+    _check_score_inputs(q, w, keys, None, q_scale, k_scale, None)
     nq, h, d = q.shape
     nk = keys.shape[0]
     if out is None:
@@ -348,8 +379,7 @@ def topk_select(scores: torch.Tensor, k: int, num_keys: Optional[int] = None,
           "scores must be a float32 [Nq, ld] GPU matrix with unit column stride")
     nq = scores.shape[0]
     nk = scores.shape[1] if num_keys is None else num_keys
-    if causal_offsets is not None:
-        _on_gpu(causal_offsets)
+    _check_rows(nq, causal_offsets, options)
     if out is None:
         out = (torch.empty((nq, k), dtype=torch.int32, device=scores.device),
                torch.empty((nq, k), dtype=torch.float32, device=scores.device))
@@ -370,6 +400,7 @@ def topk_radix(scores: torch.Tensor, k: int, num_keys: Optional[int] = None,
           "scores must be a float32 [Nq, ld] GPU matrix with unit column stride")
     nq = scores.shape[0]
     nk = scores.shape[1] if num_keys is None else num_keys
+    _check_rows(nq, causal_offsets, None)
     if out is None:
         out = (torch.empty((nq, k), dtype=torch.int32, device=scores.device),
                torch.empty((nq, k), dtype=torch.float32, device=scores.device))

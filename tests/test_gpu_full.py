@@ -44,7 +44,7 @@ def test_full_size_parity(lib, name):
     x = workloads.generate(cfg, seed=workloads.CONFIG_SEEDS[name])
     d = to_dev(x)
     nq, nk, k = cfg.nq, cfg.nk, cfg.k
-    stats = torch.zeros((nq, 4), dtype=torch.int32, device="cuda")
+    stats = torch.zeros((nq, lt.LT_ROW_STATS), dtype=torch.int32, device="cuda")
     fi, fs = lt.indexer_topk(d["q"], d["w"], d["keys"], k, d["offsets"], d["q_scale"], d["k_scale"],
                              mode=cfg.mode, options=lt.make_options(row_stats=stats))
     dense = lt.indexer_scores(d["q"], d["w"], d["keys"], d["q_scale"], d["k_scale"], mode=cfg.mode)
@@ -82,7 +82,7 @@ def test_full_size_retrieval(lib):
     x = workloads.generate(cfg, seed=workloads.CONFIG_SEEDS[name])
     d = to_dev(x)
     nq, nk, k = cfg.nq, cfg.nk, cfg.k
-    stats = torch.zeros((nq, 4), dtype=torch.int32, device="cuda")
+    stats = torch.zeros((nq, lt.LT_ROW_STATS), dtype=torch.int32, device="cuda")
     fi, fs = lt.indexer_topk(d["q"], None, d["keys"], k, None, mode="ip", options=lt.make_options(row_stats=stats))
     torch.cuda.synchronize()
     gi, gs = _sorted_pairs(fi, fs)
@@ -129,7 +129,7 @@ def test_sample_scan_around_4gib_of_keys(lib, dtype, h, mode, over):
         qs = torch.rand((nq, h), device="cuda", generator=g) * 1e-2 + 1e-3
         ks = torch.rand((nk,), device="cuda", generator=g) * 1e-2 + 1e-3
     w = torch.rand((nq, h), device="cuda", generator=g) if mode == "dsa" else None
-    stats = torch.zeros((nq, 4), dtype=torch.int32, device="cuda")
+    stats = torch.zeros((nq, lt.LT_ROW_STATS), dtype=torch.int32, device="cuda")
     # a sample large enough for the range estimate to hold the top-k of 2^25
     # keys (the default 3k keys would put every top-k key in the clamped top
     # bin and send the rows to the fallback by design)
@@ -143,3 +143,128 @@ def test_sample_scan_around_4gib_of_keys(lib, dtype, h, mode, over):
     np.testing.assert_array_equal(gi, ri.cpu().numpy())
     np.testing.assert_array_equal(gs.view(np.uint32), rs.cpu().numpy().view(np.uint32))
     assert int((stats[:, 2] != 0).sum()) == 0, "rows took the fallback"
+
+
+def _dense_radix_check(d, mode, k, fi, fs, rows=None):
+    """Every row of the fused result equals radix selection over the dense
+    scores (same arithmetic), bit for bit after sorting both."""
+    q = d["q"] if rows is None else d["q"][rows].contiguous()
+    w = d["w"] if (rows is None or d["w"] is None) else d["w"][rows].contiguous()
+    qs = d["q_scale"] if (rows is None or d["q_scale"] is None) else d["q_scale"][rows].contiguous()
+    offs = d["offsets"] if (rows is None or d["offsets"] is None) else d["offsets"][rows].contiguous()
+    dense = lt.indexer_scores(q, w, d["keys"], qs, d["k_scale"], mode=mode)
+    ri, rs = lt.topk_radix(dense, k, causal_offsets=offs, sorted_output=True)
+    del dense
+    torch.cuda.synchronize()
+    gi, gs = _sorted_pairs(fi, fs)
+    np.testing.assert_array_equal(gi, ri.cpu().numpy(), err_msg="fused sets differ from radix over dense scores")
+    np.testing.assert_array_equal(gs.view(np.uint32), rs.cpu().numpy().view(np.uint32),
+                                  err_msg="fused scores differ from dense scores")
+
+
+def _oracle_rows(x, cfg, k, fi, fs, rows, xrows=None):
+    """Rows `rows` of the fused result against the CPU oracle (tolerance and
+    swap rule); xrows are the same rows' indices into x (default: rows)."""
+    xrows = rows if xrows is None else xrows
+    oi, os_, full = oracle_topk(x, cfg.dtype, k, cfg.mode, rows=xrows)
+    ev = visible(None if x["offsets"] is None else x["offsets"].numpy(), x["q"].shape[0], cfg.nk)
+    for j, (t, tx) in enumerate(zip(rows, xrows)):
+        check_row_tol(fi[t], fs[t], oi[j], os_[j], full[j], int(ev[tx]), k, RTOL[cfg.dtype])
+
+
+@pytest.mark.parametrize("opt,reason", [(dict(capacity=8192), 1), (dict(capacity=262144, num_bins=2), 2)],
+                         ids=["overflow", "tie-bin"])
+def test_fallback_at_full_size_adversarial(lib, opt, reason):
+    """The adversarial 1024 x 256K workload at full size, in two forms that
+    send rows to the exact fallback for real: candidate buffers below its
+    ~21K survivors per row (the capacity is per key split; the launch splits
+    the keys in two, ~10.6K survivors each; reason 1: buffer overflow), and
+    two bins with room for every key (reason 2: the threshold bin is too
+    large to sort).
+    Every row equals radix selection over the dense scores bit for bit;
+    evenly spaced rows meet the oracle."""
+    name = "adversarial_bf16_256k"
+    cfg = workloads.CONFIGS[name]
+    x = workloads.generate(cfg, seed=workloads.CONFIG_SEEDS[name])
+    d = to_dev(x)
+    k = cfg.k
+    stats = torch.zeros((cfg.nq, lt.LT_ROW_STATS), dtype=torch.int32, device="cuda")
+    fi, fs = lt.indexer_topk(d["q"], d["w"], d["keys"], k, d["offsets"], mode=cfg.mode,
+                             options=lt.make_options(row_stats=stats, **opt))
+    torch.cuda.synchronize()
+    st = stats.cpu().numpy()
+    n_fb = int((st[:, 2] == reason).sum())
+    print("%s: %d of %d rows took the fallback with reason %d" % (name, n_fb, cfg.nq, reason), flush=True)
+    assert n_fb >= cfg.nq // 4, "too few rows reached the fallback"
+    assert set(np.unique(st[:, 2]).tolist()) <= {0, reason}
+    _dense_radix_check(d, cfg.mode, k, fi, fs)
+    rows = sorted(set(np.linspace(0, cfg.nq - 1, 8).round().astype(int).tolist()))
+    _oracle_rows(x, cfg, k, fi.cpu().numpy(), fs.cpu().numpy(), rows)
+
+
+@pytest.fixture(scope="module")
+def fp8_1m_rows():
+    """64 evenly spaced rows of the 2048 x 1M fp8 workload (all 1M keys)."""
+    name = "dsa_fp8_1m"
+    cfg = workloads.CONFIGS[name]
+    x = workloads.generate(cfg, seed=workloads.CONFIG_SEEDS[name])
+    rows = np.linspace(0, cfg.nq - 1, 64).round().astype(np.int64)
+    xs = dict(x)
+    for key in ("q", "q_scale", "w", "offsets"):
+        xs[key] = x[key][torch.from_numpy(rows)].contiguous()
+    return cfg, x, xs, rows
+
+
+@pytest.mark.parametrize("opt,reason", [(dict(force_fallback=True), 3), (dict(num_bins=1), 1)],
+                         ids=["forced", "one-bin"])
+def test_fallback_at_full_size_fp8_1m(lib, fp8_1m_rows, opt, reason):
+    """64 rows of the 1M-context fp8 workload through the exact fallback at
+    full context: forced (reason 3), and one bin, where every key passes the
+    gate and the 24576-entry buffers overflow (reason 1). The fallback
+    re-scores each row's 1M keys into its scratch row and radix-selects it."""
+    cfg, x, xs, rows = fp8_1m_rows
+    d = to_dev(xs)
+    k = cfg.k
+    nq = len(rows)
+    stats = torch.zeros((nq, lt.LT_ROW_STATS), dtype=torch.int32, device="cuda")
+    fi, fs = lt.indexer_topk(d["q"], d["w"], d["keys"], k, d["offsets"], d["q_scale"], d["k_scale"],
+                             mode=cfg.mode, options=lt.make_options(row_stats=stats, **opt))
+    torch.cuda.synchronize()
+    st = stats.cpu().numpy()
+    assert np.all(st[:, 2] == reason), np.unique(st[:, 2])
+    _dense_radix_check(d, cfg.mode, k, fi, fs)
+    sel = list(range(0, nq, 8)) + [nq - 1]
+    _oracle_rows(x, cfg, k, fi.cpu().numpy(), fs.cpu().numpy(), sel, xrows=[int(rows[i]) for i in sel])
+
+
+# Every row of the 128K and 256K workloads against the oracle, in blocks of
+# rows (the fused call runs once per workload and is kept for its blocks).
+ALL_ROWS = {"dsa_bf16_128k": 256, "adversarial_bf16_256k": 128}
+
+
+@pytest.fixture(scope="module")
+def full_fused():
+    cache = {}
+
+    def get(name):
+        if name not in cache:
+            cache.clear()
+            cfg = workloads.CONFIGS[name]
+            x = workloads.generate(cfg, seed=workloads.CONFIG_SEEDS[name])
+            d = to_dev(x)
+            fi, fs = lt.indexer_topk(d["q"], d["w"], d["keys"], cfg.k, d["offsets"], d["q_scale"], d["k_scale"],
+                                     mode=cfg.mode)
+            torch.cuda.synchronize()
+            cache[name] = (cfg, x, fi.cpu().numpy(), fs.cpu().numpy())
+            del d
+        return cache[name]
+    return get
+
+
+@pytest.mark.parametrize("name,block", [(n, b) for n, rows in ALL_ROWS.items()
+                                        for b in range(workloads.CONFIGS[n].nq // rows)])
+def test_every_row_against_oracle(lib, full_fused, name, block):
+    cfg, x, fi, fs = full_fused(name)
+    per = ALL_ROWS[name]
+    rows = list(range(block * per, (block + 1) * per))
+    _oracle_rows(x, cfg, cfg.k, fi, fs, rows)

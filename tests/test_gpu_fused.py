@@ -23,7 +23,7 @@ pytestmark = pytest.mark.gpu
 def _fused(x, k, mode="dsa", **opt):
     d = to_dev(x)
     nq = d["q"].shape[0]
-    stats = torch.full((nq, 4), -7, dtype=torch.int32, device="cuda")
+    stats = torch.full((nq, lt.LT_ROW_STATS), -7, dtype=torch.int32, device="cuda")
     opts = lt.make_options(row_stats=stats, **opt)
     gi, gs = lt.indexer_topk(d["q"], d["w"], d["keys"], k, d["offsets"], d["q_scale"], d["k_scale"], mode=mode,
                              options=opts)

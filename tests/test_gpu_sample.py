@@ -155,7 +155,7 @@ def test_sample_list_keeps_fused_exact(lib, base):
     e = visible(None if x["offsets"] is None else x["offsets"].numpy(), cfg.nq, cfg.nk)
     for name, lst in _lists(rng, x, k, cfg.nk, ref_i).items():
         keys = torch.from_numpy(np.ascontiguousarray(lst, dtype=np.int32)).cuda()
-        stats = torch.zeros((cfg.nq, 4), dtype=torch.int32, device="cuda")
+        stats = torch.zeros((cfg.nq, lt.LT_ROW_STATS), dtype=torch.int32, device="cuda")
         gi, gs = lt.indexer_topk(d["q"], d["w"], d["keys"], k, d["offsets"], d["q_scale"], d["k_scale"],
                                  mode=cfg.mode,
                                  options=lt.make_options(sorted_output=True, sample_keys=keys, row_stats=stats))
@@ -200,12 +200,12 @@ def test_chunked_prefill_with_previous_chunk_sample(lib):
     for c0 in range(0, cfg.nq, chunk):
         sl = slice(c0, c0 + chunk)
         q, w, offs = d["q"][sl].contiguous(), d["w"][sl].contiguous(), d["offsets"][sl].contiguous()
-        st_r = torch.zeros((chunk, 4), dtype=torch.int32, device="cuda")
+        st_r = torch.zeros((chunk, lt.LT_ROW_STATS), dtype=torch.int32, device="cuda")
         ri, rs = lt.indexer_topk(q, w, d["keys"], k, offs, options=lt.make_options(sorted_output=True, row_stats=st_r))
         np.testing.assert_array_equal(ri.cpu().numpy(), ref_i[sl].cpu().numpy())
         if prev is not None:
             hint = lt.sample_from_topk(prev, cfg.nk, 3 * k)
-            st_h = torch.zeros((chunk, 4), dtype=torch.int32, device="cuda")
+            st_h = torch.zeros((chunk, lt.LT_ROW_STATS), dtype=torch.int32, device="cuda")
             hi, hs = lt.indexer_topk(q, w, d["keys"], k, offs,
                                      options=lt.make_options(sorted_output=True, sample_keys=hint, row_stats=st_h))
             torch.cuda.synchronize()

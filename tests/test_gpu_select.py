@@ -33,7 +33,7 @@ def _run(scores, nk, k, offs, entry, **opt):
     o = None if offs is None else torch.from_numpy(offs).to(dev)
     sorted_out = opt.pop("sorted_output", False)
     if entry == "select":
-        stats = torch.full((scores.shape[0], 4), -7, dtype=torch.int32, device=dev)
+        stats = torch.full((scores.shape[0], lt.LT_ROW_STATS), -7, dtype=torch.int32, device=dev)
         opts = lt.make_options(sorted_output=sorted_out, row_stats=stats, **opt)
         gi, gs = lt.topk_select(s, k, num_keys=nk, causal_offsets=o, options=opts)
     else:

@@ -35,7 +35,7 @@ E7 = workloads.CONFIGS["retrieval_e7_bf16_5m"]
 def _fused(x, k, mode="ip", **opt):
     d = to_dev(x)
     nq = d["q"].shape[0]
-    stats = torch.full((nq, 4), -7, dtype=torch.int32, device="cuda")
+    stats = torch.full((nq, lt.LT_ROW_STATS), -7, dtype=torch.int32, device="cuda")
     gi, gs = lt.indexer_topk(d["q"], d["w"], d["keys"], k, d["offsets"], None, None, mode=mode,
                              options=lt.make_options(row_stats=stats, **opt))
     torch.cuda.synchronize()
@@ -217,7 +217,7 @@ def _oracle_rows_chunked(q_bits, keys_dev, rows, k, chunk=1 << 19):
 def test_wide_full_size(lib, k):
     x = workloads.unit_corpus_gpu(E7, seed=workloads.CONFIG_SEEDS[E7.name], device="cuda")
     nq, nk = E7.nq, E7.nk
-    stats = torch.zeros((nq, 4), dtype=torch.int32, device="cuda")
+    stats = torch.zeros((nq, lt.LT_ROW_STATS), dtype=torch.int32, device="cuda")
     fi, fs = lt.indexer_topk(x["q"], None, x["keys"], k, None, mode="ip", options=lt.make_options(row_stats=stats))
     dense = lt.indexer_scores(x["q"], None, x["keys"], mode="ip")
     ri, rs = lt.topk_radix(dense, k, sorted_output=True)
