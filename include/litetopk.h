@@ -53,12 +53,15 @@ extern "C" {
 #define LT_EUNSUPPORTED (-2)  /* (dtype, heads, head_dim) not built, or k > LT_K_MAX */
 #define LT_EWORKSPACE (-3)    /* workspace smaller than the *_workspace_size value */
 #define LT_EHIP (-4)          /* a HIP launch or event call failed                 */
+#define LT_ESCRATCH (-5)      /* lt_indexer_topk_static: the shape needs more workspace
+                                 than LT_STATIC_SCRATCH_BYTES                      */
 
 #define LT_K_MAX 8192         /* largest k (the paper's largest, sec. 4.1 retrieval) */
 #define LT_MAX_BINS 256
 #define LT_SAMPLE_LIST_MAX 32768  /* longest caller-supplied sample list */
 #define LT_UNION_MAX 32768        /* largest group * k for lt_dsa_union */
 #define LT_ROW_STATS 12           /* int32 fields per row of lt_options.row_stats */
+#define LT_STATIC_SCRATCH_BYTES (256u << 20)  /* workspace of lt_indexer_topk_static, per GPU */
 
 /* ---- enums --------------------------------------------------------------- */
 typedef enum {
@@ -194,6 +197,27 @@ int lt_indexer_topk(const void* q, const float* q_scale, const float* w, const v
                     int32_t num_keys, int32_t num_heads, int32_t head_dim, int32_t k,
                     const int32_t* causal_offsets, int32_t* out_idx, float* out_scores,
                     void* workspace, size_t workspace_bytes, const lt_options* opts, void* stream);
+
+/* For callers that cannot allocate device memory (code under HIP graph
+   capture, tight serving loops, harnesses that forbid hipMalloc): the same
+   operation, arguments and results as lt_indexer_topk, with the workspace
+   taken from a static device array of LT_STATIC_SCRATCH_BYTES that the library
+   holds on every GPU it runs on until the process ends. The call allocates
+   nothing. It uses the array of the device current on the calling thread
+   (the stream must belong to that device); its address is looked up on the
+   first call made on each device.
+   Returns LT_ESCRATCH, before any device work, when
+   lt_indexer_topk_workspace_size(...) of the shape exceeds
+   LT_STATIC_SCRATCH_BYTES, and the argument errors of lt_indexer_topk.
+   Every call on one GPU shares that GPU's array: calls whose work overlaps
+   (on different streams, or from different threads without ordering) race
+   and give undefined results. Calls ordered on one stream are safe; each
+   call initialises what it reads from the array. */
+int lt_indexer_topk_static(const void* q, const float* q_scale, const float* w, const void* keys,
+                           const float* k_scale, lt_dtype dtype, lt_score_mode mode, int32_t num_queries,
+                           int32_t num_keys, int32_t num_heads, int32_t head_dim, int32_t k,
+                           const int32_t* causal_offsets, int32_t* out_idx, float* out_scores,
+                           const lt_options* opts, void* stream);
 
 /* ---- dense scores (the decoupled baseline's score stage, sec. 1) --------- */
 

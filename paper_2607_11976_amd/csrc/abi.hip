@@ -3,11 +3,18 @@
 #include <string.h>
 
 #include <algorithm>
+#include <mutex>
 
 #include "internal.hpp"
 #include "select_dev.hpp"
 
 using namespace lt;
+
+// Workspace of lt_indexer_topk_static: one copy per GPU, held until the
+// process ends. In host code `scratch` names a host-side stand-in, never the
+// device memory: host code uses only the address hipGetSymbolAddress returns
+// for the current device (static_scratch below).
+static __device__ __align__(256) uint8_t scratch[LT_STATIC_SCRATCH_BYTES];
 
 namespace {
 
@@ -202,6 +209,26 @@ int check_score_args(const void* q, const float* q_scale, const void* keys, cons
   return LT_OK;
 }
 
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices];  // device address of `scratch`, per device
+
+// This device's copy of `scratch`: looked up once per device, with that
+// device current, on the first call made there.
+int static_scratch(void** out) {
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess) return LT_EHIP;
+  if (dev < 0 || dev >= kMaxDevices) return LT_EUNSUPPORTED;
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void* p = nullptr;
+    if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess || !p) return LT_EHIP;
+    g_scratch_ptr[dev] = p;
+  }
+  *out = g_scratch_ptr[dev];
+  return LT_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -228,6 +255,7 @@ const char* lt_strerror(int status) {
     case LT_EUNSUPPORTED: return "unsupported (dtype, heads, head_dim, mode) or k";
     case LT_EWORKSPACE: return "workspace too small";
     case LT_EHIP: return "HIP runtime error";
+    case LT_ESCRATCH: return "shape needs more workspace than the static scratch (LT_STATIC_SCRATCH_BYTES)";
     default: return "unknown status";
   }
 }
@@ -299,6 +327,24 @@ int lt_indexer_topk(const void* q, const float* q_scale, const float* w, const v
     return hip_status(e);
   record(r, LT_NUM_STAGE_EVENTS - 1, st);
   return LT_OK;
+}
+
+int lt_indexer_topk_static(const void* q, const float* q_scale, const float* w, const void* keys,
+                           const float* k_scale, lt_dtype dtype, lt_score_mode mode, int32_t nq, int32_t nk,
+                           int32_t h, int32_t d, int32_t k, const int32_t* offs, int32_t* out_idx,
+                           float* out_scores, const lt_options* opts, void* stream) {
+  int rc = check_score_args(q, q_scale, keys, k_scale, dtype, mode, nq, nk, h, d);
+  if (rc) return rc;
+  if (k < 1) return LT_EINVAL;
+  if (k > LT_K_MAX) return LT_EUNSUPPORTED;
+  if (nq == 0) return LT_OK;
+  const size_t need = lt_indexer_topk_workspace_size(nq, nk, h, d, dtype, mode, k, opts);
+  if (need == 0) return LT_EINVAL;
+  if (need > (size_t)LT_STATIC_SCRATCH_BYTES) return LT_ESCRATCH;
+  void* ws = nullptr;
+  if ((rc = static_scratch(&ws)) != LT_OK) return rc;
+  return lt_indexer_topk(q, q_scale, w, keys, k_scale, dtype, mode, nq, nk, h, d, k, offs, out_idx, out_scores, ws,
+                         (size_t)LT_STATIC_SCRATCH_BYTES, opts, stream);
 }
 
 int lt_indexer_scores(const void* q, const float* q_scale, const float* w, const void* keys,

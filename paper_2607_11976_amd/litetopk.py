@@ -23,7 +23,7 @@ import torch
 _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "liblitetopk.so")
 
-LT_OK, LT_EINVAL, LT_EUNSUPPORTED, LT_EWORKSPACE, LT_EHIP = 0, -1, -2, -3, -4
+LT_OK, LT_EINVAL, LT_EUNSUPPORTED, LT_EWORKSPACE, LT_EHIP, LT_ESCRATCH = 0, -1, -2, -3, -4, -5
 LT_F32, LT_BF16, LT_FP8_E4M3FN = 0, 1, 2
 LT_SCORE_DSA, LT_SCORE_IP = 0, 1
 LT_SORTED_OUTPUT, LT_FORCE_FALLBACK = 1, 2
@@ -31,11 +31,13 @@ LT_K_MAX = 8192
 LT_SAMPLE_LIST_MAX = 32768
 LT_UNION_MAX = 32768
 LT_ROW_STATS = 12
+LT_STATIC_SCRATCH_BYTES = 256 << 20
 LT_NUM_STAGE_EVENTS = 6
 STAGES = ("sample", "range", "filter", "select", "fallback")
 
 EXPORTED = (
-    "lt_options_default", "lt_indexer_topk_workspace_size", "lt_indexer_topk", "lt_indexer_scores",
+    "lt_options_default", "lt_indexer_topk_workspace_size", "lt_indexer_topk", "lt_indexer_topk_static",
+    "lt_indexer_scores",
     "lt_topk_select_workspace_size", "lt_topk_select", "lt_topk_radix",
     "lt_sample_from_topk_workspace_size", "lt_sample_from_topk", "lt_dsa_union", "lt_event_create",
     "lt_event_destroy", "lt_event_record", "lt_event_elapsed_ms", "lt_strerror",
@@ -84,6 +86,9 @@ def load(path: str = LIB_PATH):
     lib.lt_indexer_topk.argtypes = [_P, _P, _P, _P, _P, ctypes.c_int, ctypes.c_int, _I32, _I32, _I32, _I32, _I32,
                                     _P, _P, _P, _P, _SZ, ctypes.POINTER(LtOptions), _P]
     lib.lt_indexer_topk.restype = ctypes.c_int
+    lib.lt_indexer_topk_static.argtypes = [_P, _P, _P, _P, _P, ctypes.c_int, ctypes.c_int, _I32, _I32, _I32, _I32,
+                                           _I32, _P, _P, _P, ctypes.POINTER(LtOptions), _P]
+    lib.lt_indexer_topk_static.restype = ctypes.c_int
     lib.lt_indexer_scores.argtypes = [_P, _P, _P, _P, _P, ctypes.c_int, ctypes.c_int, _I32, _I32, _I32, _I32,
                                       _P, _I64, _P]
     lib.lt_indexer_scores.restype = ctypes.c_int
@@ -139,6 +144,13 @@ def lt_indexer_topk(q, q_scale, w, keys, k_scale, dtype, mode, nq, nk, h, d, k, 
     return load().lt_indexer_topk(q, q_scale, w, keys, k_scale, dtype, mode, nq, nk, h, d, k, causal_offsets,
                                   out_idx, out_scores, workspace, workspace_bytes,
                                   ctypes.byref(opts) if opts is not None else None, stream)
+
+
+def lt_indexer_topk_static(q, q_scale, w, keys, k_scale, dtype, mode, nq, nk, h, d, k, causal_offsets, out_idx,
+                           out_scores, opts, stream) -> int:
+    return load().lt_indexer_topk_static(q, q_scale, w, keys, k_scale, dtype, mode, nq, nk, h, d, k,
+                                         causal_offsets, out_idx, out_scores,
+                                         ctypes.byref(opts) if opts is not None else None, stream)
 
 
 def lt_indexer_scores(q, q_scale, w, keys, k_scale, dtype, mode, nq, nk, h, d, scores, ld, stream) -> int:
@@ -347,6 +359,33 @@ def indexer_topk(q: torch.Tensor, w: Optional[torch.Tensor], keys: torch.Tensor,
                          h, d, k, _ptr(causal_offsets), _ptr(out[0]), _ptr(out[1]), _ptr(workspace),
                          workspace.numel(), options, _stream(stream))
     _check(st, "lt_indexer_topk")
+    return out
+
+
+def indexer_topk_static(q: torch.Tensor, w: Optional[torch.Tensor], keys: torch.Tensor, k: int,
+                        causal_offsets: Optional[torch.Tensor] = None, q_scale: Optional[torch.Tensor] = None,
+                        k_scale: Optional[torch.Tensor] = None, mode: str = "dsa",
+                        options: Optional[LtOptions] = None, out=None, stream=None):
+    """indexer_topk with the library's static per-GPU workspace
+    (lt_indexer_topk_static): the call allocates no device memory when `out`
+    is given. Calls whose work overlaps on one GPU race."""
+    _on_gpu(q, w, keys, causal_offsets, q_scale, k_scale)
+    _need(q.dim() == 3 and keys.dim() == 2 and q.shape[2] == keys.shape[1], "q [Nq,H,d] and keys [Nk,d] required")
+    dt = _dtype_code(q)
+    _need(_dtype_code(keys) == dt, "q and keys must share a dtype")
+    nq, h, d = q.shape
+    nk = keys.shape[0]
+    _check_score_inputs(q, w, keys, causal_offsets, q_scale, k_scale, options)
+    if out is None:
+        out = (torch.empty((nq, k), dtype=torch.int32, device=q.device),
+               torch.empty((nq, k), dtype=torch.float32, device=q.device))
+    _on_gpu(*out)
+    _need(tuple(out[0].shape) == (nq, k) and out[0].dtype == torch.int32 and tuple(out[1].shape) == (nq, k)
+          and out[1].dtype == torch.float32, "out must be (int32 [Nq, k], float32 [Nq, k])")
+    st = lt_indexer_topk_static(_ptr(q), _ptr(q_scale), _ptr(w), _ptr(keys), _ptr(k_scale), dt, _mode_code(mode), nq,
+                                nk, h, d, k, _ptr(causal_offsets), _ptr(out[0]), _ptr(out[1]), options,
+                                _stream(stream))
+    _check(st, "lt_indexer_topk_static")
     return out
 
 

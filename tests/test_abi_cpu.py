@@ -141,6 +141,19 @@ def test_argument_checks_reject_before_any_device_work(lib):
     assert lt.lt_dsa_union(P, 8, 4, 8, 0, P, P, P, None) == lt.LT_EINVAL
     assert lt.lt_dsa_union(P, 8, 4, 8, 2, P, None, P, None) == lt.LT_EINVAL
     assert lt.lt_dsa_union(None, 8, 0, 8, 2, None, None, None, None) == lt.LT_OK
+    # the static-scratch variant: argument errors as lt_indexer_topk, and a
+    # shape whose workspace exceeds the static array is refused on the host
+    assert lt.lt_indexer_topk_static(None, None, None, P, None, lt.LT_F32, lt.LT_SCORE_DSA, 4, 8, 4, 64, 2, None,
+                                     P, P, None, None) == lt.LT_EINVAL
+    assert lt.lt_indexer_topk_static(P, None, None, P, None, lt.LT_F32, lt.LT_SCORE_DSA, 4, 8, 3, 64, 2, None,
+                                     P, P, None, None) == lt.LT_EUNSUPPORTED
+    need = lt.lt_indexer_topk_workspace_size(4096, 131072, 64, 128, lt.LT_BF16, lt.LT_SCORE_DSA, 2048)
+    assert need > lt.LT_STATIC_SCRATCH_BYTES
+    assert lt.lt_indexer_topk_static(P, None, P, P, None, lt.LT_BF16, lt.LT_SCORE_DSA, 4096, 131072, 64, 128, 2048,
+                                     None, P, P, None, None) == lt.LT_ESCRATCH
+    assert "static scratch" in lt.lt_strerror(lt.LT_ESCRATCH)
+    assert lt.lt_indexer_topk_static(None, None, None, None, None, lt.LT_F32, lt.LT_SCORE_DSA, 0, 0, 4, 64, 2, None,
+                                     None, None, None, None) == lt.LT_OK
     # empty problems are valid and do nothing
     assert lt.lt_indexer_topk(None, None, None, None, None, lt.LT_F32, lt.LT_SCORE_DSA, 0, 0, 4, 64, 2, None,
                               None, None, None, 0, None, None) == lt.LT_OK
