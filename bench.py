@@ -16,10 +16,12 @@ fallback, inputs resident in HBM. Prints ONE JSON line with
   ctx_1m         the same measurement for the 2048 x 1M fp8 workload;
   dsa_union      LiteDSA's group union + membership masks (sec. 3.3) of the
                  timed workload's top-k lists, groups of 4 / 8 / 16 queries;
-  chunked_prefill  the same 4096 queries processed in chunks (sec. 4.2's
-                 chunked-prefill protocol), with a random sample per chunk and
-                 with the sample taken from the previous chunk's top-k
-                 (sec. 3.2 "Sampling"), total time over all chunks.
+  chunked_prefill  the paper's kernel benchmark protocol (sec. 4.1, 4.2):
+                 8192 query tokens at the end of a 256K (bf16) and a 1M (fp8)
+                 context, in chunks of 128 to 8192 queries, with a random
+                 sample per chunk and with the sample taken from the previous
+                 chunk's top-k (sec. 3.2 "Sampling"); total time over all
+                 chunks, stage times, survivors.
   other_configs  the remaining synthetic workloads, one short measurement
                  each: the 64 x 4096 fp32 case, the 10000 x 4M one-head
                  inner-product retrieval (k = 100) and the 1024 x 256K
@@ -61,7 +63,7 @@ HBM_PEAK_GBS = 8000.0
 # (`bench.py --copy-calib 1024 --steps 3`): FETCH_SIZE reads half the bytes,
 # WRITE_SIZE all of them. A kernel change since these were taken makes them
 # stale: set the entry to None until they are taken again.
-TRAFFIC_KIB = {"dsa_bf16_128k": (293568.2, 281895.8), "dsa_fp8_1m": (549560.8, 209531.3),
+TRAFFIC_KIB = {"dsa_bf16_128k": (293568.2, 281895.8), "dsa_fp8_1m": None,
                "retrieval_e7_bf16_5m": (3780593.9, 36472.1), "retrieval_bf16_4m": (2587643.2, 318512.4),
                "adversarial_bf16_256k": (149156.7, 172718.2)}
 COPY_FACTOR = (0.5000, 1.0000)
@@ -96,7 +98,12 @@ def step_summary(res) -> dict:
     return out
 
 
-def measure(name: str, steps: int, warmup: int, unfused: bool, cold: int = 5):
+def measure(name: str, steps: int, warmup: int, unfused: bool, cold: int = 5, sorted_reps: int = 0,
+            extra: dict = None):
+    """Timed lt_indexer_topk calls of one workload (options `extra` on top of
+    the defaults), with per-stage device times, cold-cache calls, row
+    statistics, and optionally the unfused baseline and sorted-output calls."""
+    extra = extra or {}
     cfg = workloads.CONFIGS[name]
     x = workloads.generate(cfg, seed=workloads.CONFIG_SEEDS[name])
     dev = torch.device("cuda")
@@ -112,7 +119,7 @@ def measure(name: str, steps: int, warmup: int, unfused: bool, cold: int = 5):
     out = (torch.empty((nq, k), dtype=torch.int32, device=dev), torch.empty((nq, k), dtype=torch.float32, device=dev))
     # one set of stage events per timed step, read after the timed region
     evs = [lt.StageEvents() for _ in range(steps)]
-    optss = [lt.make_options(stage_events=e) for e in evs]
+    optss = [lt.make_options(stage_events=e, **extra) for e in evs]
     ws = lt.indexer_topk_workspace(nq, nk, cfg.h, cfg.d, dt, cfg.mode, k, optss[0], dev)
 
     def step(i):
@@ -141,7 +148,7 @@ def measure(name: str, steps: int, warmup: int, unfused: bool, cold: int = 5):
     # inputs are no longer in the L2s or the 256 MB Infinity Cache
     flush = torch.empty(512 << 20, dtype=torch.uint8, device=dev)
     cold_ms = []
-    opt_plain = lt.make_options()
+    opt_plain = lt.make_options(**extra)
     for i in range(cold):
         flush.fill_(i & 0xFF)
         e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
@@ -154,13 +161,20 @@ def measure(name: str, steps: int, warmup: int, unfused: bool, cold: int = 5):
 
     # survivors and fallback rows (untimed call with row statistics)
     stats = torch.zeros((nq, lt.LT_ROW_STATS), dtype=torch.int32, device=dev)
-    lt.indexer_topk(q, w, keys, k, offs, qs, ks, mode=cfg.mode, options=lt.make_options(row_stats=stats),
+    lt.indexer_topk(q, w, keys, k, offs, qs, ks, mode=cfg.mode, options=lt.make_options(row_stats=stats, **extra),
                     out=out, workspace=ws)
     st = stats.cpu().numpy()
     res = dict(ms=ms, pairs=pairs, stages=stages, call_ms=call_ms, cold_ms=cold_ms,
                survivors_mean=float(st[:, 0].mean()),
                survivors_max=int(st[:, 0].max()), fallback_rows=int((st[:, 2] != 0).sum()),
-               tie_bin_mean=float(st[:, 3].mean()))
+               tie_bin_mean=float(st[:, 3].mean()),
+               fallback_reasons={int(r_): int((st[:, 2] == r_).sum()) for r_ in np.unique(st[:, 2]) if r_ != 0})
+    if sorted_reps:
+        # the same call with every row sorted by the total order
+        opt_s = lt.make_options(sorted_output=True, **extra)
+        res["sorted_ms"] = timed_steps(lambda: lt.indexer_topk(q, w, keys, k, offs, qs, ks, mode=cfg.mode,
+                                                               options=opt_s, out=out, workspace=ws),
+                                       sorted_reps, 1)
 
     # LiteDSA union of the top-k lists over groups of neighbouring queries
     # (sec. 3.3): time per call and union size relative to group * k
@@ -194,57 +208,90 @@ def measure(name: str, steps: int, warmup: int, unfused: bool, cold: int = 5):
     return cfg, res
 
 
-def chunked_prefill(name: str, chunk: int, reps: int):
-    """All queries of `name` in chunks of `chunk` rows over the same keys;
-    'random' samples every chunk at random, 'previous' takes each chunk's
-    sample from the previous chunk's output (lt_sample_from_topk, included in
-    the time). Returns total milliseconds over the chunks (mean of reps) and
-    mean survivors per row."""
-    cfg = workloads.CONFIGS[name]
-    x = workloads.generate(cfg, seed=workloads.CONFIG_SEEDS[name])
+# sec. 4.1 "Sparse-Attention Kernel Benchmark": the latency of the kernel
+# summed over 8192 query tokens of a prefill split into chunks, at 256K and
+# 1M context; chunk sizes 128 to 8192 (sec. 4.2). The paper's own figures
+# (B200, chunk 8192, k = 2048): 12.6 ms at 256K and 41.9 ms at 1M.
+CHUNK_TOKENS = 8192
+CHUNK_SIZES = (128, 512, 1024, 2048, 8192)
+CHUNK_CONTEXTS = (("dsa_bf16_128k", 262144, "dsa_bf16_256k"), ("dsa_fp8_1m", 1048576, "dsa_fp8_1m"))
+PAPER_CHUNKED_MS = {262144: 12.6, 1048576: 41.9}
+
+
+def chunked_prefill(base: str, ctx: int, label: str, sizes=CHUNK_SIZES, reps: int = 3):
+    """The last CHUNK_TOKENS tokens of a context of `ctx` keys, as queries
+    (query t sees keys [0, ctx - CHUNK_TOKENS + t + 1)), processed in chunks
+    of each size in `sizes`. 'random': every chunk draws its own random
+    sample; 'previous': every chunk after the first takes its sample from the
+    previous chunk's top-k (lt_sample_from_topk, its time included). Per
+    chunk size: total time over the chunks (wall clock around the whole
+    sequence of calls, mean of `reps`), the summed device time of each stage,
+    survivors per row and fallback rows."""
+    cfg = workloads.scaled(workloads.CONFIGS[base], nq=CHUNK_TOKENS, nk=ctx)
+    x = workloads.generate(cfg, seed=workloads.CONFIG_SEEDS[base])
     dev = torch.device("cuda")
     d = {kk: (None if v is None else v.to(dev)) for kk, v in x.items()
          if kk in ("q", "w", "keys", "q_scale", "k_scale", "offsets")}
     del x
-    nq, nk, k = cfg.nq, cfg.nk, cfg.k
+    nk, k = cfg.nk, cfg.k
     ns = 3 * k
-    starts = list(range(0, nq, chunk))
-    parts = [{kk: (None if d[kk] is None else d[kk][c0:c0 + chunk].contiguous())
-              for kk in ("q", "w", "q_scale", "offsets")} for c0 in starts]
-    outs = [(torch.empty((p["q"].shape[0], k), dtype=torch.int32, device=dev),
-             torch.empty((p["q"].shape[0], k), dtype=torch.float32, device=dev)) for p in parts]
-    hints = [torch.empty(ns, dtype=torch.int32, device=dev) for _ in parts]
-    hws = torch.empty(lt.lt_sample_from_topk_workspace_size(nk), dtype=torch.uint8, device=dev)
+    pairs = visible_pairs(cfg)
     dt = lt._dtype_code(d["q"])
-    opt_r = lt.make_options()
-    ws = lt.indexer_topk_workspace(chunk, nk, cfg.h, cfg.d, dt, cfg.mode, k, opt_r, dev)
-    opt_h = [lt.make_options(sample_keys=h) for h in hints]
-    ws_h = lt.indexer_topk_workspace(chunk, nk, cfg.h, cfg.d, dt, cfg.mode, k, opt_h[0], dev)
+    hws = torch.empty(lt.lt_sample_from_topk_workspace_size(nk), dtype=torch.uint8, device=dev)
+    runs = []
+    for chunk in sizes:
+        starts = list(range(0, cfg.nq, chunk))
+        parts = [{kk: (None if d[kk] is None else d[kk][c0:c0 + chunk].contiguous())
+                  for kk in ("q", "w", "q_scale", "offsets")} for c0 in starts]
+        outs = [(torch.empty((p["q"].shape[0], k), dtype=torch.int32, device=dev),
+                 torch.empty((p["q"].shape[0], k), dtype=torch.float32, device=dev)) for p in parts]
+        hints = [torch.empty(ns, dtype=torch.int32, device=dev) for _ in parts]
+        ws = lt.indexer_topk_workspace(chunk, nk, cfg.h, cfg.d, dt, cfg.mode, k, lt.make_options(), dev)
+        ws_h = lt.indexer_topk_workspace(chunk, nk, cfg.h, cfg.d, dt, cfg.mode, k,
+                                         lt.make_options(sample_keys=hints[0]), dev)
 
-    def run(previous, stats=None):
-        for j, p in enumerate(parts):
-            o = opt_r if (not previous or j == 0) else opt_h[j - 1]
-            if stats is not None:
-                o = lt.make_options(row_stats=stats[j], sample_keys=hints[j - 1] if (previous and j) else None)
-            lt.indexer_topk(p["q"], p["w"], d["keys"], k, p["offsets"], p["q_scale"], d["k_scale"], mode=cfg.mode,
-                            options=o, out=outs[j], workspace=ws_h if (previous and j) else ws)
-            if previous and j + 1 < len(parts):
-                lt.sample_from_topk(outs[j][0], nk, ns, out=hints[j], workspace=hws)
+        def run(previous, extra=None):
+            for j, p in enumerate(parts):
+                hint = hints[j - 1] if (previous and j) else None
+                kw = {} if extra is None else extra(j)
+                o = lt.make_options(sample_keys=hint, **kw)
+                lt.indexer_topk(p["q"], p["w"], d["keys"], k, p["offsets"], p["q_scale"], d["k_scale"],
+                                mode=cfg.mode, options=o, out=outs[j], workspace=ws_h if hint is not None else ws)
+                if previous and j + 1 < len(parts):
+                    lt.sample_from_topk(outs[j][0], nk, ns, out=hints[j], workspace=hws)
 
-    res = {"workload": name, "chunk": chunk, "chunks": len(parts), "sample_size": ns}
-    for mode in ("random", "previous"):
-        res[mode + "_ms"] = round(timed_steps(lambda: run(mode == "previous"), reps, 1), 4)
-        st = [torch.zeros((p["q"].shape[0], lt.LT_ROW_STATS), dtype=torch.int32, device=dev) for p in parts]
-        run(mode == "previous", st)
-        sv = torch.cat(st).cpu().numpy()
-        res[mode + "_survivors_per_row"] = round(float(sv[:, 0].mean()), 1)
-        res[mode + "_fallback_rows"] = int((sv[:, 2] != 0).sum())
-    # the previous-chunk sampler alone
-    res["sample_from_topk_ms"] = round(timed_steps(
-        lambda: lt.sample_from_topk(outs[0][0], nk, ns, out=hints[0], workspace=hws), 5, 1), 4)
-    del d, parts, outs, ws, ws_h
+        r = {"chunk": chunk, "chunks": len(parts)}
+        for mode in ("random", "previous"):
+            prev = mode == "previous"
+            ms = timed_steps(lambda: run(prev), reps, 1)
+            evs = [lt.StageEvents() for _ in parts]
+            run(prev, lambda j: {"stage_events": evs[j]})
+            stg = {s_: 0.0 for s_ in lt.STAGES}
+            for e in evs:
+                for s_, v in e.stage_ms().items():
+                    stg[s_] += v
+                e.close()
+            st = [torch.zeros((p["q"].shape[0], lt.LT_ROW_STATS), dtype=torch.int32, device=dev) for p in parts]
+            run(prev, lambda j: {"row_stats": st[j]})
+            sv = torch.cat(st).cpu().numpy()
+            r[mode] = {"total_ms": round(ms, 4), "pairs_per_s": pairs / (ms * 1e-3),
+                       "stages_ms": {s_: round(v, 4) for s_, v in stg.items()},
+                       "survivors_per_row": round(float(sv[:, 0].mean()), 1),
+                       "fallback_rows": int((sv[:, 2] != 0).sum())}
+        if len(parts) > 1:
+            r["sample_from_topk_ms_each"] = round(timed_steps(
+                lambda: lt.sample_from_topk(outs[0][0], nk, ns, out=hints[0], workspace=hws), 5, 1), 4)
+        runs.append(r)
+        print("[bench] chunked %s chunk %d: random %.2f ms, previous %.2f ms (survivors %.0f / %.0f)" % (
+            label, chunk, r["random"]["total_ms"], r["previous"]["total_ms"], r["random"]["survivors_per_row"],
+            r["previous"]["survivors_per_row"]), file=sys.stderr, flush=True)
+        del parts, outs, hints, ws, ws_h
+        torch.cuda.empty_cache()
+    del d, hws
     torch.cuda.empty_cache()
-    return res
+    return {"workload": label, "dtype": cfg.dtype, "context": nk, "query_tokens": cfg.nq, "k": k,
+            "heads": cfg.h, "head_dim": cfg.d, "visible_pairs": pairs, "sample_size": ns,
+            "paper_b200_ms_chunk8192": PAPER_CHUNKED_MS.get(nk), "runs": runs}
 
 
 def retrieval_sweep(steps: int):
@@ -310,7 +357,8 @@ def retrieval_sweep(steps: int):
     del x, q, keys, qt
     torch.cuda.empty_cache()
     ref = [p for p in points if p["corpus"] == 5000000 and p["k"] == 1024][0]
-    kib = TRAFFIC_KIB.get(cfg.name)
+    # counter traffic was taken with the default options only
+    kib = None if extra else TRAFFIC_KIB.get(cfg.name)
     traffic = None if kib is None else round(kib[0] * 1024.0 / COPY_FACTOR[0] + kib[1] * 1024.0 / COPY_FACTOR[1])
     return {"workload": cfg.name, "num_queries": cfg.nq, "dim": cfg.d, "dtype": "bf16", "mode": "ip",
             "data": "synthetic unit-normalised Gaussian passages (torch Philox, seeded); queries are corpus passages",
@@ -321,34 +369,61 @@ def retrieval_sweep(steps: int):
             "points": points}
 
 
-def roofline(cfg, res):
+def algorithmic_bytes(cfg, survivors_mean: float) -> int:
+    """HBM bytes one fused scan must move: the keys (and their scales), the
+    queries, head weights and scales once, and the candidates it writes
+    (8 B each)."""
+    es = {"bf16": 2, "fp8": 1, "f32": 4}[cfg.dtype]
+    b = cfg.nk * cfg.d * es + cfg.nq * cfg.h * cfg.d * es + cfg.nq * cfg.h * 4 + cfg.nq * 4
+    if cfg.dtype == "fp8":
+        b += cfg.nk * 4 + cfg.nq * cfg.h * 4
+    return int(b + survivors_mean * cfg.nq * 8)
+
+
+def roofline(cfg, res, extra=None):
     flops = 2.0 * cfg.h * cfg.d * res["pairs"]
     filt_ms = res["stages"]["filter"]
     achieved = flops / (filt_ms * 1e-3) / 1e12
     peak = PEAK_TFLOPS[cfg.dtype]
     traffic = None
-    kib = TRAFFIC_KIB.get(cfg.name)
+    # counter traffic was taken with the default options only
+    kib = None if extra else TRAFFIC_KIB.get(cfg.name)
     if kib is not None and COPY_FACTOR is not None:
         traffic = round(kib[0] * 1024.0 / COPY_FACTOR[0] + kib[1] * 1024.0 / COPY_FACTOR[1])
+    alg = algorithmic_bytes(cfg, res["survivors_mean"])
+    hbm = {"algorithmic_bytes": alg, "algorithmic_gbs": round(alg / (filt_ms * 1e-3) / 1e9, 1),
+           "peak_gbs": HBM_PEAK_GBS}
+    if traffic is not None:
+        gbs = traffic / (filt_ms * 1e-3) / 1e9
+        hbm.update({"traffic_gbs": round(gbs, 1), "frac": round(gbs / HBM_PEAK_GBS, 4)})
+    else:
+        hbm["frac"] = round(hbm["algorithmic_gbs"] / HBM_PEAK_GBS, 4)
+        hbm["frac_of"] = "algorithmic bytes (no current counter traffic)"
     return {"bound": "mfma", "achieved": round(achieved, 2), "peak": peak, "unit": "TFLOP/s",
-            "frac": round(achieved / peak, 4), "traffic": traffic, "kernel": "k_fused (score+filter scan)",
-            "kernel_ms": round(filt_ms, 4), "algorithmic_flops": flops}
+            "frac": round(achieved / peak, 4), "traffic": traffic, "hbm_frac": hbm["frac"], "hbm": hbm,
+            "kernel": "k_fused (score+filter scan)", "kernel_ms": round(filt_ms, 4), "algorithmic_flops": flops}
 
 
-def other_config(name: str, unfused: bool):
+def other_config(name: str, unfused: bool, extra: dict = None, note: str = None):
     """One short measurement of a workload besides the headline ones (the
     unfused baseline only where its dense score matrix fits: not for the 4M
     retrieval, whose matrix would take 160 GB)."""
-    cfg, res = measure(name, 5, 2, unfused, cold=2)
+    cfg, res = measure(name, 5, 2, unfused, cold=2, extra=extra)
     out = {"workload": name, "dtype": cfg.dtype, "mode": cfg.mode, "num_queries": cfg.nq, "num_keys": cfg.nk,
            "heads": cfg.h, "head_dim": cfg.d, "k": cfg.k, "ms_per_step": round(res["ms"], 4),
            "value": res["pairs"] / (res["ms"] * 1e-3), "unit": "pairs/s", "visible_pairs": res["pairs"],
-           "roofline": roofline(cfg, res), "stages_ms": {k: round(v, 4) for k, v in res["stages"].items()},
-           "survivors_per_row_mean": round(res["survivors_mean"], 1), "fallback_rows": res["fallback_rows"]}
+           "roofline": roofline(cfg, res, extra), "stages_ms": {k: round(v, 4) for k, v in res["stages"].items()},
+           "survivors_per_row_mean": round(res["survivors_mean"], 1), "fallback_rows": res["fallback_rows"],
+           "fallback_reasons": res["fallback_reasons"]}
+    if extra:
+        out["options"] = extra
+    if note:
+        out["note"] = note
     if "unfused_ms" in res:
         out["unfused_ms_per_step"] = round(res["unfused_ms"], 4)
         out["unfused_same_sets"] = res["unfused_same_sets"]
-    print("[bench] %s: %.3f ms/step" % (name, res["ms"]), file=sys.stderr, flush=True)
+    print("[bench] %s%s: %.3f ms/step" % (name, " " + str(extra) if extra else "", res["ms"]), file=sys.stderr,
+          flush=True)
     return out
 
 
@@ -390,7 +465,17 @@ def cpu_oracle_rate(name: str, budget_s: float):
     rows = np.unique(np.linspace(0, cfg.nq - 1, n).round().astype(int)).tolist()
     t = run(rows)
     pr = float(e[rows].sum())
-    return {"value": pr / t, "unit": "pairs/s", "cores": int(threads), "kind": "oracle",
+    model = "unknown"
+    try:
+        with open("/proc/cpuinfo") as f:
+            for ln in f:
+                if ln.startswith("model name"):
+                    model = ln.split(":", 1)[1].strip()
+                    break
+    except OSError:  # pragma: no cover
+        pass
+    return {"value": pr / t, "unit": "pairs/s", "cores": int(threads), "kind": "oracle", "cpu_model": model,
+            "affinity_cpus": len(os.sched_getaffinity(0)),
             "sample": "%d evenly spaced rows of %s (first and last included), %.0f pairs in %.1f s; numpy float64"
                       % (len(rows), name, pr, t), "seconds": round(t, 2)}
 
@@ -407,9 +492,12 @@ def main():
     ap.add_argument("--no-retrieval", action="store_true", help="skip the 768-d retrieval sweep")
     ap.add_argument("--no-others", action="store_true", help="skip the other synthetic workloads")
     ap.add_argument("--retrieval-only", action="store_true", help="run only the 768-d retrieval sweep")
+    ap.add_argument("--chunked-only", action="store_true", help="run only the chunked-prefill measurement")
     ap.add_argument("--cpu-budget", type=float, default=15.0)
     ap.add_argument("--profile-only", default=None, metavar="WORKLOAD",
                     help="run only `steps` fused calls of one workload (for rocprofv3 counter passes)")
+    ap.add_argument("--unfused", action="store_true",
+                    help="with --profile-only: run the unfused pair (dense scores + radix select) instead")
     ap.add_argument("--copy-calib", type=int, default=0, metavar="MIB",
                     help="run only device copies of MIB MiB (calibrates FETCH_SIZE / WRITE_SIZE)")
     args = ap.parse_args()
@@ -439,17 +527,28 @@ def main():
             x = workloads.generate(cfg, seed=workloads.CONFIG_SEEDS[args.profile_only])
         d = {kk: (None if v is None else v.to("cuda")) for kk, v in x.items()
              if kk in ("q", "w", "keys", "q_scale", "k_scale", "offsets")}
-        for _ in range(max(1, args.steps)):
-            lt.indexer_topk(d["q"], d["w"], d["keys"], cfg.k, d["offsets"], d["q_scale"], d["k_scale"],
-                            mode=cfg.mode)
+        if args.unfused:
+            dense = torch.empty((cfg.nq, cfg.nk), dtype=torch.float32, device="cuda")
+            for _ in range(max(1, args.steps)):
+                lt.indexer_scores(d["q"], d["w"], d["keys"], d["q_scale"], d["k_scale"], mode=cfg.mode, out=dense)
+                lt.topk_radix(dense, cfg.k, causal_offsets=d["offsets"])
+        else:
+            for _ in range(max(1, args.steps)):
+                lt.indexer_topk(d["q"], d["w"], d["keys"], cfg.k, d["offsets"], d["q_scale"], d["k_scale"],
+                                mode=cfg.mode)
         torch.cuda.synchronize()
-        print(json.dumps({"profiled": args.profile_only, "calls": max(1, args.steps)}))
+        print(json.dumps({"profiled": args.profile_only, "unfused": args.unfused, "calls": max(1, args.steps)}))
         return
 
+    if args.chunked_only:
+        print(json.dumps({"chunked_prefill": [chunked_prefill(b, c, lbl) for b, c, lbl in CHUNK_CONTEXTS]}),
+              flush=True)
+        return
     if args.retrieval_only:
         print(json.dumps({"retrieval_e7": retrieval_sweep(max(1, args.steps))}), flush=True)
         return
-    cfg, res = measure("dsa_bf16_128k", args.steps, args.warmup, not args.no_unfused)
+    cfg, res = measure("dsa_bf16_128k", args.steps, args.warmup, not args.no_unfused,
+                       sorted_reps=max(3, args.steps // 4))
     print("[bench] dsa_bf16_128k: %.3f ms/step, stages %s" % (res["ms"], {k: round(v, 3) for k, v in
                                                                          res["stages"].items()}),
           file=sys.stderr, flush=True)
@@ -475,6 +574,7 @@ def main():
         "survivors_per_row": {"mean": round(res["survivors_mean"], 1), "max": res["survivors_max"],
                               "threshold_bin_mean": round(res["tie_bin_mean"], 1)},
         "fallback_rows": res["fallback_rows"],
+        "sorted_output_ms_per_step": round(res["sorted_ms"], 4),
         "dsa_union": res["dsa_union"],
         "bytes_written_per_query": {
             "fused": round(res["survivors_mean"] * 8 + cfg.k * 8, 1),
@@ -486,13 +586,14 @@ def main():
                            "pairs_per_s": res["pairs"] / (res["unfused_ms"] * 1e-3),
                            "same_sets": res["unfused_same_sets"]}
     if not args.no_1m:
-        cfg2, res2 = measure("dsa_fp8_1m", max(3, args.steps // 4), 2, not args.no_unfused)
+        cfg2, res2 = measure("dsa_fp8_1m", max(3, args.steps // 4), 2, not args.no_unfused, sorted_reps=3)
         print("[bench] dsa_fp8_1m: %.3f ms/step" % res2["ms"], file=sys.stderr, flush=True)
         m = {"workload": "dsa_fp8_1m", "dtype": "fp8", "ms_per_step": round(res2["ms"], 4),
              "value": res2["pairs"] / (res2["ms"] * 1e-3), "unit": "pairs/s", "visible_pairs": res2["pairs"],
              "roofline": roofline(cfg2, res2), "stages_ms": {k: round(v, 4) for k, v in res2["stages"].items()},
              "call_ms": step_summary(res2),
-             "survivors_per_row_mean": round(res2["survivors_mean"], 1), "fallback_rows": res2["fallback_rows"]}
+             "survivors_per_row_mean": round(res2["survivors_mean"], 1), "fallback_rows": res2["fallback_rows"],
+             "sorted_output_ms_per_step": round(res2["sorted_ms"], 4)}
         if "unfused_ms" in res2:
             m["unfused_ms_per_step"] = round(res2["unfused_ms"], 4)
             m["unfused_same_sets"] = res2["unfused_same_sets"]
@@ -501,9 +602,17 @@ def main():
         line["other_configs"] = [other_config(n, unf and not args.no_unfused)
                                  for n, unf in (("tiny_fp32", True), ("retrieval_bf16_4m", False),
                                                 ("adversarial_bf16_256k", True))]
+        # the adversarial workload with candidate buffers below its survivors
+        # (8192 per key split, ~10.6K survivors per split): every row
+        # overflows, and a second filter pass gated at the row's exact final
+        # bin completes it (the 'fallback' stage)
+        line["other_configs"].append(other_config(
+            "adversarial_bf16_256k", False, extra={"capacity": 8192},
+            note="candidate buffers below the survivors: every row overflows and is completed by a second "
+                 "filter pass gated at its exact final bin (stage 'fallback'; row_stats reason 6)"))
         print("[bench] other workloads done", file=sys.stderr, flush=True)
     if not args.no_chunked:
-        line["chunked_prefill"] = [chunked_prefill("dsa_bf16_128k", c, 3) for c in (256, 1024)]
+        line["chunked_prefill"] = [chunked_prefill(b, c, lbl) for b, c, lbl in CHUNK_CONTEXTS]
         print("[bench] chunked prefill done", file=sys.stderr, flush=True)
     if not args.no_retrieval:
         line["retrieval_e7"] = retrieval_sweep(3)

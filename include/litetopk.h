@@ -119,13 +119,19 @@ typedef struct lt_options {
                               [0] candidates written (summed over splits);
                               [1] final threshold bin tau_f (-2 if the row was
                                   queued before it was found);
-                              [2] fallback reason: 0 none, 1 candidate buffer
-                                  overflow, 2 threshold bin too large to sort,
-                                  3 forced, 4 candidate count disagrees with
-                                  the histogram, 5 tau_f below the sample's
+                              [2] how the row was completed: 0 by the
+                                  final select; by the exact dense fallback
+                                  because of 1 candidate buffer overflow,
+                                  2 threshold bin too large to sort, 3 forced,
+                                  4 candidate count disagrees with the
+                                  histogram, 5 tau_f below the sample's
                                   initial bin (sample and scan scores
                                   disagree; sec. 3.2 "Sampling" guarantees
-                                  tau_f >= tau0 otherwise);
+                                  tau_f >= tau0 otherwise); 6 buffer overflow
+                                  finished by a second filter pass gated at
+                                  the final bin tau_f (the histograms keep
+                                  counting past the buffer, so tau_f is exact;
+                                  shapes other than the 768-dimensional ones);
                               [3] candidates in bin tau_f;
                               [4] the sample's initial bin tau0 (-1 = no gate);
                               [5] bits of the float32 k-th largest visible

@@ -46,7 +46,7 @@ struct Resolved {
 };
 
 struct Layout {
-  size_t qctl, queue, params, list, samp, cnt, hist, cand, gate, scratch, total;
+  size_t qctl, queue, rqueue, rflag, params, list, samp, cnt, hist, cand, gate, scratch, total;
 };
 
 Layout carve(int nq, int nk, const Resolved& r, bool fused) {
@@ -59,6 +59,8 @@ Layout carve(int nq, int nk, const Resolved& r, bool fused) {
   };
   L.qctl = take(256);
   L.queue = take((size_t)nq * 4);
+  L.rqueue = fused ? take((size_t)nq * 4) : 0;  // rows of the second filter pass
+  L.rflag = fused ? take((size_t)nq * 4) : 0;
   L.params = take((size_t)nq * sizeof(RowParam));
   L.list = take((size_t)r.ns * 4);
   L.samp = fused ? take((size_t)nq * r.ns * 4) : 0;
@@ -298,6 +300,8 @@ int lt_indexer_topk(const void* q, const float* q_scale, const float* w, const v
   int2* cand = reinterpret_cast<int2*>(ws + L.cand);
   float* scratch = reinterpret_cast<float*>(ws + L.scratch);
   int* gate = reinterpret_cast<int*>(ws + L.gate);
+  int32_t* rqueue = reinterpret_cast<int32_t*>(ws + L.rqueue);
+  int32_t* rflag = reinterpret_cast<int32_t*>(ws + L.rflag);
   ScoreArgs a{q, q_scale, w, keys, k_scale, (int)dtype, (int)mode, nq, nk, h, d, offs, r.starts};
 
   hipError_t e;
@@ -306,22 +310,33 @@ int lt_indexer_topk(const void* q, const float* q_scale, const float* w, const v
   if ((e = make_list(r, nk, 1, list, st)) != hipSuccess) return hip_status(e);
   if (r.ns > 0 && (e = launch_sample_scores(a, list, r.ns, samp, st)) != hipSuccess) return hip_status(e);
   record(r, LT_STAGE_RANGE, st);
-  if ((e = launch_range(false, samp, r.ns, nq, nk, offs, r.starts, list, r.ns, r.m, k, params, r.stats, st)) !=
-      hipSuccess)
+  if ((e = launch_range(false, samp, r.ns, nq, nk, offs, r.starts, list, r.ns, r.m, k, params, r.stats, rflag,
+                        st)) != hipSuccess)
     return hip_status(e);
   record(r, LT_STAGE_FILTER, st);
   e = r.shared ? launch_wide_fused(a, params, r.S, r.L, r.cap, r.m, k, gate, cnt, hist, cand, st)
-               : launch_fused_scan(a, params, r.S, r.L, r.cap, r.m, k, gate, cnt, hist, cand, st);
+               : launch_fused_scan(a, params, r.S, r.L, r.cap, r.m, k, gate, cnt, hist, cand, nullptr, nullptr, st);
   if (e != hipSuccess) return hip_status(e);
   record(r, LT_STAGE_SELECT, st);
   // lists in arrival order: ties by key, every row sorted (also the rows the
-  // fallback completes)
-  const uint32_t sel_flags = r.flags | (sh.arrival_order ? kSelKeyed : 0u) | (r.shared ? kSelIlv : 0u);
+  // fallback completes). Overflowed rows of the one-list-per-split scans get
+  // a second filter pass at their final bin before any dense fallback.
+  const bool refilter = !r.shared;
+  const uint32_t sel_flags = r.flags | (sh.arrival_order ? kSelKeyed : 0u) | (r.shared ? kSelIlv : 0u) |
+                             (refilter ? kSelRefilter : 0u);
   const uint32_t fb_flags = r.flags | (sh.arrival_order ? LT_SORTED_OUTPUT : 0u);
   if ((e = launch_select(params, cnt, hist, cand, nq, r.S, r.HS, r.cap, r.m, k, r.E, sel_flags, out_idx, out_scores,
-                         qctl, queue, r.stats, st)) != hipSuccess)
+                         qctl, queue, rqueue, rflag, r.stats, st)) != hipSuccess)
     return hip_status(e);
   record(r, LT_STAGE_FALLBACK, st);
+  if (refilter) {
+    if ((e = launch_fused_scan(a, params, r.S, r.L, r.cap, r.m, k, gate, cnt, hist, cand, rflag, qctl, st)) !=
+        hipSuccess)
+      return hip_status(e);
+    if ((e = launch_select_second(params, cnt, hist, cand, nq, r.S, r.HS, r.cap, r.m, k, r.E, sel_flags, out_idx,
+                                  out_scores, qctl, queue, rqueue, r.stats, st)) != hipSuccess)
+      return hip_status(e);
+  }
   if ((e = launch_fused_fallback(a, k, fb_flags, qctl, queue, scratch, kFallbackGridFused, out_idx, out_scores,
                                  st)) != hipSuccess)
     return hip_status(e);
@@ -400,8 +415,8 @@ int lt_topk_select(const float* scores, int64_t stride, int32_t nq, int32_t nk, 
   if ((e = launch_init(qctl, st)) != hipSuccess) return hip_status(e);
   if ((e = make_list(r, nk, kSampleBlockScores, list, st)) != hipSuccess) return hip_status(e);
   record(r, LT_STAGE_RANGE, st);
-  if ((e = launch_range(true, scores, stride, nq, nk, offs, r.starts, list, r.ns, r.m, k, params, r.stats, st)) !=
-      hipSuccess)
+  if ((e = launch_range(true, scores, stride, nq, nk, offs, r.starts, list, r.ns, r.m, k, params, r.stats, nullptr,
+                        st)) != hipSuccess)
     return hip_status(e);
   record(r, LT_STAGE_FILTER, st);
   if ((e = launch_filter(scores, stride, nq, nk, offs, r.starts, params, r.S, r.L, r.cap, r.m, k, cnt, hist, cand,
@@ -409,7 +424,7 @@ int lt_topk_select(const float* scores, int64_t stride, int32_t nq, int32_t nk, 
     return hip_status(e);
   record(r, LT_STAGE_SELECT, st);
   if ((e = launch_select(params, cnt, hist, cand, nq, r.S, r.HS, r.cap, r.m, k, r.E, r.flags, out_idx, out_scores, qctl,
-                         queue, r.stats, st)) != hipSuccess)
+                         queue, nullptr, nullptr, r.stats, st)) != hipSuccess)
     return hip_status(e);
   record(r, LT_STAGE_FALLBACK, st);
   if ((e = launch_fallback_scores(scores, stride, nk, offs, r.starts, k, r.flags, qctl, queue, out_idx, out_scores,

@@ -16,19 +16,28 @@ hipError_t launch_init(uint32_t* qctl, hipStream_t st);
 // (NULL = num_keys) and `starts` the starts (NULL = 0).
 // With stats non-NULL, also writes row_stats fields 4..11 (the sample's
 // initial bin and k-th score, the bin map, the bins in use).
+// rflag (or NULL): per-row flags of the second filter pass, cleared here.
 hipError_t launch_range(bool from_scores, const float* src, int64_t stride, int nq, int nk,
                         const int32_t* offs, const int32_t* starts, const int32_t* list, int ns, int m, int k,
-                        RowParam* params, int32_t* stats, hipStream_t st);
+                        RowParam* params, int32_t* stats, int32_t* rflag, hipStream_t st);
 hipError_t launch_filter(const float* scores, int64_t stride, int nq, int nk, const int32_t* offs,
                          const int32_t* starts, const RowParam* params, int S, int L, int cap, int m, int k,
                          uint32_t* cnt, uint32_t* hist, int2* cand, hipStream_t st);
 size_t select_lds_bytes(int E);
 // S candidate lists per row (cnt [nq, S], cand [nq, S, cap]); HS histograms
 // per row (hist [nq, HS, m]), HS = S or 1.
-hipError_t launch_select(const RowParam* params, const uint32_t* cnt, const uint32_t* hist,
-                         const int2* cand, int nq, int S, int HS, int cap, int m, int k, int E,
-                         uint32_t flags, int32_t* out_i, float* out_s, uint32_t* qctl,
-                         int32_t* queue, int32_t* stats, hipStream_t st);
+// Rows that need the dense fallback go to queue (count qctl[0]); with
+// kSelRefilter in flags, overflowed rows whose final bins fit go to rqueue
+// (count qctl[1]) with rflag set and params[row].tau0 = their final bin.
+hipError_t launch_select(RowParam* params, const uint32_t* cnt, const uint32_t* hist, const int2* cand, int nq,
+                         int S, int HS, int cap, int m, int k, int E, uint32_t flags, int32_t* out_i, float* out_s,
+                         uint32_t* qctl, int32_t* queue, int32_t* rqueue, int32_t* rflag, int32_t* stats,
+                         hipStream_t st);
+// The select of the rows in rqueue after their second filter pass.
+hipError_t launch_select_second(RowParam* params, const uint32_t* cnt, const uint32_t* hist, const int2* cand,
+                                int nq, int S, int HS, int cap, int m, int k, int E, uint32_t flags, int32_t* out_i,
+                                float* out_s, uint32_t* qctl, int32_t* queue, int32_t* rqueue, int32_t* stats,
+                                hipStream_t st);
 hipError_t launch_fallback_scores(const float* scores, int64_t stride, int nk, const int32_t* offs,
                                   const int32_t* starts, int k, uint32_t flags, const uint32_t* qctl,
                                   const int32_t* queue, int32_t* out_i, float* out_s, int grid, hipStream_t st);
@@ -83,8 +92,12 @@ hipError_t launch_dense_scores(const ScoreArgs& a, float* out, int64_t ld, hipSt
 // Fused score + gate + write-back scan over S key splits of L keys each;
 // pub [nq * 8 bytes] holds the bins the splits of each row publish where they
 // share thresholds (initialised here).
+// rflag NULL: every row. Else the second filter pass: only rows with
+// rflag[t] set are scanned and written (blocks without such rows, and every
+// block when qctl[1] == 0, return at once).
 hipError_t launch_fused_scan(const ScoreArgs& a, const RowParam* params, int S, int L, int cap, int m,
-                             int k, int* pub, uint32_t* cnt, uint32_t* hist, int2* cand, hipStream_t st);
+                             int k, int* pub, uint32_t* cnt, uint32_t* hist, int2* cand, const int32_t* rflag,
+                             const uint32_t* qctl, hipStream_t st);
 // Exact fallback for queued rows: dense re-score into scratch [grid, nk], then radix select.
 hipError_t launch_fused_fallback(const ScoreArgs& a, int k, uint32_t flags, const uint32_t* qctl,
                                  const int32_t* queue, float* scratch, int grid, int32_t* out_i,
@@ -113,5 +126,11 @@ hipError_t launch_wide_fallback(const ScoreArgs& a, int k, uint32_t flags, const
 // wide scan); rows are few and long, so the select runs 1024-thread blocks.
 constexpr uint32_t kSelKeyed = 1u << 30;
 constexpr uint32_t kSelIlv = 1u << 29;
+// kSelRefilter: a row whose lists overflowed but whose keys at or above its
+// final bin fit in one list is queued for a second filter pass gated at that
+// bin (rqueue, qctl[1], rflag) instead of the dense fallback.
+// kSelSecond: the select of the rows of that second pass.
+constexpr uint32_t kSelRefilter = 1u << 28;
+constexpr uint32_t kSelSecond = 1u << 27;
 
 }  // namespace lt

@@ -89,11 +89,17 @@ struct Mfma<DT_FP8> {
 // ---------------------------------------------------------------------------
 // Static configuration of one (dtype, H, d) variant.
 // ---------------------------------------------------------------------------
-template <int DT_, int H_, int D_, int QW_, int NT_, int WAVES_, bool RELU_>
+template <int DT_, int H_, int D_, int QW_, int NT_, int WAVES_, bool RELU_, bool UNITW_ = false>
 struct Cfg {
   using M = Mfma<DT_>;
   static constexpr int DT = DT_, H = H_, D = D_, QW = QW_, NT = NT_, WAVES = WAVES_;
   static constexpr bool RELU = RELU_;
+  // one head, no ReLU and no head weights (w = NULL): the score is the dot
+  // product itself, taken from the accumulator with no epilogue arithmetic
+  // (the weighted form fmaf(1, x, +0) gives the same bits: an accumulator
+  // that starts at +0 never holds -0)
+  static constexpr bool UNITW = UNITW_;
+  static_assert(!UNITW || (H == 1 && !RELU), "unit weights: one head, inner product");
   static constexpr int MT = QW * H / 32;               // M tiles per wave
   static constexpr int KS = D / M::KI;                 // K steps per key
   static constexpr int KT = 32 * NT;                   // keys per tile
@@ -325,7 +331,8 @@ __device__ __forceinline__ void reduce_half(const WaveQ<C>& s, const f32x16_t (&
 #pragma unroll
           for (int r = 0; r < C::H; ++r) {
             const int v = 4 * i + sq * C::H + r;
-            sum = fmaf(s.wv[mt][v], relu<C>(acc[mt][v]), sum);
+            if constexpr (C::UNITW) sum = acc[mt][v];
+            else sum = fmaf(s.wv[mt][v], relu<C>(acc[mt][v]), sum);
           }
           out[(mt * 4 + i) * C::GPQ + sq] = sum;
         }
@@ -790,22 +797,25 @@ struct FusedSink {
   uint32_t* hist;     // LDS, [QW][m] for this wave
   int2* cand;
   int2* crow[C::QW];  // this split's candidate list of each query
+  const int32_t* rflag;  // second filter pass: only rows with rflag[t] set (else NULL: every row)
   int qbase, nq, S, split, cap, m, k;
 
-  __device__ void set_tau(int q, int t) {
+  __device__ __forceinline__ bool row_on(int t) const { return t < nq && (!rflag || rflag[t]); }
+
+  __device__ __forceinline__ void set_tau(int q, int t) {
     tau[q] = t;
     thr[q] = gate_thr(t);
     thr_up[q] = t < m - 1 ? (float)(t + 1) : __builtin_nanf("");
   }
 
-  __device__ void init(const ScoreArgs& a, const RowParam* params, int kend) {
+  __device__ __forceinline__ void init(const ScoreArgs& a, const RowParam* params, int kend) {
 #pragma unroll
     for (int q = 0; q < C::QW; ++q) {
       const int t = qbase + q;
       RowRange rr{0, 0};
       float dl = 1.0f, c = 0.0f;
       int t0 = -1;
-      if (t < nq) {
+      if (row_on(t)) {
         rr = row_range(a.offs, a.starts, t, a.nk);
         const RowParam p = params[t];
         dl = p.delta;
@@ -823,7 +833,7 @@ struct FusedSink {
     }
   }
 
-  __device__ void consume(int, int k0, int, const float (&sc)[C::NI], bool live) {
+  __device__ __forceinline__ void consume(int, int k0, int, const float (&sc)[C::NI], bool live) {
     const int l = lane_id(), h = l >> 5, r32 = l & 31;
     float x[C::NI];
     bool ps[C::NI];
@@ -886,13 +896,13 @@ struct FusedSink {
     }
   }
 
-  __device__ void finish(uint32_t* cnt, uint32_t* hist_out) {
+  __device__ __forceinline__ void finish(uint32_t* cnt, uint32_t* hist_out) {
     __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "wavefront");
     const int l = lane_id();
 #pragma unroll
     for (int q = 0; q < C::QW; ++q) {
       const int t = qbase + q;
-      if (t >= nq) continue;
+      if (!row_on(t)) continue;
       const int64_t u = (int64_t)t * S + split;
       for (int b = l; b < m; b += kWave) hist_out[u * m + b] = hist[q * m + b];
       if (l == 0) cnt[u] = tail[q];
@@ -983,9 +993,12 @@ struct GroupedSink {
   uint32_t* hist;     // LDS, [QW][m] for this wave
   int2* cand;
   int64_t lbase, lstride;  // list of query q: cand + lbase + q * lstride
+  const int32_t* rflag;    // second filter pass: only rows with rflag[t] set (else NULL: every row)
   int qbase, nq, S, split, cap, m, k;
 
-  __device__ void bind(uint8_t* lds) {
+  __device__ __forceinline__ bool row_on(int t) const { return t < nq && (!rflag || rflag[t]); }
+
+  __device__ __forceinline__ void bind(uint8_t* lds) {
     qs = reinterpret_cast<QState*>(lds);
     tail = reinterpret_cast<uint32_t*>(lds + C::QW * sizeof(QState));
     above = tail + C::QW;
@@ -994,18 +1007,18 @@ struct GroupedSink {
     rhdr = reinterpret_cast<uint32_t*>(rec + kRecs * C::NI);
   }
 
-  __device__ static float gate_floor(float delta, float c, int tau) {
+  __device__ __forceinline__ static float gate_floor(float delta, float c, int tau) {
     if (tau < 0) return -__builtin_inff();
     const float t = (float)tau, i0 = (t - c) / delta;
     const float err = ((fabsf(t) + fabsf(c)) / delta + fabsf(i0)) * 0x1p-20f;
     return i0 - err;
   }
 
-  __device__ float up_of(int t) const { return t < m - 1 ? (float)(t + 1) : __builtin_inff(); }
+  __device__ __forceinline__ float up_of(int t) const { return t < m - 1 ? (float)(t + 1) : __builtin_inff(); }
 
   // the per-item copies of T, and the ungated flag (the query of item j in
   // lane half h is item_q(j, 0) + h * 4 / H)
-  __device__ void update_gates() {
+  __device__ __forceinline__ void update_gates() {
     const int l = lane_here();
     __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "wavefront");
     const QState* qh = qs + (l >> 5) * (4 / C::H);
@@ -1014,13 +1027,13 @@ struct GroupedSink {
       static_assert(C::item_q(j, 1) - C::item_q(j, 0) == 4 / C::H, "query of an item in the upper half");
       tq[j] = qh[C::item_q(j, 0)].gate;
     });
-    const bool valid = l < C::QW && qbase + l < nq;
+    const bool valid = l < C::QW && row_on(qbase + l);
     ungated = __ballot(valid && tau_v < 0) != 0;
   }
 
-  __device__ void init(const ScoreArgs& a, const RowParam* params, int kend) {
+  __device__ __forceinline__ void init(const ScoreArgs& a, const RowParam* params, int kend) {
     const int l = lane_id(), t = qbase + l;
-    const bool valid = l < C::QW && t < nq;
+    const bool valid = l < C::QW && row_on(t);
     RowRange rr{0, 0};
     float dl = 1.0f, c = 0.0f;
     int t0 = -1;
@@ -1072,7 +1085,7 @@ struct GroupedSink {
 
   // every kShareEvery steps: read the rows' published bins (lands by the
   // step's tile wait)
-  __device__ void pre() {
+  __device__ __forceinline__ void pre() {
     if (!pub) return;
     if (steps++ % kShareEvery != 0) return;
     const int l = lane_id();
@@ -1082,7 +1095,7 @@ struct GroupedSink {
   }
 
   // lane lq: its query's bin moves to t (above already adjusted)
-  __device__ void move_tau(int lq, int t, uint32_t ab) {
+  __device__ __forceinline__ void move_tau(int lq, int t, uint32_t ab) {
     above[lq] = ab;
     QState& r = qs[lq];
     r.up = up_of(t);
@@ -1090,7 +1103,7 @@ struct GroupedSink {
     tau_v = t;
   }
 
-  __device__ void consume(int, int k0, int, const float (&sc)[C::NI], bool live) {
+  __device__ __forceinline__ void consume(int, int k0, int, const float (&sc)[C::NI], bool live) {
     if (!live) return;
     static_assert(C::NI <= 32, "one bit per item");
     typedef float fNI __attribute__((ext_vector_type(C::NI)));
@@ -1100,7 +1113,7 @@ struct GroupedSink {
       int g = 255;
       for (int j = 0; j < S; ++j) g = min(g, (int)((gw >> (8 * j)) & 0xFFu));
       g -= 1;
-      const bool raise = l < C::QW && qbase + l < nq && g > tau_v;
+      const bool raise = l < C::QW && row_on(qbase + l) && g > tau_v;
       if (__ballot(raise) != 0) {
         __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "wavefront");
         if (raise) {
@@ -1186,7 +1199,7 @@ struct GroupedSink {
   // counts of a written candidate of query q: its bin, and above tau / tau_s
   // (only when x >= 0: not NaN, not below the range; the adds are issued
   // either way, of 0 for the others, so that no branch is taken)
-  __device__ void count(int q, float s, const f32x4_t& f) {
+  __device__ __forceinline__ void count(int q, float s, const f32x4_t& f) {
     const float x = fmaf(s, f[0], f[1]);
     const int b = min(max(__float2int_rz(x), 0), m - 1);
     lds_add(&hist[q * m + b], x >= 0.0f ? 1u : 0u);
@@ -1197,7 +1210,7 @@ struct GroupedSink {
   // the queue, one record per lane: the record's scores still at or above
   // their row's gate and inside its visible range take a slot, are written
   // and counted
-  __device__ void drain() {
+  __device__ __forceinline__ void drain() {
     static_assert(kRecs <= kWave, "one record per lane");
     const int l = lane_here();
     if (l < qlen) {
@@ -1235,7 +1248,7 @@ struct GroupedSink {
 
   // threshold refresh: each lane walks its own query's histogram, for tau
   // (k) and, where the splits share, for tau_s (ks)
-  __device__ void refresh() {
+  __device__ __forceinline__ void refresh() {
     const int l = lane_id();
     __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "wavefront");
     const bool mine = l < C::QW;
@@ -1274,22 +1287,23 @@ struct GroupedSink {
   }
 
   // Query of item it in lane half h, with a run-time item index.
-  __device__ static int item_query(int it, int h) {
+  __device__ __forceinline__ static int item_query(int it, int h) {
     const int s = it % C::GPQ, g = it / C::GPQ, i = g % 4, mt = (g / 4) % C::MT;
     return (32 * mt + 8 * i + 4 * h + s * C::H) / C::H;
   }
 
-  __device__ void finish(uint32_t* cnt, uint32_t* hist_out) {
+  __device__ __forceinline__ void finish(uint32_t* cnt, uint32_t* hist_out) {
     if (qlen != 0) drain();
     __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "wavefront");
     const int l = lane_id();
     for (int q = 0; q < C::QW; ++q) {
       const int t = qbase + q;
       if (t >= nq) break;
+      if (!row_on(t)) continue;
       const int64_t u = (int64_t)t * S + split;
       for (int b = l; b < m; b += kWave) hist_out[u * m + b] = hist[q * m + b];
     }
-    if (l < C::QW && qbase + l < nq) cnt[(int64_t)(qbase + l) * S + split] = tail[l];
+    if (l < C::QW && row_on(qbase + l)) cnt[(int64_t)(qbase + l) * S + split] = tail[l];
   }
 };
 
@@ -1332,7 +1346,8 @@ constexpr int fused_sink_lds() {
 template <class C>
 __global__ __launch_bounds__(C::NTHREADS) void k_fused(ScoreArgs a, const RowParam* params, int S, int L, int cap,
                                                        int m, int k, uint8_t* pub, uint32_t* cnt,
-                                                       uint32_t* hist_out, int2* cand) {
+                                                       uint32_t* hist_out, int2* cand, const int32_t* rflag,
+                                                       const uint32_t* qctl) {
   extern __shared__ __align__(16) uint8_t lds[];
   uint32_t* hist = reinterpret_cast<uint32_t*>(lds + C::SCAN_LDS + fused_sink_lds<C>());
   int* emax = reinterpret_cast<int*>(hist + C::QT * m);
@@ -1340,13 +1355,17 @@ __global__ __launch_bounds__(C::NTHREADS) void k_fused(ScoreArgs a, const RowPar
   const int tile = blockIdx.x / S, split = blockIdx.x - tile * S;
   const int q0 = tile * C::QT, wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave),
             qbase = q0 + wave * C::QW;
+  // second filter pass: nothing queued, or none of this block's rows
+  if (rflag && qctl[1] == 0u) return;
+  const bool on = threadIdx.x < C::QT && q0 + (int)threadIdx.x < a.nq && (!rflag || rflag[q0 + threadIdx.x]);
+  if (rflag && !__syncthreads_or(on)) return;
   for (int i = threadIdx.x; i < C::QT * m; i += C::NTHREADS) hist[i] = 0u;
   if (threadIdx.x == 0) {
     *emax = 0;
     *smin = a.nk;
   }
   __syncthreads();
-  if (threadIdx.x < C::QT && q0 + (int)threadIdx.x < a.nq) {
+  if (on) {
     const RowRange rr = row_range(a.offs, a.starts, q0 + threadIdx.x, a.nk);
     if (rr.e > rr.s) {
       atomicMax(emax, rr.e);
@@ -1368,6 +1387,7 @@ __global__ __launch_bounds__(C::NTHREADS) void k_fused(ScoreArgs a, const RowPar
     sink.pub = S > 1 && S <= 8 ? pub : nullptr;
   }
   sink.cand = cand;
+  sink.rflag = rflag;
   sink.qbase = qbase;
   sink.nq = a.nq;
   sink.S = S;
@@ -1418,13 +1438,21 @@ __global__ __launch_bounds__(C::NTHREADS) void k_fused_fallback(ScoreArgs a, int
   X(DT_BF16, 1, 128, 32, 2, 8, false)    \
   X(DT_FP8, 64, 128, 1, 2, 8, true)
 
+// unitw: the inner-product one-head shapes without head weights take the
+// UNITW variant (same results, no epilogue arithmetic)
 template <class F>
-static bool with_cfg(int dt, int mode, int h, int d, F&& f) {
+static bool with_cfg(int dt, int mode, int h, int d, bool unitw, F&& f) {
   const bool relu = mode == LT_SCORE_DSA;
-#define LT_CASE(DT, H, D, QW, NT, WV, RELU)                          \
-  if (dt == DT && h == H && d == D && relu == RELU) {                \
-    f.template operator()<Cfg<DT, H, D, QW, NT, WV, RELU>>();        \
-    return true;                                                     \
+#define LT_CASE(DT, H, D, QW, NT, WV, RELU)                                  \
+  if (dt == DT && h == H && d == D && relu == RELU) {                        \
+    if constexpr (H == 1 && !RELU) {                                         \
+      if (unitw) {                                                           \
+        f.template operator()<Cfg<DT, H, D, QW, NT, WV, RELU, true>>();      \
+        return true;                                                         \
+      }                                                                      \
+    }                                                                        \
+    f.template operator()<Cfg<DT, H, D, QW, NT, WV, RELU>>();                \
+    return true;                                                             \
   }
   LT_VARIANTS(LT_CASE)
 #undef LT_CASE
@@ -1433,7 +1461,7 @@ static bool with_cfg(int dt, int mode, int h, int d, F&& f) {
 
 ScoreShape score_shape(int dtype, int mode, int h, int d) {
   ScoreShape s{0, 0, 0, 0, 0, 0, 0};
-  const bool found = with_cfg(dtype, mode, h, d, [&]<class C>() {
+  const bool found = with_cfg(dtype, mode, h, d, false, [&]<class C>() {
     s.supported = 1;
     s.arrival_order = C::GROUPED ? 1 : 0;
     s.queries_per_block = C::QT;
@@ -1450,7 +1478,7 @@ static constexpr int kSampleBlocks = 256;  // the sample scorer aims at one bloc
 hipError_t launch_sample_scores(const ScoreArgs& a, const int32_t* list, int ns, float* samp, hipStream_t st) {
   if (wide_shape(a.dtype, a.mode, a.h, a.d).supported) return launch_wide_sample(a, list, ns, samp, st);
   hipError_t err = hipErrorInvalidValue;
-  with_cfg(a.dtype, a.mode, a.h, a.d, [&]<class C>() {
+  with_cfg(a.dtype, a.mode, a.h, a.d, a.w == nullptr, [&]<class C>() {
     // few query tiles (a short chunk): cut the sample into more slices so
     // that the launch still covers the GPU
     const int tiles = (a.nq + C::QT - 1) / C::QT;
@@ -1477,7 +1505,7 @@ hipError_t launch_sample_scores(const ScoreArgs& a, const int32_t* list, int ns,
 hipError_t launch_dense_scores(const ScoreArgs& a, float* out, int64_t ld, hipStream_t st) {
   if (wide_shape(a.dtype, a.mode, a.h, a.d).supported) return launch_wide_dense(a, out, ld, st);
   hipError_t err = hipErrorInvalidValue;
-  with_cfg(a.dtype, a.mode, a.h, a.d, [&]<class C>() {
+  with_cfg(a.dtype, a.mode, a.h, a.d, a.w == nullptr, [&]<class C>() {
     dim3 grid((a.nq + C::QT - 1) / C::QT, (a.nk + kSlice - 1) / kSlice);
     if (grid.x == 0 || grid.y == 0) {
       err = hipSuccess;
@@ -1496,9 +1524,10 @@ __global__ void k_pub_init(const RowParam* params, int nq, uint64_t* pub) {
 }
 
 hipError_t launch_fused_scan(const ScoreArgs& a, const RowParam* params, int S, int L, int cap, int m, int k,
-                             int* pub, uint32_t* cnt, uint32_t* hist, int2* cand, hipStream_t st) {
+                             int* pub, uint32_t* cnt, uint32_t* hist, int2* cand, const int32_t* rflag,
+                             const uint32_t* qctl, hipStream_t st) {
   hipError_t err = hipErrorInvalidValue;
-  with_cfg(a.dtype, a.mode, a.h, a.d, [&]<class C>() {
+  with_cfg(a.dtype, a.mode, a.h, a.d, a.w == nullptr, [&]<class C>() {
     const int tiles = (a.nq + C::QT - 1) / C::QT;
     if (tiles == 0) {
       err = hipSuccess;
@@ -1513,7 +1542,7 @@ hipError_t launch_fused_scan(const ScoreArgs& a, const RowParam* params, int S, 
     if (lds > 65536)
       (void)hipFuncSetAttribute((const void*)k_fused<C>, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
     hipLaunchKernelGGL(k_fused<C>, dim3(tiles * S), dim3(C::NTHREADS), lds, st, a, params, S, L, cap, m, k,
-                       reinterpret_cast<uint8_t*>(pub), cnt, hist, cand);
+                       reinterpret_cast<uint8_t*>(pub), cnt, hist, cand, rflag, qctl);
     err = hipGetLastError();
   });
   return err;
@@ -1525,7 +1554,7 @@ hipError_t launch_fused_fallback(const ScoreArgs& a, int k, uint32_t flags, cons
   if (wide_shape(a.dtype, a.mode, a.h, a.d).supported)
     return launch_wide_fallback(a, k, flags, qctl, queue, scratch, grid, out_i, out_s, st);
   hipError_t err = hipErrorInvalidValue;
-  with_cfg(a.dtype, a.mode, a.h, a.d, [&]<class C>() {
+  with_cfg(a.dtype, a.mode, a.h, a.d, a.w == nullptr, [&]<class C>() {
     size_t lds = C::SCAN_LDS;
     const size_t rl = radix_lds_bytes(k);
     if (rl > lds) lds = rl;

@@ -51,7 +51,7 @@ template <int NTH, bool FROM_SCORES>
 __global__ __launch_bounds__(NTH) void k_range(const float* src, int64_t stride, int nq, int nk,
                                                          const int32_t* offs, const int32_t* starts,
                                                          const int32_t* list, int ns, int m, int k,
-                                                         RowParam* params, int32_t* stats) {
+                                                         RowParam* params, int32_t* stats, int32_t* rflag) {
   constexpr int NW = NTH / kWave;
   __shared__ uint32_t hist[kMaxBins];
   __shared__ float red_mn[NW], red_mx[NW];
@@ -62,6 +62,7 @@ __global__ __launch_bounds__(NTH) void k_range(const float* src, int64_t stride,
   const float* rp = src + (int64_t)row * stride;
 
   for (int b = threadIdx.x; b < kMaxBins; b += NTH) hist[b] = 0u;
+  if (rflag && threadIdx.x == 0) rflag[row] = 0;
   float mn = __builtin_inff(), mx = -__builtin_inff();
   uint32_t nvis = 0;
   for (int base = 0; base < ns; base += NTH * kRangeUnroll) {
@@ -279,21 +280,22 @@ constexpr int kSelPer = 4;         // list entries per thread per step
 constexpr int kSelThreadsWide = 1024;  // keyed rows, and launches of few rows
 constexpr int kSelPerWide = 8;
 constexpr int kSelFewRows = 512;     // launches of at most this many rows use the wide blocks
+constexpr int kSecondSelectGrid = 512;  // blocks of the second select (persistent over its queue)
 
 // LDS byte offset of the sort entries of k_select with NTH threads.
 constexpr size_t select_ent_offset(int nth) { return ((size_t)kMaxBins + 32 + nth + 16) * 4; }
 
 template <int NTH, int PER>
-__global__ __launch_bounds__(NTH) void k_select(
-    const RowParam* params, const uint32_t* cnt, const uint32_t* hist, const int2* cand, int nq,
-    int S, int HS, int cap, int m, int k, int E, uint32_t flags, int32_t* out_i, float* out_s,
-    uint32_t* qctl, int32_t* queue, int32_t* stats) {
+__device__ __forceinline__ void select_row(int row, RowParam* params, const uint32_t* cnt, const uint32_t* hist,
+                           const int2* cand, int nq, int S, int HS, int cap, int m, int k, int E, uint32_t flags,
+                           int32_t* out_i, float* out_s, uint32_t* qctl, int32_t* queue, int32_t* rqueue,
+                           int32_t* rflag, int32_t* stats) {
   extern __shared__ __align__(16) uint8_t lds[];
   uint32_t* hsum = reinterpret_cast<uint32_t*>(lds);          // [256]
   uint32_t* tmp = hsum + kMaxBins;                             // [32]
   uint32_t* off = tmp + 32;                                    // [NTH + 1]: list offsets of a group
   uint64_t* ent = reinterpret_cast<uint64_t*>(lds + select_ent_offset(NTH));  // [E]
-  const int row = blockIdx.x, tid = threadIdx.x;
+  const int tid = threadIdx.x;
   // keyed: the lists are not in key order, so the tie-break position is the
   // key itself, the output is rebuilt from the sort entries, and every row
   // is sorted (the order of arrival would make it vary between calls)
@@ -323,14 +325,14 @@ __global__ __launch_bounds__(NTH) void k_select(
       queue[slot] = row;
       if (stats) {
         int32_t* st = stats + (int64_t)row * LT_ROW_STATS;
-        st[0] = (int32_t)total_c;
+        if (!(flags & kSelSecond)) st[0] = (int32_t)total_c;
         st[1] = tau;
         st[2] = why;
         st[3] = (int32_t)nt;
       }
     }
   };
-  if (reason) {
+  if (reason == 3) {
     enqueue(reason, -2, 0);
     return;
   }
@@ -354,7 +356,34 @@ __global__ __launch_bounds__(NTH) void k_select(
   __syncthreads();
   const int tau = (int)tmp[24];
   const uint32_t c_above = tmp[25];
+  const uint32_t c_tie = tau >= 0 ? hsum[tau] : 0u;
   __syncthreads();
+  if (reason == 1) {
+    // The lists overflowed, but the histograms kept counting: bins >= tau
+    // are complete and tau is the row's exact final bin. A second filter
+    // pass gated at tau from its first key writes exactly the c_above +
+    // c_tie keys of those bins; when they fit in one list (and the sort
+    // buffer) the row is queued for that pass, else for the dense fallback.
+    const bool sorted_all = (flags & LT_SORTED_OUTPUT) || (flags & kSelKeyed);
+    const uint32_t nsort = sorted_all ? c_above + c_tie : c_tie;
+    if ((flags & kSelRefilter) && tau >= 0 && c_above + c_tie <= (uint32_t)cap && nsort <= (uint32_t)E) {
+      if (tid == 0) {
+        params[row].tau0 = tau;
+        rflag[row] = 1;
+        rqueue[atomicAdd(&qctl[1], 1u)] = row;
+        if (stats) {
+          int32_t* st = stats + (int64_t)row * LT_ROW_STATS;
+          st[0] = (int32_t)total_c;
+          st[1] = tau;
+          st[2] = 6;
+          st[3] = (int32_t)c_tie;
+        }
+      }
+      return;
+    }
+    enqueue(1, tau, c_tie);
+    return;
+  }
   const RowParam p = params[row];
   // Every visible sample key in a bin >= tau0 passes the gate or is
   // outranked by k counted keys, so an exact scan ends with tau >= tau0. A
@@ -485,10 +514,37 @@ __global__ __launch_bounds__(NTH) void k_select(
   }
   if (stats && tid == 0) {
     int32_t* st = stats + (int64_t)row * LT_ROW_STATS;
-    st[0] = (int32_t)total_c;
+    // a row finished by the second filter pass keeps its candidates written
+    // by the first pass (field 0) and reports reason 6
+    if (!(flags & kSelSecond)) st[0] = (int32_t)total_c;
     st[1] = tau;
-    st[2] = 0;
+    st[2] = (flags & kSelSecond) ? 6 : 0;
     st[3] = (int32_t)run_tie;
+  }
+}
+
+// One block per row.
+template <int NTH, int PER>
+__global__ __launch_bounds__(NTH) void k_select(
+    RowParam* params, const uint32_t* cnt, const uint32_t* hist, const int2* cand, int nq,
+    int S, int HS, int cap, int m, int k, int E, uint32_t flags, int32_t* out_i, float* out_s,
+    uint32_t* qctl, int32_t* queue, int32_t* rqueue, int32_t* rflag, int32_t* stats) {
+  select_row<NTH, PER>(blockIdx.x, params, cnt, hist, cand, nq, S, HS, cap, m, k, E, flags, out_i, out_s, qctl,
+                       queue, rqueue, rflag, stats);
+}
+
+// The rows of the second filter pass (queue rqueue, length qctl[1]);
+// persistent: block b takes entries b, b + grid, ...
+template <int NTH, int PER>
+__global__ __launch_bounds__(NTH) void k_select_second(
+    RowParam* params, const uint32_t* cnt, const uint32_t* hist, const int2* cand, int nq,
+    int S, int HS, int cap, int m, int k, int E, uint32_t flags, int32_t* out_i, float* out_s,
+    uint32_t* qctl, int32_t* queue, int32_t* rqueue, int32_t* stats) {
+  const uint32_t n = qctl[1];
+  for (uint32_t i = blockIdx.x; i < n; i += gridDim.x) {
+    select_row<NTH, PER>(rqueue[i], params, cnt, hist, cand, nq, S, HS, cap, m, k, E, flags | kSelSecond, out_i,
+                         out_s, qctl, queue, rqueue, nullptr, stats);
+    __syncthreads();
   }
 }
 
@@ -534,11 +590,11 @@ hipError_t launch_init(uint32_t* qctl, hipStream_t st) {
 
 hipError_t launch_range(bool from_scores, const float* src, int64_t stride, int nq, int nk,
                         const int32_t* offs, const int32_t* starts, const int32_t* list, int ns, int m, int k,
-                        RowParam* params, int32_t* stats, hipStream_t st) {
+                        RowParam* params, int32_t* stats, int32_t* rflag, hipStream_t st) {
   dim3 grid(nq);
   auto go = [&](auto kernel, int nth) {
     hipLaunchKernelGGL(kernel, grid, dim3(nth), 0, st, src, stride, nq, nk, offs, starts, list, ns, m, k, params,
-                       stats);
+                       stats, rflag);
   };
   // a long sample is read in fewer, wider steps (the kernel waits on loads);
   // so are the rows of a launch of few rows, which otherwise leaves most of
@@ -566,15 +622,15 @@ hipError_t launch_filter(const float* scores, int64_t stride, int nq, int nk, co
 
 size_t select_lds_bytes(int E) { return select_ent_offset(kSelThreadsWide) + (size_t)E * 8; }
 
-hipError_t launch_select(const RowParam* params, const uint32_t* cnt, const uint32_t* hist,
-                         const int2* cand, int nq, int S, int HS, int cap, int m, int k, int E,
-                         uint32_t flags, int32_t* out_i, float* out_s, uint32_t* qctl,
-                         int32_t* queue, int32_t* stats, hipStream_t st) {
+hipError_t launch_select(RowParam* params, const uint32_t* cnt, const uint32_t* hist, const int2* cand, int nq,
+                         int S, int HS, int cap, int m, int k, int E, uint32_t flags, int32_t* out_i, float* out_s,
+                         uint32_t* qctl, int32_t* queue, int32_t* rqueue, int32_t* rflag, int32_t* stats,
+                         hipStream_t st) {
   auto go = [&](auto kernel, int nth) {
     const size_t lds = select_ent_offset(nth) + (size_t)E * 8;
     if (lds > 65536) (void)hipFuncSetAttribute((const void*)kernel, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
     hipLaunchKernelGGL(kernel, dim3(nq), dim3(nth), lds, st, params, cnt, hist, cand, nq, S, HS, cap, m, k, E, flags,
-                       out_i, out_s, qctl, queue, stats);
+                       out_i, out_s, qctl, queue, rqueue, rflag, stats);
   };
   // one block per row: a launch of few rows (a short chunk) fills the GPU
   // only with wide blocks, whose more loads in flight also shorten the walk
@@ -583,6 +639,23 @@ hipError_t launch_select(const RowParam* params, const uint32_t* cnt, const uint
   // 0.16 ms at 256 threads against 0.37 ms at 1024)
   if ((flags & kSelIlv) || nq <= kSelFewRows) go(k_select<kSelThreadsWide, kSelPerWide>, kSelThreadsWide);
   else go(k_select<kSelThreads, kSelPer>, kSelThreads);
+  return hipGetLastError();
+}
+
+hipError_t launch_select_second(RowParam* params, const uint32_t* cnt, const uint32_t* hist, const int2* cand,
+                                int nq, int S, int HS, int cap, int m, int k, int E, uint32_t flags, int32_t* out_i,
+                                float* out_s, uint32_t* qctl, int32_t* queue, int32_t* rqueue, int32_t* stats,
+                                hipStream_t st) {
+  const int grid = nq < kSecondSelectGrid ? nq : kSecondSelectGrid;
+  if (grid == 0) return hipSuccess;
+  auto go = [&](auto kernel, int nth) {
+    const size_t lds = select_ent_offset(nth) + (size_t)E * 8;
+    if (lds > 65536) (void)hipFuncSetAttribute((const void*)kernel, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+    hipLaunchKernelGGL(kernel, dim3(grid), dim3(nth), lds, st, params, cnt, hist, cand, nq, S, HS, cap, m, k, E,
+                       flags & ~kSelRefilter, out_i, out_s, qctl, queue, rqueue, stats);
+  };
+  if (flags & kSelIlv) go(k_select_second<kSelThreadsWide, kSelPerWide>, kSelThreadsWide);
+  else go(k_select_second<kSelThreads, kSelPer>, kSelThreads);
   return hipGetLastError();
 }
 

@@ -70,7 +70,7 @@ __host__ __device__ __forceinline__ size_t radix_lds_bytes(int k) {
 // visible with a block-scope fence and barrier. `fetch(idx)` returns the score
 // of key idx (used to rebuild the float exactly, -0 and NaN payloads included).
 template <int NTH, class Fetch>
-__device__ void sort_output_row(int32_t* oi, float* os, int n, uint64_t* ent, Fetch fetch) {
+__device__ __forceinline__ void sort_output_row(int32_t* oi, float* os, int n, uint64_t* ent, Fetch fetch) {
   if (n <= 1) return;
   const int P = next_pow2(n);
   for (int i = threadIdx.x; i < P; i += NTH) ent[i] = i < n ? comp_key(os[i], (uint32_t)oi[i]) : 0ull;
@@ -90,13 +90,13 @@ __device__ void sort_output_row(int32_t* oi, float* os, int n, uint64_t* ent, Fe
 // one ordered pass keeps every key > K* and the lowest-index keys == K*.
 // Output order: ascending key index, or the total order when `sorted`.
 template <int NTH>
-__device__ void radix_select_row_at(const float* row, int n, int k, int32_t* oi, float* os, bool sorted,
+__device__ __forceinline__ void radix_select_row_at(const float* row, int n, int k, int32_t* oi, float* os, bool sorted,
                                     uint8_t* lds);
 
 // radix_select_row over keys [base, base + n) of a row whose key `base` is at
 // row[0]: the written indices are shifted by `base`.
 template <int NTH>
-__device__ void radix_select_row(const float* row, int n, int k, int32_t* oi, float* os, bool sorted,
+__device__ __forceinline__ void radix_select_row(const float* row, int n, int k, int32_t* oi, float* os, bool sorted,
                                  uint8_t* lds, int base = 0) {
   radix_select_row_at<NTH>(row, n, k, oi, os, sorted, lds);
   if (base != 0) {
@@ -108,7 +108,7 @@ __device__ void radix_select_row(const float* row, int n, int k, int32_t* oi, fl
 }
 
 template <int NTH>
-__device__ void radix_select_row_at(const float* row, int n, int k, int32_t* oi, float* os, bool sorted,
+__device__ __forceinline__ void radix_select_row_at(const float* row, int n, int k, int32_t* oi, float* os, bool sorted,
                                     uint8_t* lds) {
   uint32_t* hist = reinterpret_cast<uint32_t*>(lds);
   uint32_t* tmp = hist + 256;                // 16 words

@@ -172,17 +172,20 @@ def _oracle_rows(x, cfg, k, fi, fs, rows, xrows=None):
         check_row_tol(fi[t], fs[t], oi[j], os_[j], full[j], int(ev[tx]), k, RTOL[cfg.dtype])
 
 
-@pytest.mark.parametrize("opt,reason", [(dict(capacity=8192), 1), (dict(capacity=262144, num_bins=2), 2)],
-                         ids=["overflow", "tie-bin"])
+@pytest.mark.parametrize("opt,reason", [(dict(capacity=8192), 6), (dict(capacity=1024), 1),
+                                        (dict(capacity=262144, num_bins=2), 2)],
+                         ids=["overflow-refilter", "overflow-dense", "tie-bin"])
 def test_fallback_at_full_size_adversarial(lib, opt, reason):
-    """The adversarial 1024 x 256K workload at full size, in two forms that
-    send rows to the exact fallback for real: candidate buffers below its
+    """The adversarial 1024 x 256K workload at full size, in three forms that
+    send rows past the first select for real. Candidate buffers below its
     ~21K survivors per row (the capacity is per key split; the launch splits
-    the keys in two, ~10.6K survivors each; reason 1: buffer overflow), and
-    two bins with room for every key (reason 2: the threshold bin is too
-    large to sort).
-    Every row equals radix selection over the dense scores bit for bit;
-    evenly spaced rows meet the oracle."""
+    the keys in two, ~10.6K survivors each) overflow: with 8192 slots the
+    keys at or above each row's exact final bin fit in one list, so a second
+    filter pass gated at that bin finishes the row (reason 6); with 1024
+    slots (below k) they cannot, and the dense fallback does (reason 1).
+    Two bins with room for every key leave a threshold bin too large to sort
+    (reason 2: dense fallback). Every row equals radix selection over the
+    dense scores bit for bit; evenly spaced rows meet the oracle."""
     name = "adversarial_bf16_256k"
     cfg = workloads.CONFIGS[name]
     x = workloads.generate(cfg, seed=workloads.CONFIG_SEEDS[name])
@@ -268,3 +271,34 @@ def test_every_row_against_oracle(lib, full_fused, name, block):
     per = ALL_ROWS[name]
     rows = list(range(block * per, (block + 1) * per))
     _oracle_rows(x, cfg, cfg.k, fi, fs, rows)
+
+
+def test_chunked_prefill_1m_equals_one_launch(lib):
+    """The paper's chunked-prefill setting at 1M context (sec. 4.1, 4.2): the
+    last 8192 tokens as queries in chunks of 1024, every chunk after the first
+    sampling the previous chunk's most frequent top-k keys, and the first 2048
+    tokens again in chunks of 128; each chunk's rows equal one launch over all
+    8192 rows, bit for bit."""
+    cfg = workloads.scaled(workloads.CONFIGS["dsa_fp8_1m"], nq=8192)
+    x = workloads.generate(cfg, seed=workloads.CONFIG_SEEDS["dsa_fp8_1m"])
+    d = to_dev(x)
+    k, nk = cfg.k, cfg.nk
+    sopt = lt.make_options(sorted_output=True)
+    ri, rs = lt.indexer_topk(d["q"], d["w"], d["keys"], k, d["offsets"], d["q_scale"], d["k_scale"], options=sopt)
+    torch.cuda.synchronize()
+    ri, rs = ri.cpu().numpy(), rs.cpu().numpy()
+    for chunk, upto in ((1024, cfg.nq), (128, 2048)):
+        prev = None
+        for c0 in range(0, upto, chunk):
+            sl = slice(c0, c0 + chunk)
+            part = {n: d[n][sl].contiguous() for n in ("q", "w", "q_scale", "offsets")}
+            hint = None if prev is None else lt.sample_from_topk(prev, nk, 3 * k)
+            stats = torch.zeros((chunk, lt.LT_ROW_STATS), dtype=torch.int32, device="cuda")
+            gi, gs = lt.indexer_topk(part["q"], part["w"], d["keys"], k, part["offsets"], part["q_scale"],
+                                     d["k_scale"], options=lt.make_options(sorted_output=True, sample_keys=hint,
+                                                                           row_stats=stats))
+            torch.cuda.synchronize()
+            np.testing.assert_array_equal(gi.cpu().numpy(), ri[sl], err_msg="chunk %d at %d" % (chunk, c0))
+            np.testing.assert_array_equal(gs.cpu().numpy().view(np.uint32), rs[sl].view(np.uint32))
+            assert not np.any(stats.cpu().numpy()[:, 2] == 5)
+            prev = gi

@@ -173,3 +173,41 @@ def test_grouped_forced_paths_are_exact(lib, law, opt):
     _check_tol(x, cfg.dtype, k, mode, got[0], got[1])
     if opt.get("force_fallback"):
         assert np.all(got[2][:, 2] == 3)
+
+
+@pytest.mark.parametrize("law", [
+    # id, base config, nq, nk, k, mode
+    ("dsa_bf16_h64", "dsa_bf16_128k", 10, 9000, 256, "dsa"),
+    ("dsa_fp8_h64", "dsa_fp8_1m", 9, 30001, 2048, "dsa"),
+    ("ip_bf16_h1", "retrieval_bf16_4m", 300, 50001, 100, "ip"),
+    ("dsa_f32_h4", "tiny_fp32", 40, 9001, 256, "dsa"),
+], ids=lambda l: l[0])
+def test_overflow_second_filter_pass(lib, law):
+    """Rows whose candidate buffer overflows but whose keys at or above the
+    exact final bin fit in one list are finished by a second filter pass
+    gated at that bin (row_stats reason 6): results bit-identical to the
+    default launch, and within tolerance of the oracle. One key split. The
+    capacity comes from a first launch: fewer than k keys lie above a row's
+    final bin, so a row with k - 1 + (its threshold-bin count) <= capacity
+    < (its candidate count) must take the second pass; the capacity is the
+    value that makes the most rows do so. Other overflowed rows may take the
+    second pass or the dense fallback; rows that fit take neither."""
+    name, base, nq, nk, k, mode = law
+    cfg = workloads.scaled(workloads.CONFIGS[base], nq=nq, nk=nk)
+    x = workloads.generate(cfg, seed=14)
+    ref = _fused(x, k, mode, sorted_output=True, key_splits=1)
+    need, cand = k - 1 + ref[2][:, 3].astype(np.int64), ref[2][:, 0].astype(np.int64)
+    caps = np.unique(need)
+    hits = [int(((need <= c) & (cand > c)).sum()) for c in caps]
+    cap = int(caps[int(np.argmax(hits))])
+    must = (need <= cap) & (cand > cap)
+    assert must.sum() >= nq // 4, "too few rows would take the second pass (cap %d, candidates %s, need %s)" % (
+        cap, cand, need)
+    got = _fused(x, k, mode, sorted_output=True, key_splits=1, capacity=cap)
+    np.testing.assert_array_equal(got[0], ref[0])
+    np.testing.assert_array_equal(got[1].view(np.uint32), ref[1].view(np.uint32))
+    reasons = got[2][:, 2]
+    np.testing.assert_array_equal(reasons[cand <= cap], 0)
+    np.testing.assert_array_equal(reasons[must], 6)
+    assert np.all(np.isin(reasons[(cand > cap) & ~must], (1, 2, 6)))
+    _check_tol(x, cfg.dtype, k, mode, got[0], got[1])
