@@ -58,6 +58,54 @@ def build(verbose: bool = False) -> str:
     return OUT
 
 
+SAN_OUT = os.path.join(OBJDIR, "liblitetopk_san.so")
+
+
+def build_sanitized(verbose: bool = False) -> str:
+    """The same library with the host code of the C ABI (abi.hip: argument
+    checks, workspace sizing and carving) built under AddressSanitizer and
+    UndefinedBehaviorSanitizer; the device code and the other translation
+    units are the regular objects (built first if missing). The sanitizer
+    runtime is not linked in: a process loads it first (LD_PRELOAD of the
+    path sanitizer_runtime() returns)."""
+    os.makedirs(OBJDIR, exist_ok=True)
+    others = [os.path.join(OBJDIR, os.path.splitext(s)[0] + ".o") for s in SOURCES if s != "abi.hip"]
+    if not all(os.path.exists(o) for o in others):
+        build(verbose=verbose)
+    obj = os.path.join(OBJDIR, "abi_san.o")
+    cmd = [hipcc()] + flags() + ["-Xarch_host", "-fsanitize=address", "-Xarch_host", "-fsanitize=undefined",
+                                 "-Xarch_host", "-fno-sanitize-recover=undefined",
+                                 "-Xarch_host", "-fno-omit-frame-pointer", "-g",
+                                 "-c", os.path.join(CSRC, "abi.hip"), "-o", obj]
+    r = subprocess.run(cmd, capture_output=True, text=True)
+    if r.returncode != 0:
+        raise RuntimeError("hipcc failed for the sanitized abi.hip:\n%s\n%s" % (" ".join(cmd), r.stderr))
+    tmp = SAN_OUT + ".tmp"
+    cmd = [hipcc(), "--offload-arch=" + ARCH, "-shared", "-fPIC", "-o", tmp, obj] + others
+    r = subprocess.run(cmd, capture_output=True, text=True)
+    if r.returncode != 0:
+        raise RuntimeError("link failed:\n%s\n%s" % (" ".join(cmd), r.stderr))
+    os.replace(tmp, SAN_OUT)
+    if verbose:
+        print("built", SAN_OUT)
+    return SAN_OUT
+
+
+def sanitizer_runtime() -> str:
+    """Path of the compiler's AddressSanitizer runtime (with the
+    UndefinedBehaviorSanitizer handlers), or '' if it is not installed."""
+    r = subprocess.run([hipcc(), "-print-file-name=libclang_rt.asan-x86_64.so"], capture_output=True, text=True)
+    p = r.stdout.strip()
+    if r.returncode == 0 and os.path.isabs(p) and os.path.exists(p):
+        return p
+    base = os.path.join(os.environ.get("ROCM_PATH", "/opt/rocm"), "llvm", "lib", "clang")
+    for v in sorted(os.listdir(base)) if os.path.isdir(base) else []:
+        c = os.path.join(base, v, "lib", "linux", "libclang_rt.asan-x86_64.so")
+        if os.path.exists(c):
+            return c
+    return ""
+
+
 if __name__ == "__main__":
     build(verbose=True)
     sys.exit(0)

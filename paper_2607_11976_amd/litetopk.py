@@ -21,7 +21,9 @@ from typing import Optional, Sequence
 import torch
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(_HERE, "liblitetopk.so")
+# LT_LIBRARY names another build of the same library (the host-sanitizer
+# build that tests/test_abi_sanitized.py makes); default: the in-tree build
+LIB_PATH = os.environ.get("LT_LIBRARY") or os.path.join(_HERE, "liblitetopk.so")
 
 LT_OK, LT_EINVAL, LT_EUNSUPPORTED, LT_EWORKSPACE, LT_EHIP, LT_ESCRATCH = 0, -1, -2, -3, -4, -5
 LT_F32, LT_BF16, LT_FP8_E4M3FN = 0, 1, 2
