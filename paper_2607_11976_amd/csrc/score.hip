@@ -136,7 +136,10 @@ struct Cfg {
 #ifndef LT_FP8_VALU_PER_MFMA
 #define LT_FP8_VALU_PER_MFMA 20
 #endif
-  static constexpr int VALU_PER_MFMA = H == 64 && QW == 1 && DT == DT_BF16  ? 5
+#ifndef LT_BF16_VALU_PER_MFMA
+#define LT_BF16_VALU_PER_MFMA 5
+#endif
+  static constexpr int VALU_PER_MFMA = H == 64 && QW == 1 && DT == DT_BF16  ? LT_BF16_VALU_PER_MFMA
                                        : H == 64 && QW == 1 && DT == DT_FP8 ? LT_FP8_VALU_PER_MFMA
                                                                             : (32 * MT + KS * MT - 1) / (KS * MT);
   static_assert((QW * H) % 32 == 0, "a wave must fill whole M tiles");
@@ -1350,22 +1353,25 @@ __global__ __launch_bounds__(C::NTHREADS) void k_fused(ScoreArgs a, const RowPar
                                                        const uint32_t* qctl) {
   extern __shared__ __align__(16) uint8_t lds[];
   uint32_t* hist = reinterpret_cast<uint32_t*>(lds + C::SCAN_LDS + fused_sink_lds<C>());
+  // three words of block state after the histograms
   int* emax = reinterpret_cast<int*>(hist + C::QT * m);
   int* smin = emax + 1;
+  int* anyon = emax + 2;
   const int tile = blockIdx.x / S, split = blockIdx.x - tile * S;
   const int q0 = tile * C::QT, wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave),
             qbase = q0 + wave * C::QW;
-  // second filter pass: nothing queued, or none of this block's rows
+  // second filter pass: nothing queued
   if (rflag && qctl[1] == 0u) return;
   const bool on = threadIdx.x < C::QT && q0 + (int)threadIdx.x < a.nq && (!rflag || rflag[q0 + threadIdx.x]);
-  if (rflag && !__syncthreads_or(on)) return;
   for (int i = threadIdx.x; i < C::QT * m; i += C::NTHREADS) hist[i] = 0u;
   if (threadIdx.x == 0) {
     *emax = 0;
     *smin = a.nk;
+    *anyon = 0;
   }
   __syncthreads();
   if (on) {
+    *anyon = 1;
     const RowRange rr = row_range(a.offs, a.starts, q0 + threadIdx.x, a.nk);
     if (rr.e > rr.s) {
       atomicMax(emax, rr.e);
@@ -1373,6 +1379,7 @@ __global__ __launch_bounds__(C::NTHREADS) void k_fused(ScoreArgs a, const RowPar
     }
   }
   __syncthreads();
+  if (*anyon == 0) return;  // block-uniform: none of the block's rows is scanned (second pass)
   // the split's keys within the union of the block's rows' ranges
   const int kb = max(split * L, *smin);
   const int ke = min(min(split * L + L, a.nk), *emax);
