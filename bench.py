@@ -63,10 +63,22 @@ HBM_PEAK_GBS = 8000.0
 # (`bench.py --copy-calib 1024 --steps 3`): FETCH_SIZE reads half the bytes,
 # WRITE_SIZE all of them. A kernel change since these were taken makes them
 # stale: set the entry to None until they are taken again.
-TRAFFIC_KIB = {"dsa_bf16_128k": (293568.2, 281895.8), "dsa_fp8_1m": None,
-               "retrieval_e7_bf16_5m": (3780593.9, 36472.1), "retrieval_bf16_4m": (2587643.2, 318512.4),
-               "adversarial_bf16_256k": (149156.7, 172718.2)}
+TRAFFIC_KIB = {"dsa_bf16_128k": (293569.0, 281894.6), "dsa_fp8_1m": (549569.2, 209557.7),
+               "retrieval_e7_bf16_5m": (3780593.9, 36472.1), "retrieval_bf16_4m": None,
+               "adversarial_bf16_256k": (149383.0, 172718.4)}
 COPY_FACTOR = (0.5000, 1.0000)
+# WRITE_SIZE KiB per call of each kernel of one lt_indexer_topk call
+# ("fused": sample scores, candidate lists + histograms, the select's output)
+# and of the unfused pair (the dense score matrix, then radix select), from
+# `--profile-only W [--unfused]` under rocprofv3 --pmc WRITE_SIZE
+# (profiles/k_fused_hbm_traffic.md); divided by the calibration factor and
+# the query count they give the bytes written per query.
+WRITE_KIB = {
+    "dsa_bf16_128k": {"fused": {"k_sample": 98304.0, "k_fused": 281894.6, "k_select": 65776.4},
+                      "unfused": {"k_dense": 2097152.0, "k_radix": 70145.5}},
+    "dsa_fp8_1m": {"fused": {"k_sample": 49152.0, "k_fused": 209557.7, "k_select": 32879.8},
+                   "unfused": {"k_dense": 8388608.0, "k_radix": 55509.1}},
+}
 
 
 def visible_pairs(cfg) -> int:
@@ -357,8 +369,7 @@ def retrieval_sweep(steps: int):
     del x, q, keys, qt
     torch.cuda.empty_cache()
     ref = [p for p in points if p["corpus"] == 5000000 and p["k"] == 1024][0]
-    # counter traffic was taken with the default options only
-    kib = None if extra else TRAFFIC_KIB.get(cfg.name)
+    kib = TRAFFIC_KIB.get(cfg.name)
     traffic = None if kib is None else round(kib[0] * 1024.0 / COPY_FACTOR[0] + kib[1] * 1024.0 / COPY_FACTOR[1])
     return {"workload": cfg.name, "num_queries": cfg.nq, "dim": cfg.d, "dtype": "bf16", "mode": "ip",
             "data": "synthetic unit-normalised Gaussian passages (torch Philox, seeded); queries are corpus passages",
@@ -378,6 +389,21 @@ def algorithmic_bytes(cfg, survivors_mean: float) -> int:
     if cfg.dtype == "fp8":
         b += cfg.nk * 4 + cfg.nq * cfg.h * 4
     return int(b + survivors_mean * cfg.nq * 8)
+
+
+def written_per_query(cfg, res) -> dict:
+    """HBM bytes written per query by one call, fused and unfused: from the
+    WRITE_SIZE counters where they were taken, and as derived from the
+    survivors (8 B per candidate and per output entry; 4 B per score of the
+    dense matrix)."""
+    out = {"fused_derived": round(res["survivors_mean"] * 8 + cfg.k * 8, 1),
+           "unfused_derived": cfg.nk * 4 + cfg.k * 8}
+    w = WRITE_KIB.get(cfg.name)
+    if w is not None:
+        for side in ("fused", "unfused"):
+            out[side + "_write_size"] = round(sum(w[side].values()) * 1024.0 / COPY_FACTOR[1] / cfg.nq, 1)
+        out["source"] = "rocprofv3 WRITE_SIZE per kernel (profiles/k_fused_hbm_traffic.md)"
+    return out
 
 
 def roofline(cfg, res, extra=None):
@@ -576,9 +602,7 @@ def main():
         "fallback_rows": res["fallback_rows"],
         "sorted_output_ms_per_step": round(res["sorted_ms"], 4),
         "dsa_union": res["dsa_union"],
-        "bytes_written_per_query": {
-            "fused": round(res["survivors_mean"] * 8 + cfg.k * 8, 1),
-            "unfused": cfg.nk * 4 + cfg.k * 8},
+        "bytes_written_per_query": written_per_query(cfg, res),
     }
     if "unfused_ms" in res:
         line["unfused"] = {"ms_per_step": round(res["unfused_ms"], 4),
@@ -597,6 +621,7 @@ def main():
         if "unfused_ms" in res2:
             m["unfused_ms_per_step"] = round(res2["unfused_ms"], 4)
             m["unfused_same_sets"] = res2["unfused_same_sets"]
+        m["bytes_written_per_query"] = written_per_query(cfg2, res2)
         line["ctx_1m"] = m
     if not args.no_others:
         line["other_configs"] = [other_config(n, unf and not args.no_unfused)
@@ -610,6 +635,13 @@ def main():
             "adversarial_bf16_256k", False, extra={"capacity": 8192},
             note="candidate buffers below the survivors: every row overflows and is completed by a second "
                  "filter pass gated at its exact final bin (stage 'fallback'; row_stats reason 6)"))
+        # ... and with buffers below k (1024 per split): no second pass can
+        # hold the keys at or above the final bin, so every row is re-scored
+        # densely and radix-selected (the exact fallback, reason 1)
+        line["other_configs"].append(other_config(
+            "adversarial_bf16_256k", False, extra={"capacity": 1024},
+            note="candidate buffers below k: every row takes the exact dense fallback (stage 'fallback'; "
+                 "row_stats reason 1)"))
         print("[bench] other workloads done", file=sys.stderr, flush=True)
     if not args.no_chunked:
         line["chunked_prefill"] = [chunked_prefill(b, c, lbl) for b, c, lbl in CHUNK_CONTEXTS]
