@@ -19,7 +19,7 @@ static __device__ __align__(256) uint8_t scratch[LT_STATIC_SCRATCH_BYTES];
 namespace {
 
 constexpr int kDefaultBins = 256;
-constexpr int kFallbackGridFused = 64;      // rows re-scored concurrently (scratch rows)
+constexpr size_t kFallbackScratchBudget = 2ull << 30;  // bytes of scratch the dense fallback may take
 constexpr int kFallbackGridScores = 256;
 constexpr int kTargetBlocks = 256;          // one block per CU before key splitting stops
 constexpr int kMinSplitKeys = 512;          // shortest key split the automatic choice makes
@@ -49,6 +49,27 @@ struct Layout {
   size_t qctl, queue, rqueue, rflag, params, list, samp, cnt, hist, cand, gate, scratch, total;
 };
 
+// The dense fallback's blocks and the rows of one query tile each block
+// re-scores per pass (one fp32 row of Nk scores per (block, batch slot) of
+// scratch). Up to 256 rows: one row per block, one block per row. More rows:
+// one block per CU, each taking up to kMaxFallbackBatch rows of a tile per
+// pass, so that a tile whose rows all fall back is scored once or twice
+// instead of once per row. Within the scratch budget: fewer rows per pass,
+// then fewer blocks (down to 64).
+struct FallbackShape {
+  int grid, batch;
+};
+FallbackShape fallback_shape(int nq, int nk) {
+  const size_t row = (size_t)std::max(nk, 1) * 4;
+  FallbackShape f{std::max(1, std::min(nq, 256)), 1};
+  if (nq > 256) f.batch = std::min(kMaxFallbackBatch, (nq + 255) / 256);
+  if ((size_t)f.grid * f.batch * row > kFallbackScratchBudget)
+    f.batch = (int)std::max<size_t>(1, kFallbackScratchBudget / ((size_t)f.grid * row));
+  if ((size_t)f.grid * f.batch * row > kFallbackScratchBudget)
+    f.grid = (int)std::max<size_t>(std::min(f.grid, 64), kFallbackScratchBudget / row);
+  return f;
+}
+
 Layout carve(int nq, int nk, const Resolved& r, bool fused) {
   Layout L{};
   size_t off = 0;
@@ -60,7 +81,7 @@ Layout carve(int nq, int nk, const Resolved& r, bool fused) {
   L.qctl = take(256);
   L.queue = take((size_t)nq * 4);
   L.rqueue = fused ? take((size_t)nq * 4) : 0;  // rows of the second filter pass
-  L.rflag = fused ? take((size_t)nq * 4) : 0;
+  L.rflag = fused ? take((size_t)nq * 8) : 0;  // second-pass flags [nq], then dense-fallback flags [nq]
   L.params = take((size_t)nq * sizeof(RowParam));
   L.list = take((size_t)r.ns * 4);
   L.samp = fused ? take((size_t)nq * r.ns * 4) : 0;
@@ -68,7 +89,8 @@ Layout carve(int nq, int nk, const Resolved& r, bool fused) {
   L.hist = take((size_t)nq * r.HS * r.m * 4);
   L.cand = take((size_t)nq * r.S * r.cap * 8);
   L.gate = fused ? take((size_t)nq * 8) : 0;  // published bins: [nq] ints (wide), [nq][8] bytes
-  L.scratch = fused ? take((size_t)kFallbackGridFused * nk * 4) : 0;
+  const FallbackShape fs = fallback_shape(nq, nk);
+  L.scratch = fused ? take((size_t)fs.grid * fs.batch * nk * 4) : 0;
   L.total = off;
   return L;
 }
@@ -334,11 +356,12 @@ int lt_indexer_topk(const void* q, const float* q_scale, const float* w, const v
         hipSuccess)
       return hip_status(e);
     if ((e = launch_select_second(params, cnt, hist, cand, nq, r.S, r.HS, r.cap, r.m, k, r.E, sel_flags, out_idx,
-                                  out_scores, qctl, queue, rqueue, r.stats, st)) != hipSuccess)
+                                  out_scores, qctl, queue, rqueue, rflag, r.stats, st)) != hipSuccess)
       return hip_status(e);
   }
-  if ((e = launch_fused_fallback(a, k, fb_flags, qctl, queue, scratch, kFallbackGridFused, out_idx, out_scores,
-                                 st)) != hipSuccess)
+  const FallbackShape fs = fallback_shape(nq, nk);
+  if ((e = launch_fused_fallback(a, k, fb_flags, qctl, queue, rflag + nq, fs.batch, scratch, fs.grid, out_idx,
+                                 out_scores, st)) != hipSuccess)
     return hip_status(e);
   record(r, LT_NUM_STAGE_EVENTS - 1, st);
   return LT_OK;

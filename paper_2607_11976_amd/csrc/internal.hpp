@@ -16,7 +16,9 @@ hipError_t launch_init(uint32_t* qctl, hipStream_t st);
 // (NULL = num_keys) and `starts` the starts (NULL = 0).
 // With stats non-NULL, also writes row_stats fields 4..11 (the sample's
 // initial bin and k-th score, the bin map, the bins in use).
-// rflag (or NULL): per-row flags of the second filter pass, cleared here.
+// rflag (or NULL): [2 * nq] per-row flags, cleared here: [0, nq) the second
+// filter pass, [nq, 2 nq) the dense fallback (set by the select when it
+// queues a row there).
 hipError_t launch_range(bool from_scores, const float* src, int64_t stride, int nq, int nk,
                         const int32_t* offs, const int32_t* starts, const int32_t* list, int ns, int m, int k,
                         RowParam* params, int32_t* stats, int32_t* rflag, hipStream_t st);
@@ -36,8 +38,8 @@ hipError_t launch_select(RowParam* params, const uint32_t* cnt, const uint32_t* 
 // The select of the rows in rqueue after their second filter pass.
 hipError_t launch_select_second(RowParam* params, const uint32_t* cnt, const uint32_t* hist, const int2* cand,
                                 int nq, int S, int HS, int cap, int m, int k, int E, uint32_t flags, int32_t* out_i,
-                                float* out_s, uint32_t* qctl, int32_t* queue, int32_t* rqueue, int32_t* stats,
-                                hipStream_t st);
+                                float* out_s, uint32_t* qctl, int32_t* queue, int32_t* rqueue, int32_t* rflag,
+                                int32_t* stats, hipStream_t st);
 hipError_t launch_fallback_scores(const float* scores, int64_t stride, int nk, const int32_t* offs,
                                   const int32_t* starts, int k, uint32_t flags, const uint32_t* qctl,
                                   const int32_t* queue, int32_t* out_i, float* out_s, int grid, hipStream_t st);
@@ -98,9 +100,14 @@ hipError_t launch_dense_scores(const ScoreArgs& a, float* out, int64_t ld, hipSt
 hipError_t launch_fused_scan(const ScoreArgs& a, const RowParam* params, int S, int L, int cap, int m,
                              int k, int* pub, uint32_t* cnt, uint32_t* hist, int2* cand, const int32_t* rflag,
                              const uint32_t* qctl, hipStream_t st);
-// Exact fallback for queued rows: dense re-score into scratch [grid, nk], then radix select.
+// Exact fallback for queued rows: dense re-score into scratch
+// [grid, batch, nk], then radix select. fbflag (or NULL) [nq]: 1 for the
+// queued rows; a block that takes a row also claims up to batch - 1 other
+// queued rows of the same query tile (1 -> 2) and re-scores them in the same
+// pass.
+constexpr int kMaxFallbackBatch = 8;  // rows of one query tile re-scored in one fallback pass
 hipError_t launch_fused_fallback(const ScoreArgs& a, int k, uint32_t flags, const uint32_t* qctl,
-                                 const int32_t* queue, float* scratch, int grid, int32_t* out_i,
+                                 const int32_t* queue, int32_t* fbflag, int batch, float* scratch, int grid, int32_t* out_i,
                                  float* out_s, hipStream_t st);
 
 // ---- wide-vector scan (wide.hip): bf16, one head, long vectors ----

@@ -761,11 +761,15 @@ struct DenseSink {
   }
 };
 
-// Writes only the scores of one query row (the fallback's re-score).
+// Writes the scores of the fallback's batch of rows: query t of the block's
+// tile goes to out[slot * ld + position] when slot = smap[t - q0] >= 0 (the
+// map is in LDS, [QT] entries).
 template <class C>
 struct RowSink {
   float* out;
-  int qbase, target;
+  int64_t ld;
+  const int8_t* smap;
+  int qbase, q0;
   __device__ void consume(int, int k0, int kend, const float (&sc)[C::NI], bool live) {
     const int l = lane_id(), h = l >> 5, r32 = l & 31;
 #pragma unroll
@@ -773,7 +777,8 @@ struct RowSink {
       const int q = h ? C::item_q(it, 1) : C::item_q(it, 0);
       const int nt = h ? C::item_nt(it, 1) : C::item_nt(it, 0);
       const int pos = k0 + nt * 32 + r32;
-      if (live && qbase + q == target && pos < kend) out[pos] = sc[it];
+      const int slot = smap[qbase + q - q0];
+      if (live && slot >= 0 && pos < kend) out[slot * ld + pos] = sc[it];
     }
   }
 };
@@ -1407,27 +1412,71 @@ __global__ __launch_bounds__(C::NTHREADS) void k_fused(ScoreArgs a, const RowPar
   sink.finish(cnt, hist_out);
 }
 
+// LDS bytes of the fallback's batch: the slot map of the tile's rows and the
+// batch's rows.
+template <class C>
+constexpr int fallback_meta_lds() { return ((C::QT + 15) & ~15) + kMaxFallbackBatch * 4 + 16; }
+
 template <class C>
 __global__ __launch_bounds__(C::NTHREADS) void k_fused_fallback(ScoreArgs a, int k, uint32_t flags,
                                                                 const uint32_t* qctl, const int32_t* queue,
+                                                                int32_t* fbflag, int batch, size_t meta_off,
                                                                 float* scratch, int32_t* out_i, float* out_s) {
   extern __shared__ __align__(16) uint8_t lds[];
+  int8_t* smap = reinterpret_cast<int8_t*>(lds + meta_off);            // [QT]
+  int* brow = reinterpret_cast<int*>(lds + meta_off + ((C::QT + 15) & ~15));  // [kMaxFallbackBatch]
+  int* bn = brow + kMaxFallbackBatch;
   const uint32_t n = qctl[0];
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
   for (uint32_t r = blockIdx.x; r < n; r += gridDim.x) {
     const int row = queue[r];
     const int q0 = (row / C::QT) * C::QT, qbase = q0 + wave * C::QW;
-    const RowRange rr = row_range(a.offs, a.starts, row, a.nk);
-    float* srow = scratch + (int64_t)blockIdx.x * a.nk;
+    // the batch: this row unless another block took it with its own tile,
+    // then other queued rows of the tile that no block has taken yet
+    if (threadIdx.x == 0) {
+      int nb = 0;
+      if (!fbflag || atomicExch(&fbflag[row], 2) == 1) {
+        brow[nb++] = row;
+        if (fbflag) {
+          const int qe = min(q0 + C::QT, a.nq);
+          for (int t = q0; t < qe && nb < batch; ++t)
+            if (t != row && atomicCAS(&fbflag[t], 1, 2) == 1) brow[nb++] = t;
+        }
+      }
+      *bn = nb;
+    }
+    for (int i = threadIdx.x; i < C::QT; i += C::NTHREADS) smap[i] = -1;
+    __syncthreads();
+    const int nb = *bn;
+    if (nb == 0) {  // block-uniform
+      __syncthreads();  // every thread has read *bn before the next row rewrites it
+      continue;
+    }
+    if (threadIdx.x < nb) smap[brow[threadIdx.x] - q0] = (int8_t)threadIdx.x;
+    // scan the union of the batch rows' ranges; each row selects from its own
+    int kb = a.nk, ke = 0;
+    for (int j = 0; j < nb; ++j) {
+      const RowRange rr = row_range(a.offs, a.starts, brow[j], a.nk);
+      if (rr.e > rr.s) {
+        kb = min(kb, rr.s);
+        ke = max(ke, rr.e);
+      }
+    }
+    __syncthreads();
+    float* sblk = scratch + (int64_t)blockIdx.x * batch * a.nk;
     WaveQ<C> wq;
     load_q<C>(wq, a, qbase);
-    RowSink<C> sink{srow, qbase, row};
-    wg_scan<C>(a, SrcContig{}, rr.s, rr.e, lds, wq, sink);
+    RowSink<C> sink{sblk, a.nk, smap, qbase, q0};
+    wg_scan<C>(a, SrcContig{}, kb, ke, lds, wq, sink);
     __threadfence_block();
     __syncthreads();
-    radix_select_row<C::NTHREADS>(srow + rr.s, rr.e - rr.s, k, out_i + (int64_t)row * k, out_s + (int64_t)row * k,
-                                  flags & LT_SORTED_OUTPUT, lds, rr.s);
-    __syncthreads();
+    for (int j = 0; j < nb; ++j) {
+      const int t = brow[j];
+      const RowRange rr = row_range(a.offs, a.starts, t, a.nk);
+      radix_select_row<C::NTHREADS>(sblk + (int64_t)j * a.nk + rr.s, rr.e - rr.s, k, out_i + (int64_t)t * k,
+                                    out_s + (int64_t)t * k, flags & LT_SORTED_OUTPUT, lds, rr.s);
+      __syncthreads();
+    }
   }
 }
 
@@ -1556,8 +1605,8 @@ hipError_t launch_fused_scan(const ScoreArgs& a, const RowParam* params, int S, 
 }
 
 hipError_t launch_fused_fallback(const ScoreArgs& a, int k, uint32_t flags, const uint32_t* qctl,
-                                 const int32_t* queue, float* scratch, int grid, int32_t* out_i, float* out_s,
-                                 hipStream_t st) {
+                                 const int32_t* queue, int32_t* fbflag, int batch, float* scratch, int grid,
+                                 int32_t* out_i, float* out_s, hipStream_t st) {
   if (wide_shape(a.dtype, a.mode, a.h, a.d).supported)
     return launch_wide_fallback(a, k, flags, qctl, queue, scratch, grid, out_i, out_s, st);
   hipError_t err = hipErrorInvalidValue;
@@ -1565,10 +1614,13 @@ hipError_t launch_fused_fallback(const ScoreArgs& a, int k, uint32_t flags, cons
     size_t lds = C::SCAN_LDS;
     const size_t rl = radix_lds_bytes(k);
     if (rl > lds) lds = rl;
+    const size_t meta = (lds + 15) & ~(size_t)15;
+    lds = meta + fallback_meta_lds<C>();
     if (lds > 65536)
       (void)hipFuncSetAttribute((const void*)k_fused_fallback<C>, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+    const int b = batch < 1 ? 1 : (batch > kMaxFallbackBatch ? kMaxFallbackBatch : batch);
     hipLaunchKernelGGL(k_fused_fallback<C>, dim3(grid), dim3(C::NTHREADS), lds, st, a, k, flags, qctl, queue,
-                       scratch, out_i, out_s);
+                       fbflag, b, meta, scratch, out_i, out_s);
     err = hipGetLastError();
   });
   return err;

@@ -62,7 +62,12 @@ __global__ __launch_bounds__(NTH) void k_range(const float* src, int64_t stride,
   const float* rp = src + (int64_t)row * stride;
 
   for (int b = threadIdx.x; b < kMaxBins; b += NTH) hist[b] = 0u;
-  if (rflag && threadIdx.x == 0) rflag[row] = 0;
+  // the row's flags of the second filter pass (rflag[row]) and of the dense
+  // fallback (rflag[nq + row])
+  if (rflag && threadIdx.x == 0) {
+    rflag[row] = 0;
+    rflag[nq + row] = 0;
+  }
   float mn = __builtin_inff(), mx = -__builtin_inff();
   uint32_t nvis = 0;
   for (int base = 0; base < ns; base += NTH * kRangeUnroll) {
@@ -323,6 +328,7 @@ __device__ __forceinline__ void select_row(int row, RowParam* params, const uint
     if (tid == 0) {
       uint32_t slot = atomicAdd(&qctl[0], 1u);
       queue[slot] = row;
+      if (rflag) rflag[nq + row] = 1;  // queued for the dense fallback
       if (stats) {
         int32_t* st = stats + (int64_t)row * LT_ROW_STATS;
         if (!(flags & kSelSecond)) st[0] = (int32_t)total_c;
@@ -539,11 +545,11 @@ template <int NTH, int PER>
 __global__ __launch_bounds__(NTH) void k_select_second(
     RowParam* params, const uint32_t* cnt, const uint32_t* hist, const int2* cand, int nq,
     int S, int HS, int cap, int m, int k, int E, uint32_t flags, int32_t* out_i, float* out_s,
-    uint32_t* qctl, int32_t* queue, int32_t* rqueue, int32_t* stats) {
+    uint32_t* qctl, int32_t* queue, int32_t* rqueue, int32_t* rflag, int32_t* stats) {
   const uint32_t n = qctl[1];
   for (uint32_t i = blockIdx.x; i < n; i += gridDim.x) {
     select_row<NTH, PER>(rqueue[i], params, cnt, hist, cand, nq, S, HS, cap, m, k, E, flags | kSelSecond, out_i,
-                         out_s, qctl, queue, rqueue, nullptr, stats);
+                         out_s, qctl, queue, rqueue, rflag, stats);
     __syncthreads();
   }
 }
@@ -644,7 +650,8 @@ hipError_t launch_select(RowParam* params, const uint32_t* cnt, const uint32_t* 
 
 hipError_t launch_select_second(RowParam* params, const uint32_t* cnt, const uint32_t* hist, const int2* cand,
                                 int nq, int S, int HS, int cap, int m, int k, int E, uint32_t flags, int32_t* out_i,
-                                float* out_s, uint32_t* qctl, int32_t* queue, int32_t* rqueue, int32_t* stats,
+                                float* out_s, uint32_t* qctl, int32_t* queue, int32_t* rqueue, int32_t* rflag,
+                                int32_t* stats,
                                 hipStream_t st) {
   const int grid = nq < kSecondSelectGrid ? nq : kSecondSelectGrid;
   if (grid == 0) return hipSuccess;
@@ -652,7 +659,7 @@ hipError_t launch_select_second(RowParam* params, const uint32_t* cnt, const uin
     const size_t lds = select_ent_offset(nth) + (size_t)E * 8;
     if (lds > 65536) (void)hipFuncSetAttribute((const void*)kernel, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
     hipLaunchKernelGGL(kernel, dim3(grid), dim3(nth), lds, st, params, cnt, hist, cand, nq, S, HS, cap, m, k, E,
-                       flags & ~kSelRefilter, out_i, out_s, qctl, queue, rqueue, stats);
+                       flags & ~kSelRefilter, out_i, out_s, qctl, queue, rqueue, rflag, stats);
   };
   if (flags & kSelIlv) go(k_select_second<kSelThreadsWide, kSelPerWide>, kSelThreadsWide);
   else go(k_select_second<kSelThreads, kSelPer>, kSelThreads);
