@@ -64,7 +64,7 @@ HBM_PEAK_GBS = 8000.0
 # WRITE_SIZE all of them. A kernel change since these were taken makes them
 # stale: set the entry to None until they are taken again.
 TRAFFIC_KIB = {"dsa_bf16_128k": (293569.0, 281894.6), "dsa_fp8_1m": (549569.2, 209557.7),
-               "retrieval_e7_bf16_5m": (3780593.9, 36472.1), "retrieval_bf16_4m": None,
+               "retrieval_e7_bf16_5m": (3780593.9, 36472.1), "retrieval_bf16_4m": (2614471.4, 319192.2),
                "adversarial_bf16_256k": (149383.0, 172718.4)}
 COPY_FACTOR = (0.5000, 1.0000)
 # WRITE_SIZE KiB per call of each kernel of one lt_indexer_topk call
