@@ -211,3 +211,38 @@ def test_overflow_second_filter_pass(lib, law):
     np.testing.assert_array_equal(reasons[must], 6)
     assert np.all(np.isin(reasons[(cand > cap) & ~must], (1, 2, 6)))
     _check_tol(x, cfg.dtype, k, mode, got[0], got[1])
+
+
+@pytest.mark.parametrize("law", [
+    # id, base config, nq, boundary row b, k, capacity, mode
+    ("dsa_bf16_h64", "dsa_bf16_128k", 600, 195, 400, 300, "dsa"),
+    ("dsa_fp8_h64", "dsa_fp8_1m", 520, 99, 256, 200, "dsa"),
+    ("ip_bf16_h1", "retrieval_bf16_4m", 700, 77, 300, 250, "ip"),
+], ids=lambda l: l[0])
+def test_dense_fallback_batches_rows_of_a_tile(lib, law):
+    """More than 256 queued rows make the dense fallback take several queued
+    rows of one query tile per pass (ceil(Nq / 256) of them). Causal rows see
+    Nk - Nq + 1 + t keys, with Nk chosen so that rows t > b see more than the
+    capacity: with k above the capacity those rows overflow and go to the
+    dense fallback (reason 1), the others return every visible key, so the
+    query tile around row b holds queued and unqueued rows together. Every
+    row equals radix selection over the dense scores bit for bit (sorted),
+    and evenly spaced rows meet the oracle."""
+    name, base, nq, b, k, cap, mode = law
+    nk = cap + nq - 1 - b
+    assert nk % 4 == 0, "the dense score rows must stay 16-byte aligned"
+    cfg = workloads.scaled(workloads.CONFIGS[base], nq=nq, nk=nk)
+    x = workloads.generate(cfg, seed=23)
+    if x["offsets"] is None:
+        x["offsets"] = torch.from_numpy(workloads.causal_offsets(nq, nk))
+    gi, gs, st = _fused(x, k, mode, sorted_output=True, key_splits=1, capacity=cap)
+    reasons = st[:, 2]
+    np.testing.assert_array_equal(reasons, np.where(np.arange(nq) > b, 1, 0))
+    d = to_dev(x)
+    dense = lt.indexer_scores(d["q"], d["w"], d["keys"], d["q_scale"], d["k_scale"], mode=mode)
+    ri, rs = lt.topk_radix(dense, k, causal_offsets=d["offsets"], sorted_output=True)
+    torch.cuda.synchronize()
+    np.testing.assert_array_equal(gi, ri.cpu().numpy())
+    np.testing.assert_array_equal(gs.view(np.uint32), rs.cpu().numpy().view(np.uint32))
+    rows = sorted(set(np.linspace(0, nq - 1, 24).round().astype(int).tolist()) | {b, b + 1})
+    _check_tol(x, cfg.dtype, k, mode, gi, gs, rows=rows)
