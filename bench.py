@@ -98,6 +98,50 @@ def timed_steps(fn, steps, warmup):
     return (time.perf_counter() - t0) * 1e3 / steps
 
 
+def vendor_gemm(dtype: str, n: int = 16384, reps: int = 10) -> dict:
+    """The matrix throughput the vendor's GEMM library reaches on this GPU,
+    for context next to the roofline: a square n^3 GEMM through
+    torch.matmul (hipBLASLt; bf16) or torch._scaled_mm (fp8 E4M3FN, unit
+    scales), timed with events after three warm-up calls."""
+    a = torch.randn(n, n, device="cuda", dtype=torch.bfloat16)
+    b = torch.randn(n, n, device="cuda", dtype=torch.bfloat16)
+    if dtype == "fp8":
+        a8 = a.to(torch.float8_e4m3fn)
+        b8 = b.to(torch.float8_e4m3fn).t().contiguous().t()
+        one = torch.ones((), device="cuda", dtype=torch.float32)
+        fn = lambda: torch._scaled_mm(a8, b8, scale_a=one, scale_b=one, out_dtype=torch.bfloat16)  # noqa: E731
+        what = "torch._scaled_mm fp8 e4m3 %d^3" % n
+    else:
+        fn = lambda: torch.matmul(a, b)  # noqa: E731
+        what = "torch.matmul bf16 %d^3 (hipBLASLt)" % n
+    for _ in range(3):
+        fn()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(reps):
+        fn()
+    e1.record()
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / reps
+    tf = 2.0 * n ** 3 / (ms * 1e-3) / 1e12
+    del a, b
+    torch.cuda.empty_cache()
+    return {"kernel": what, "tflops": round(tf, 1)}
+
+
+def with_vendor(roof: dict, dtype: str) -> dict:
+    """Adds the vendor GEMM's throughput on this GPU and the scan's fraction of it."""
+    try:
+        v = vendor_gemm(dtype)
+    except Exception as ex:  # pragma: no cover - context only
+        roof["vendor_gemm"] = {"error": str(ex)[:200]}
+        return roof
+    v["frac_of_peak"] = round(v["tflops"] / roof["peak"], 4)
+    roof["vendor_gemm"] = v
+    roof["frac_of_vendor_gemm"] = round(roof["achieved"] / v["tflops"], 4)
+    return roof
+
+
 def step_summary(res) -> dict:
     """Per-call device times of the timed calls (warm caches) and of calls
     after a cache flush (cold), in milliseconds."""
@@ -594,7 +638,7 @@ def main():
         "config": {"workload": "dsa_bf16_128k", "num_queries": cfg.nq, "num_keys": cfg.nk, "heads": cfg.h,
                    "head_dim": cfg.d, "k": cfg.k, "causal": cfg.causal, "visible_pairs": res["pairs"],
                    "parallelism": "single GPU"},
-        "roofline": roofline(cfg, res),
+        "roofline": with_vendor(roofline(cfg, res), "bf16"),
         "stages_ms": {k: round(v, 4) for k, v in res["stages"].items()},
         "call_ms": step_summary(res),
         "survivors_per_row": {"mean": round(res["survivors_mean"], 1), "max": res["survivors_max"],
@@ -614,7 +658,7 @@ def main():
         print("[bench] dsa_fp8_1m: %.3f ms/step" % res2["ms"], file=sys.stderr, flush=True)
         m = {"workload": "dsa_fp8_1m", "dtype": "fp8", "ms_per_step": round(res2["ms"], 4),
              "value": res2["pairs"] / (res2["ms"] * 1e-3), "unit": "pairs/s", "visible_pairs": res2["pairs"],
-             "roofline": roofline(cfg2, res2), "stages_ms": {k: round(v, 4) for k, v in res2["stages"].items()},
+             "roofline": with_vendor(roofline(cfg2, res2), "fp8"), "stages_ms": {k: round(v, 4) for k, v in res2["stages"].items()},
              "call_ms": step_summary(res2),
              "survivors_per_row_mean": round(res2["survivors_mean"], 1), "fallback_rows": res2["fallback_rows"],
              "sorted_output_ms_per_step": round(res2["sorted_ms"], 4)}
