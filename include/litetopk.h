@@ -307,8 +307,12 @@ int lt_dsa_union(const int32_t* topk_idx, int64_t ld, int32_t num_queries, int32
 
 /* ---- timing helpers ------------------------------------------------------- */
 
-/* Thin wrappers over hipEventCreate / hipEventDestroy / hipEventElapsedTime /
-   hipEventRecord / hipEventSynchronize for callers without a HIP binding. */
+/* Thin wrappers over hipEventCreateWithFlags / hipEventDestroy /
+   hipEventElapsedTime / hipEventRecord / hipEventSynchronize for callers
+   without a HIP binding. The events are for timing only: they are created
+   with hipEventDisableSystemFence, so recording one between two kernels adds
+   no cache write-back, and waiting on one does not make device writes
+   visible to the host (synchronise the stream for that). */
 int lt_event_create(void** event);
 int lt_event_destroy(void* event);
 int lt_event_record(void* event, void* stream);

@@ -495,8 +495,11 @@ int lt_dsa_union(const int32_t* idx, int64_t ld, int32_t nq, int32_t k, int32_t 
 
 int lt_event_create(void** ev) {
   if (!ev) return LT_EINVAL;
+  // timing only: no system-scope fence when the event completes, so that
+  // recording one between two kernels does not write back and invalidate
+  // the caches in between (which would show up as a gap in the timing)
   hipEvent_t e;
-  if (hipEventCreate(&e) != hipSuccess) return LT_EHIP;
+  if (hipEventCreateWithFlags(&e, hipEventDisableSystemFence) != hipSuccess) return LT_EHIP;
   *ev = (void*)e;
   return LT_OK;
 }
