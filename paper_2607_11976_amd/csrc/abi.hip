@@ -33,7 +33,7 @@ constexpr int kSharedSample = 65536;        // default sample of the shared-row 
 inline size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 
 struct Resolved {
-  int m, ns, cap, S, L, E;
+  int k, m, ns, cap, S, L, E;
   int HS;                  // histograms per row: S, or 1 when shared by the splits
   bool shared;             // the wide scan: one histogram and threshold per row
   uint32_t flags;
@@ -46,23 +46,24 @@ struct Resolved {
 };
 
 struct Layout {
-  size_t qctl, queue, rqueue, rflag, params, list, samp, cnt, hist, cand, gate, scratch, total;
+  size_t qctl, queue, rqueue, rflag, params, list, samp, cnt, hist, cand, gate, scratch, fbcand, total;
 };
 
-// The dense fallback's blocks and the rows of one query tile each block
-// re-scores per pass (one fp32 row of Nk scores per (block, batch slot) of
-// scratch). Up to 256 rows: one row per block, one block per row. More rows:
-// one block per CU, each taking up to kMaxFallbackBatch rows of a tile per
-// pass, so that a tile whose rows all fall back is scored once or twice
-// instead of once per row. Within the scratch budget: fewer rows per pass,
-// then fewer blocks (down to 64).
+// The dense fallback's scratch, in fp32 rows of Nk scores: in whole-row mode
+// `grid` blocks re-score `batch` rows of one query tile per pass, each into
+// its own scratch rows. Up to kFallbackGrid rows: one row per block. More
+// rows: kFallbackGrid blocks, each taking up to kMaxFallbackBatch rows of a
+// tile per pass, so that a tile whose rows all fall back is scored once or
+// twice instead of once per row. Within the scratch budget: fewer rows per
+// pass, then fewer blocks (down to 64). Split mode (few queued rows, each
+// row's keys over many blocks) takes one of the same rows per queued row.
 struct FallbackShape {
   int grid, batch;
 };
 FallbackShape fallback_shape(int nq, int nk) {
   const size_t row = (size_t)std::max(nk, 1) * 4;
-  FallbackShape f{std::max(1, std::min(nq, 256)), 1};
-  if (nq > 256) f.batch = std::min(kMaxFallbackBatch, (nq + 255) / 256);
+  FallbackShape f{std::max(1, std::min(nq, kFallbackGrid)), 1};
+  if (nq > kFallbackGrid) f.batch = std::min(kMaxFallbackBatch, (nq + kFallbackGrid - 1) / kFallbackGrid);
   if ((size_t)f.grid * f.batch * row > kFallbackScratchBudget)
     f.batch = (int)std::max<size_t>(1, kFallbackScratchBudget / ((size_t)f.grid * row));
   if ((size_t)f.grid * f.batch * row > kFallbackScratchBudget)
@@ -78,7 +79,7 @@ Layout carve(int nq, int nk, const Resolved& r, bool fused) {
     off = align256(off + bytes);
     return o;
   };
-  L.qctl = take(256);
+  L.qctl = take((size_t)kQctlWords * 4);
   L.queue = take((size_t)nq * 4);
   L.rqueue = fused ? take((size_t)nq * 4) : 0;  // rows of the second filter pass
   L.rflag = fused ? take((size_t)nq * 8) : 0;  // second-pass flags [nq], then dense-fallback flags [nq]
@@ -91,6 +92,9 @@ Layout carve(int nq, int nk, const Resolved& r, bool fused) {
   L.gate = fused ? take((size_t)nq * 8) : 0;  // published bins: [nq] ints (wide), [nq][8] bytes
   const FallbackShape fs = fallback_shape(nq, nk);
   L.scratch = fused ? take((size_t)fs.grid * fs.batch * nk * 4) : 0;
+  // split fallback: the chunks' top-k candidates, (index, score) arrays of
+  // kFallbackGrid * k entries each
+  L.fbcand = fused ? take((size_t)kFallbackGrid * r.k * 8) : 0;
   L.total = off;
   return L;
 }
@@ -111,6 +115,7 @@ void resolve_common(const lt_options* o, int k, Resolved& r) {
   r.seed = o->seed;
   r.ev = o->stage_events;
   r.stats = o->row_stats;
+  r.k = k;
   r.E = select_entries(k);
   r.shared = false;
   r.keys_in = o->sample_keys;
@@ -321,6 +326,8 @@ int lt_indexer_topk(const void* q, const float* q_scale, const float* w, const v
   uint32_t* hist = reinterpret_cast<uint32_t*>(ws + L.hist);
   int2* cand = reinterpret_cast<int2*>(ws + L.cand);
   float* scratch = reinterpret_cast<float*>(ws + L.scratch);
+  int32_t* fbc_idx = reinterpret_cast<int32_t*>(ws + L.fbcand);
+  float* fbc_score = reinterpret_cast<float*>(ws + L.fbcand + (size_t)kFallbackGrid * k * 4);
   int* gate = reinterpret_cast<int*>(ws + L.gate);
   int32_t* rqueue = reinterpret_cast<int32_t*>(ws + L.rqueue);
   int32_t* rflag = reinterpret_cast<int32_t*>(ws + L.rflag);
@@ -360,8 +367,8 @@ int lt_indexer_topk(const void* q, const float* q_scale, const float* w, const v
       return hip_status(e);
   }
   const FallbackShape fs = fallback_shape(nq, nk);
-  if ((e = launch_fused_fallback(a, k, fb_flags, qctl, queue, rflag + nq, fs.batch, scratch, fs.grid, out_idx,
-                                 out_scores, st)) != hipSuccess)
+  if ((e = launch_fused_fallback(a, k, fb_flags, qctl, queue, rflag + nq, fs.batch, fs.grid * fs.batch, scratch,
+                                 fbc_idx, fbc_score, out_idx, out_scores, st)) != hipSuccess)
     return hip_status(e);
   record(r, LT_NUM_STAGE_EVENTS - 1, st);
   return LT_OK;

@@ -100,15 +100,46 @@ hipError_t launch_dense_scores(const ScoreArgs& a, float* out, int64_t ld, hipSt
 hipError_t launch_fused_scan(const ScoreArgs& a, const RowParam* params, int S, int L, int cap, int m,
                              int k, int* pub, uint32_t* cnt, uint32_t* hist, int2* cand, const int32_t* rflag,
                              const uint32_t* qctl, hipStream_t st);
-// Exact fallback for queued rows: dense re-score into scratch
-// [grid, batch, nk], then radix select. fbflag (or NULL) [nq]: 1 for the
-// queued rows; a block that takes a row also claims up to batch - 1 other
-// queued rows of the same query tile (1 -> 2) and re-scores them in the same
-// pass.
+// Exact fallback for queued rows (queue, length qctl[0]): dense re-score
+// into scratch rows of nk floats (`slots` of them), then radix select. Both
+// fallback kernels run kFallbackGrid blocks in one of two modes, chosen on
+// the device from the queue length n:
+// * split (fallback_chunks(...) > 1: few rows, each with its own scratch
+//   row): the visible keys of every queued row are cut into that many chunks,
+//   one block per (row, chunk), which also selects its chunk's top-k into
+//   the candidate arrays; the block that completes a row's last chunk
+//   (counter qctl[kQctlDone + entry]) selects the row from its chunks'
+//   candidates.
+// * whole rows: blocks below slots / batch take queue entries from the
+//   cursor qctl[kQctlCursor] and re-score whole rows into their own scratch
+//   rows [blockIdx][batch][nk]. fbflag (or NULL) [nq]: 1 for the queued rows;
+//   a block that takes a row also claims up to batch - 1 other queued rows of
+//   the same query tile (1 -> 2) and re-scores them in the same pass.
+// qctl words: [0] fallback queue length, [1] second-pass queue length,
+// [kQctlCursor] the whole-row cursor, [kQctlDone, + kMaxSplitRows) the split
+// mode's chunk counters; all zeroed by launch_init.
 constexpr int kMaxFallbackBatch = 8;  // rows of one query tile re-scored in one fallback pass
-hipError_t launch_fused_fallback(const ScoreArgs& a, int k, uint32_t flags, const uint32_t* qctl,
-                                 const int32_t* queue, int32_t* fbflag, int batch, float* scratch, int grid, int32_t* out_i,
-                                 float* out_s, hipStream_t st);
+constexpr int kFallbackGrid = 256;    // blocks of a fallback launch
+constexpr int kQctlWords = 256;
+constexpr int kQctlCursor = 2;
+constexpr int kQctlDone = 4;
+constexpr int kMaxSplitRows = kFallbackGrid / 2;
+constexpr int kSplitMinKeys = 4096;  // keys per chunk at least
+static_assert(kQctlDone + kMaxSplitRows <= kQctlWords, "chunk counters must fit in qctl");
+// Chunks per queued row in split mode, or 1 (whole-row mode): split when at
+// least two blocks per row are available, every row has a scratch row of its
+// own, and the chunks keep kSplitMinKeys keys.
+__host__ __device__ inline int fallback_chunks(uint32_t n, int grid, int slots, int nk) {
+  if (n == 0 || n > (uint32_t)kMaxSplitRows || n > (uint32_t)slots || 2 * n > (uint32_t)grid) return 1;
+  int c = grid / (int)n;
+  const int by_keys = nk / kSplitMinKeys;
+  if (c > by_keys) c = by_keys;
+  return c < 2 ? 1 : c;
+}
+// cidx / cscore [kFallbackGrid * k]: the split mode's chunk candidates.
+hipError_t launch_fused_fallback(const ScoreArgs& a, int k, uint32_t flags, uint32_t* qctl, const int32_t* queue,
+                                 int32_t* fbflag, int batch, int slots, float* scratch, int32_t* cidx, float* cscore,
+                                 int32_t* out_i, float* out_s, hipStream_t st);
 
 // ---- wide-vector scan (wide.hip): bf16, one head, long vectors ----
 // wide_shape(...).supported is 0 for shapes the wide scan does not build.
@@ -121,8 +152,8 @@ hipError_t launch_wide_dense(const ScoreArgs& a, float* out, int64_t ld, hipStre
 // launch_fused_scan.
 hipError_t launch_wide_fused(const ScoreArgs& a, const RowParam* params, int S, int L, int cap, int m, int k,
                              int* gate, uint32_t* cnt, uint32_t* hist, int2* cand, hipStream_t st);
-hipError_t launch_wide_fallback(const ScoreArgs& a, int k, uint32_t flags, const uint32_t* qctl,
-                                const int32_t* queue, float* scratch, int grid, int32_t* out_i, float* out_s,
+hipError_t launch_wide_fallback(const ScoreArgs& a, int k, uint32_t flags, uint32_t* qctl, const int32_t* queue,
+                                int slots, float* scratch, int32_t* cidx, float* cscore, int32_t* out_i, float* out_s,
                                 hipStream_t st);
 
 // k_select flags (internal).

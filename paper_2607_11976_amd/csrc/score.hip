@@ -1417,66 +1417,112 @@ __global__ __launch_bounds__(C::NTHREADS) void k_fused(ScoreArgs a, const RowPar
 template <class C>
 constexpr int fallback_meta_lds() { return ((C::QT + 15) & ~15) + kMaxFallbackBatch * 4 + 16; }
 
+// Exact fallback of the queued rows: dense re-score of each row's visible keys
+// into scratch, then radix select, in split mode (few rows: each row's keys
+// cut into chunks over many blocks, each selecting its chunk's top-k, the
+// last one merging them) or whole-row mode (see launch_fused_fallback).
 template <class C>
-__global__ __launch_bounds__(C::NTHREADS) void k_fused_fallback(ScoreArgs a, int k, uint32_t flags,
-                                                                const uint32_t* qctl, const int32_t* queue,
-                                                                int32_t* fbflag, int batch, size_t meta_off,
-                                                                float* scratch, int32_t* out_i, float* out_s) {
+__global__ __launch_bounds__(C::NTHREADS) void k_fused_fallback(ScoreArgs a, int k, uint32_t flags, uint32_t* qctl,
+                                                                const int32_t* queue, int32_t* fbflag, int batch,
+                                                                int slots, size_t meta_off, float* scratch,
+                                                                int32_t* cidx, float* cscore, int32_t* out_i,
+                                                                float* out_s) {
   extern __shared__ __align__(16) uint8_t lds[];
   int8_t* smap = reinterpret_cast<int8_t*>(lds + meta_off);            // [QT]
   int* brow = reinterpret_cast<int*>(lds + meta_off + ((C::QT + 15) & ~15));  // [kMaxFallbackBatch]
-  int* bn = brow + kMaxFallbackBatch;
+  int* bn = brow + kMaxFallbackBatch;  // [0] rows of the pass, [1] select after the pass
   const uint32_t n = qctl[0];
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
-  for (uint32_t r = blockIdx.x; r < n; r += gridDim.x) {
-    const int row = queue[r];
-    const int q0 = (row / C::QT) * C::QT, qbase = q0 + wave * C::QW;
-    // the batch: this row unless another block took it with its own tile,
-    // then other queued rows of the tile that no block has taken yet
+  const int chunks = fallback_chunks(n, gridDim.x, slots, a.nk);
+  const bool split = chunks > 1;
+  // split: block = (queue entry, chunk of that row's visible keys), one pass;
+  // whole rows: the first slots / batch blocks, each with its own scratch
+  // rows, take queue entries from a shared cursor (a block whose row another
+  // block already took moves on at once)
+  if ((int)blockIdx.x >= (split ? (int)n * chunks : slots / batch)) return;
+  const int e = split ? (int)blockIdx.x / chunks : 0, c = split ? (int)blockIdx.x - e * chunks : 0;
+  float* sblk = scratch + (int64_t)(split ? e : (int)blockIdx.x * batch) * a.nk;
+  for (int pass = 0;; ++pass) {
+    // the pass's rows: split, the entry's row; whole rows, the entry's row
+    // unless another block took it with its own tile, then other queued rows
+    // of the tile that no block has taken yet
     if (threadIdx.x == 0) {
-      int nb = 0;
-      if (!fbflag || atomicExch(&fbflag[row], 2) == 1) {
-        brow[nb++] = row;
-        if (fbflag) {
-          const int qe = min(q0 + C::QT, a.nq);
-          for (int t = q0; t < qe && nb < batch; ++t)
-            if (t != row && atomicCAS(&fbflag[t], 1, 2) == 1) brow[nb++] = t;
+      int nb = -1;  // nothing left
+      if (split) {
+        if (pass == 0) {
+          brow[0] = queue[e];
+          nb = 1;
+        }
+      } else {
+        const uint32_t r = atomicAdd(&qctl[kQctlCursor], 1u);
+        if (r < n) {
+          nb = 0;
+          const int row = queue[r];
+          if (!fbflag || atomicExch(&fbflag[row], 2) == 1) {
+            brow[nb++] = row;
+            if (fbflag) {
+              const int q0 = (row / C::QT) * C::QT, qe = min(q0 + C::QT, a.nq);
+              for (int t = q0; t < qe && nb < batch; ++t)
+                if (t != row && atomicCAS(&fbflag[t], 1, 2) == 1) brow[nb++] = t;
+            }
+          }
         }
       }
-      *bn = nb;
+      bn[0] = nb;
     }
     for (int i = threadIdx.x; i < C::QT; i += C::NTHREADS) smap[i] = -1;
     __syncthreads();
-    const int nb = *bn;
-    if (nb == 0) {  // block-uniform
-      __syncthreads();  // every thread has read *bn before the next row rewrites it
+    const int nb = bn[0];
+    if (nb < 0) return;  // block-uniform
+    if (nb == 0) {
+      __syncthreads();  // every thread has read bn[0] before the next entry rewrites it
       continue;
     }
+    const int q0 = (brow[0] / C::QT) * C::QT, qbase = q0 + wave * C::QW;
     if (threadIdx.x < nb) smap[brow[threadIdx.x] - q0] = (int8_t)threadIdx.x;
-    // scan the union of the batch rows' ranges; each row selects from its own
-    int kb = a.nk, ke = 0;
-    for (int j = 0; j < nb; ++j) {
-      const RowRange rr = row_range(a.offs, a.starts, brow[j], a.nk);
-      if (rr.e > rr.s) {
-        kb = min(kb, rr.s);
-        ke = max(ke, rr.e);
+    // keys of the pass: split, the chunk; whole rows, the union of the rows'
+    // ranges (each row selects from its own)
+    int kb = a.nk, ke = 0, rs = 0, len = 0, per = 0;
+    if (split) {
+      const RowRange rr = row_range(a.offs, a.starts, brow[0], a.nk);
+      rs = rr.s;
+      len = rr.e > rr.s ? rr.e - rr.s : 0;
+      per = ((len + chunks - 1) / chunks + C::KT - 1) / C::KT * C::KT;
+      kb = min(rs + c * per, rs + len);
+      ke = min(kb + per, rs + len);
+    } else {
+      for (int j = 0; j < nb; ++j) {
+        const RowRange rr = row_range(a.offs, a.starts, brow[j], a.nk);
+        if (rr.e > rr.s) {
+          kb = min(kb, rr.s);
+          ke = max(ke, rr.e);
+        }
       }
     }
     __syncthreads();
-    float* sblk = scratch + (int64_t)blockIdx.x * batch * a.nk;
     WaveQ<C> wq;
     load_q<C>(wq, a, qbase);
     RowSink<C> sink{sblk, a.nk, smap, qbase, q0};
     wg_scan<C>(a, SrcContig{}, kb, ke, lds, wq, sink);
     __threadfence_block();
     __syncthreads();
-    for (int j = 0; j < nb; ++j) {
-      const int t = brow[j];
-      const RowRange rr = row_range(a.offs, a.starts, t, a.nk);
-      radix_select_row<C::NTHREADS>(sblk + (int64_t)j * a.nk + rr.s, rr.e - rr.s, k, out_i + (int64_t)t * k,
-                                    out_s + (int64_t)t * k, flags & LT_SORTED_OUTPUT, lds, rr.s);
-      __syncthreads();
+    if (split) {
+      // the chunk's top-k to the row's candidates; the last chunk selects
+      const int t = brow[0];
+      const int64_t cb = (int64_t)e * chunks * k;
+      split_fallback_select<C::NTHREADS>(sblk, rs, len, per, chunks, c, kb, ke, k, cidx + cb, cscore + cb,
+                                         &qctl[kQctlDone + e], out_i + (int64_t)t * k, out_s + (int64_t)t * k,
+                                         flags & LT_SORTED_OUTPUT, lds, &bn[1]);
+    } else {
+      for (int j = 0; j < nb; ++j) {
+        const int t = brow[j];
+        const RowRange rr = row_range(a.offs, a.starts, t, a.nk);
+        radix_select_row<C::NTHREADS>(sblk + (int64_t)j * a.nk + rr.s, rr.e - rr.s, k, out_i + (int64_t)t * k,
+                                      out_s + (int64_t)t * k, flags & LT_SORTED_OUTPUT, lds, rr.s);
+        __syncthreads();
+      }
     }
+    __syncthreads();  // brow and bn are rewritten by the next pass
   }
 }
 
@@ -1604,11 +1650,11 @@ hipError_t launch_fused_scan(const ScoreArgs& a, const RowParam* params, int S, 
   return err;
 }
 
-hipError_t launch_fused_fallback(const ScoreArgs& a, int k, uint32_t flags, const uint32_t* qctl,
-                                 const int32_t* queue, int32_t* fbflag, int batch, float* scratch, int grid,
+hipError_t launch_fused_fallback(const ScoreArgs& a, int k, uint32_t flags, uint32_t* qctl, const int32_t* queue,
+                                 int32_t* fbflag, int batch, int slots, float* scratch, int32_t* cidx, float* cscore,
                                  int32_t* out_i, float* out_s, hipStream_t st) {
   if (wide_shape(a.dtype, a.mode, a.h, a.d).supported)
-    return launch_wide_fallback(a, k, flags, qctl, queue, scratch, grid, out_i, out_s, st);
+    return launch_wide_fallback(a, k, flags, qctl, queue, slots, scratch, cidx, cscore, out_i, out_s, st);
   hipError_t err = hipErrorInvalidValue;
   with_cfg(a.dtype, a.mode, a.h, a.d, a.w == nullptr, [&]<class C>() {
     size_t lds = C::SCAN_LDS;
@@ -1619,8 +1665,8 @@ hipError_t launch_fused_fallback(const ScoreArgs& a, int k, uint32_t flags, cons
     if (lds > 65536)
       (void)hipFuncSetAttribute((const void*)k_fused_fallback<C>, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
     const int b = batch < 1 ? 1 : (batch > kMaxFallbackBatch ? kMaxFallbackBatch : batch);
-    hipLaunchKernelGGL(k_fused_fallback<C>, dim3(grid), dim3(C::NTHREADS), lds, st, a, k, flags, qctl, queue,
-                       fbflag, b, meta, scratch, out_i, out_s);
+    hipLaunchKernelGGL(k_fused_fallback<C>, dim3(kFallbackGrid), dim3(C::NTHREADS), lds, st, a, k, flags, qctl,
+                       queue, fbflag, b, slots, meta, scratch, cidx, cscore, out_i, out_s);
     err = hipGetLastError();
   });
   return err;

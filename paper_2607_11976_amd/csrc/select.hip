@@ -6,11 +6,11 @@
 namespace lt {
 
 // ---------------------------------------------------------------------------
-// Zero the fallback queue counter (a kernel, not a memset, so the launch
-// sequence can be captured in a graph).
+// Zero the queue counters, the fallback cursor and its chunk counters (a
+// kernel, not a memset, so the launch sequence can be captured in a graph).
 // ---------------------------------------------------------------------------
 __global__ void k_init(uint32_t* qctl) {
-  if (threadIdx.x < 4) qctl[threadIdx.x] = 0u;
+  for (int i = threadIdx.x; i < kQctlWords; i += blockDim.x) qctl[i] = 0u;
 }
 
 // ---------------------------------------------------------------------------

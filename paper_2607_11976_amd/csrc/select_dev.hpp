@@ -60,10 +60,15 @@ __host__ __device__ __forceinline__ int next_pow2(int n) {
   return p;
 }
 
+// LDS layout of radix_select_row: a 256-bin histogram per wave (up to
+// kRadixWaves waves), their sum, 32 words of exchange, then the sort entries.
+constexpr int kRadixWaves = 8;
+constexpr size_t kRadixTot = (size_t)kRadixWaves * 256 * 4;
+constexpr size_t kRadixTmp = kRadixTot + 256 * 4;
+constexpr size_t kRadixEnt = kRadixTmp + 32 * 4;
+
 // LDS bytes radix_select_row needs for a given k.
-__host__ __device__ __forceinline__ size_t radix_lds_bytes(int k) {
-  return 256 * 4 + 64 + (size_t)next_pow2(k) * 8;
-}
+__host__ __device__ __forceinline__ size_t radix_lds_bytes(int k) { return kRadixEnt + (size_t)next_pow2(k) * 8; }
 
 // Sort the first n (<= k) entries of an output row by the total order, in
 // place. The rows were written by this block; the caller has made them
@@ -87,33 +92,95 @@ __device__ __forceinline__ void sort_output_row(int32_t* oi, float* os, int n, u
 // Exact top-k of row[0, n) by (score desc, index asc), written to oi/os
 // (k entries, padded with (-1, -inf)). Plain most-significant-digit radix
 // selection over the order keys: four 8-bit passes find the k-th key K*, then
-// one ordered pass keeps every key > K* and the lowest-index keys == K*.
+// one pass writes every key > K* and the lowest-index keys == K*. Each wave
+// streams a contiguous segment of the row (kRadixUnroll loads in flight per
+// lane) into its own histogram; after each pass the wave also counts its keys
+// above the pass's digit, so that after the last pass every wave knows how
+// many keys > K* and == K* lie in the segments before its own, and the write
+// pass places each hit without block barriers.
 // Output order: ascending key index, or the total order when `sorted`.
+// pad = false: a row of n < k keys writes its n entries and nothing after.
 template <int NTH>
-__device__ __forceinline__ void radix_select_row_at(const float* row, int n, int k, int32_t* oi, float* os, bool sorted,
-                                    uint8_t* lds);
+__device__ __noinline__ void radix_select_row_at(const float* row, int n, int k, int32_t* oi, float* os, bool sorted,
+                                                 uint8_t* lds, bool pad);
 
 // radix_select_row over keys [base, base + n) of a row whose key `base` is at
 // row[0]: the written indices are shifted by `base`.
 template <int NTH>
 __device__ __forceinline__ void radix_select_row(const float* row, int n, int k, int32_t* oi, float* os, bool sorted,
-                                 uint8_t* lds, int base = 0) {
-  radix_select_row_at<NTH>(row, n, k, oi, os, sorted, lds);
+                                 uint8_t* lds, int base = 0, bool pad = true) {
+  radix_select_row_at<NTH>(row, n, k, oi, os, sorted, lds, pad);
   if (base != 0) {
     __threadfence_block();
     __syncthreads();
-    for (int i = threadIdx.x; i < k; i += NTH)
+    const int m = pad || n > k ? k : (n > 0 ? n : 0);
+    for (int i = threadIdx.x; i < m; i += NTH)
       if (oi[i] >= 0) oi[i] += base;
   }
 }
 
+// Split fallback of one queued row whose visible keys [rs, rs + len) are cut
+// into `chunks` chunks of `per` keys, chunk c = [kb, ke) scored into
+// srow[kb, ke) by this block. The chunk's own exact top-k goes to the row's
+// candidate region (cidx, cscore): chunk c's min(k, chunk length) entries
+// after those of chunks 0..c-1, in ascending key order. The block that counts
+// the row's last chunk (counter) selects the row from the candidates: the
+// union of the chunks' top-k holds the row's top-k, in ascending key order,
+// so positions order equal scores as key indices do. `flag`: one LDS word.
 template <int NTH>
-__device__ __forceinline__ void radix_select_row_at(const float* row, int n, int k, int32_t* oi, float* os, bool sorted,
-                                    uint8_t* lds) {
-  uint32_t* hist = reinterpret_cast<uint32_t*>(lds);
-  uint32_t* tmp = hist + 256;                // 16 words
-  uint64_t* ent = reinterpret_cast<uint64_t*>(lds + 256 * 4 + 64);
-  const int tid = threadIdx.x;
+__device__ __forceinline__ void split_fallback_select(const float* srow, int rs, int len, int per, int chunks, int c,
+                                                      int kb, int ke, int k, int32_t* cidx, float* cscore,
+                                                      uint32_t* counter, int32_t* oi, float* os, bool sorted,
+                                                      uint8_t* lds, int* flag) {
+  auto clen = [&](int j) { return max(0, min(per, len - j * per)); };
+  int off = 0;
+  for (int j = 0; j < c; ++j) off += min(k, clen(j));
+  radix_select_row<NTH>(srow + kb, ke - kb, k, cidx + off, cscore + off, false, lds, kb, false);
+  // publish this chunk's candidates, then count it
+  __threadfence();
+  __syncthreads();
+  if (threadIdx.x == 0) *flag = atomicAdd(counter, 1u) == (uint32_t)(chunks - 1) ? 1 : 0;
+  __syncthreads();
+  if (!*flag) return;
+  __threadfence();
+  int u = 0;
+  for (int j = 0; j < chunks; ++j) u += min(k, clen(j));
+  radix_select_row_at<NTH>(cscore, u, k, oi, os, sorted, lds, true);
+  __threadfence_block();
+  __syncthreads();
+  for (int i = threadIdx.x; i < k; i += NTH)
+    if (oi[i] >= 0) oi[i] = cidx[oi[i]];
+}
+
+// Loads in flight per lane, and the histogram passes (from the first) whose
+// lanes of the most common bins add their counts with one atomic per bin
+// (measured on MI355X, one row of 262144 / 1M / 4M keys per block: 32 loads
+// and one grouped bin in the first pass, 0.72 / 2.6 / 10.1 ms; 8 loads,
+// 0.76 / 2.8 / 12.4 ms; four grouped bins in two passes, slower).
+#ifndef LT_RADIX_UNROLL
+#define LT_RADIX_UNROLL 32
+#endif
+#ifndef LT_RADIX_GROUP_PASSES
+#define LT_RADIX_GROUP_PASSES 1
+#endif
+#ifndef LT_RADIX_GROUP_BINS
+#define LT_RADIX_GROUP_BINS 1
+#endif
+constexpr int kRadixUnroll = LT_RADIX_UNROLL;
+
+// Not inlined: the callers inline it after a register-heavy scan, and a
+// separate allocation keeps its unrolled loads from spilling the scan.
+template <int NTH>
+__device__ __noinline__ void radix_select_row_at(const float* row, int n, int k, int32_t* oi, float* os, bool sorted,
+                                                 uint8_t* lds, bool pad) {
+  constexpr int NW = NTH / kWave, U = kRadixUnroll;
+  static_assert(NW <= kRadixWaves, "one histogram per wave");
+  uint32_t* hist = reinterpret_cast<uint32_t*>(lds);              // [NW][256]
+  uint32_t* tot = reinterpret_cast<uint32_t*>(lds + kRadixTot);   // [256]
+  uint32_t* tmp = reinterpret_cast<uint32_t*>(lds + kRadixTmp);   // [32]
+  uint64_t* ent = reinterpret_cast<uint64_t*>(lds + kRadixEnt);
+  const int tid = threadIdx.x, l = lane_id(), wave = tid / kWave;
+  uint32_t* hw = hist + wave * 256;
   auto fetch = [&](uint32_t idx) { return row[idx]; };
 
   if (n <= k) {
@@ -121,7 +188,7 @@ __device__ __forceinline__ void radix_select_row_at(const float* row, int n, int
       if (i < n) {
         oi[i] = i;
         os[i] = row[i];
-      } else {
+      } else if (pad) {
         oi[i] = -1;
         os[i] = -__builtin_inff();
       }
@@ -134,71 +201,122 @@ __device__ __forceinline__ void radix_select_row_at(const float* row, int n, int
     return;
   }
 
+  // this wave's segment [s0, s1) of the row, read kWave * U keys per step
+  const int seg = ((n + NW - 1) / NW + kWave - 1) / kWave * kWave;
+  const int s0 = min(wave * seg, n), s1 = min(s0 + seg, n);
+  auto load = [&](int c0, float (&x)[U]) {
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const int i = c0 + u * kWave + l;
+      x[u] = i < s1 ? row[i] : 0.0f;
+    }
+  };
+
   uint32_t prefix = 0, pmask = 0, remaining = (uint32_t)k;
+  uint32_t gbefore = 0;  // this wave's keys above the digits chosen so far (wave-uniform)
+  uint32_t eqw = 0;      // this wave's keys == K* (after the last pass)
   for (int pass = 0; pass < 4; ++pass) {
     const int shift = 24 - 8 * pass;
-    for (int b = tid; b < 256; b += NTH) hist[b] = 0;
+    for (int b = tid; b < NW * 256; b += NTH) hist[b] = 0;
     __syncthreads();
-    for (int i = tid; i < n; i += NTH) {
-      uint32_t key = ord_key(row[i]);
-      if ((key & pmask) == prefix) atomicAdd(&hist[(key >> shift) & 255u], 1u);
+    for (int c0 = s0; c0 < s1; c0 += kWave * U) {
+      float x[U];
+      load(c0, x);
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        if (c0 + u * kWave >= s1) break;  // wave-uniform
+        const bool v = c0 + u * kWave + l < s1;
+        const uint32_t key = ord_key(x[u]);
+        const uint32_t b = (key >> shift) & 255u;
+        bool in = v && (key & pmask) == prefix;
+        if (pass < LT_RADIX_GROUP_PASSES) {
+          // concentrated scores share their leading bytes: the lanes of the
+          // few most common bins add their counts with one atomic per bin
+          uint64_t left = __ballot(in);
+#pragma unroll
+          for (int g = 0; g < LT_RADIX_GROUP_BINS; ++g) {
+            if (left == 0) break;
+            const uint32_t bg = __builtin_amdgcn_readlane(b, __builtin_ctzll(left));
+            const uint64_t mg = __ballot(in && b == bg);
+            if (l == (int)__builtin_ctzll(mg)) atomicAdd(&hw[bg], (uint32_t)__popcll(mg));
+            in = in && b != bg;
+            left &= ~mg;
+          }
+        }
+        if (in) atomicAdd(&hw[b], 1u);
+      }
+    }
+    __syncthreads();
+    for (int b = tid; b < 256; b += NTH) {
+      uint32_t t = 0;
+      for (int w = 0; w < NW; ++w) t += hist[w * 256 + b];
+      tot[b] = t;
     }
     __syncthreads();
     if (tid < kWave) {
       uint32_t above = 0;
-      int d = wave_threshold(hist, 256, remaining, &above);
+      int d = wave_threshold(tot, 256, remaining, &above);
       if (tid == 0) {
-        tmp[8] = (uint32_t)d;
-        tmp[9] = above;
+        tmp[16] = (uint32_t)d;
+        tmp[17] = above;
       }
     }
     __syncthreads();
-    const uint32_t d = tmp[8], above = tmp[9];
+    const uint32_t d = tmp[16], above = tmp[17];
+    // this wave's keys of the current prefix in bins above d (and == d)
+    uint32_t mine = 0;
+    for (int b = l; b < 256; b += kWave) mine += (uint32_t)b > d ? hw[b] : 0u;
+    gbefore += wave_sum(mine);
+    if (pass == 3) eqw = hw[d];
     __syncthreads();
     remaining -= above;
     prefix |= d << shift;
     pmask |= 0xFFu << shift;
   }
-  const uint32_t kstar = prefix, need = remaining, ngt = (uint32_t)k - remaining;
-
-  uint32_t run_gt = 0, run_eq = 0;
-  for (int base = 0; base < n; base += NTH * 4) {
-    const int i0 = base + tid * 4;
-    float v[4];
-    bool gt[4], eq[4];
-    uint32_t cg = 0, ce = 0;
-#pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const int i = i0 + j;
-      v[j] = i < n ? row[i] : 0.0f;
-      uint32_t key = i < n ? ord_key(v[j]) : 0u;
-      gt[j] = i < n && key > kstar;
-      eq[j] = i < n && key == kstar;
-      cg += gt[j];
-      ce += eq[j];
+  const uint32_t kstar = prefix, need = remaining;
+  if (l == 0) {
+    tmp[wave] = gbefore;
+    tmp[8 + wave] = eqw;
+  }
+  __syncthreads();
+  uint32_t g = 0, e = 0, cg = 0, ce = 0;
+  for (int w = 0; w < NW; ++w) {
+    if (w < wave) {
+      g += tmp[w];
+      e += tmp[8 + w];
     }
-    uint32_t tot;
-    uint32_t ex = block_scan_excl<NTH>((cg << 16) | ce, tmp, &tot);
-    uint32_t g = run_gt + (ex >> 16), e = run_eq + (ex & 0xFFFFu);
+  }
+  cg = tmp[wave];
+  ce = tmp[8 + wave];
+  __syncthreads();
+  // a key > K* goes after the keys > K* and the taken keys == K* of lower
+  // index; a key == K* is taken while fewer than `need` of lower index were
+  if (cg != 0 || (ce != 0 && e < need)) {  // wave-uniform
+    for (int c0 = s0; c0 < s1; c0 += kWave * U) {
+      float x[U];
+      load(c0, x);
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      if (gt[j]) {
-        uint32_t p = g + (e < need ? e : need);
-        oi[p] = i0 + j;
-        os[p] = v[j];
-        ++g;
-      } else if (eq[j]) {
-        if (e < need) {
-          uint32_t p = g + e;
-          oi[p] = i0 + j;
-          os[p] = v[j];
+      for (int u = 0; u < U; ++u) {
+        if (c0 + u * kWave >= s1) break;  // wave-uniform
+        const int i = c0 + u * kWave + l;
+        const uint32_t key = i < s1 ? ord_key(x[u]) : 0u;
+        const bool gt = i < s1 && key > kstar, eq = i < s1 && key == kstar;
+        const uint64_t mg = __ballot(gt), me = __ballot(eq);
+        if ((mg | me) == 0) continue;
+        const uint32_t rg = g + mbcnt64(mg), re = e + mbcnt64(me);
+        if (gt) {
+          const uint32_t p = rg + (re < need ? re : need);
+          oi[p] = i;
+          os[p] = x[u];
+        } else if (eq && re < need) {
+          const uint32_t p = rg + re;
+          oi[p] = i;
+          os[p] = x[u];
         }
-        ++e;
+        g += (uint32_t)__popcll(mg);
+        e += (uint32_t)__popcll(me);
       }
     }
-    run_gt += tot >> 16;
-    run_eq += tot & 0xFFFFu;
-    if (run_gt >= ngt && run_eq >= need) break;  // block-uniform
   }
   if (sorted) {
     __threadfence_block();

@@ -563,28 +563,51 @@ __global__ __launch_bounds__(C::NTHREADS) void k_wide_fused(ScoreArgs a, const R
   }
 }
 
-// Exact fallback for queued rows: one block per row at a time re-scores the
-// row's visible range into its scratch row, then radix-selects it.
+// Exact fallback for queued rows: the row's visible range re-scored into a
+// scratch row, then radix-selected. Split mode (few rows, fallback_chunks > 1):
+// one block per (queue entry, chunk of the row's keys) writing into the
+// entry's scratch row and selecting the chunk's top-k into the candidate
+// arrays (cidx, cscore); the block that counts the row's last chunk selects
+// the row from them. Otherwise the first `slots` blocks take one whole row at
+// a time, each into its own scratch row. One loop serves both (one item per
+// block in split mode).
 template <class C>
-__global__ __launch_bounds__(C::NTHREADS) void k_wide_fallback(ScoreArgs a, int k, uint32_t flags,
-                                                               const uint32_t* qctl, const int32_t* queue,
-                                                               float* scratch, int32_t* out_i, float* out_s) {
+__global__ __launch_bounds__(C::NTHREADS) void k_wide_fallback(ScoreArgs a, int k, uint32_t flags, uint32_t* qctl,
+                                                               const int32_t* queue, int slots, float* scratch,
+                                                               int32_t* cidx, float* cscore, int32_t* out_i,
+                                                               float* out_s) {
   extern __shared__ __align__(16) uint8_t lds[];
+  __shared__ int last;
   const uint32_t n = qctl[0];
-  for (uint32_t r = blockIdx.x; r < n; r += gridDim.x) {
-    const int row = queue[r];
-    const int q0 = (row / C::QT) * C::QT, ql = row - q0;
+  const int chunks = fallback_chunks(n, gridDim.x, slots, a.nk);
+  const int active = chunks > 1 ? (int)gridDim.x : min((int)gridDim.x, slots);
+  const uint32_t items = n * (uint32_t)chunks;
+  if ((int)blockIdx.x >= active) return;
+  for (uint32_t it = blockIdx.x; it < items; it += (uint32_t)active) {
+    const int e = (int)(it / (uint32_t)chunks), c = (int)it - e * chunks;
+    const int row = queue[e];
     const RowRange rr = row_range(a.offs, a.starts, row, a.nk);
-    float* srow = scratch + (int64_t)blockIdx.x * a.nk;
+    const int len = rr.e > rr.s ? rr.e - rr.s : 0;
+    const int per = ((len + chunks - 1) / chunks + C::STEP - 1) / C::STEP * C::STEP;
+    const int kb = min(rr.s + c * per, rr.s + len), ke = min(kb + per, rr.s + len);
+    float* srow = scratch + (int64_t)(chunks > 1 ? e : (int)blockIdx.x) * a.nk;
+    const int q0 = (row / C::QT) * C::QT, ql = row - q0;
     wide_load_q<C>(lds, a, q0);
     float wv[C::NI];
     wide_weights<C>(wv, a, q0);
     WideRowSink<C> sink{srow, 16 * (ql >> 5) + 4 * ((ql & 31) >> 3) + (ql & 3), (ql >> 2) & 1};
-    wide_scan<C>(a, WSrcContig{}, rr.s, rr.e, lds, wv, sink);
+    wide_scan<C>(a, WSrcContig{}, kb, ke, lds, wv, sink);
     __threadfence_block();
     __syncthreads();
-    radix_select_row<C::NTHREADS>(srow + rr.s, rr.e - rr.s, k, out_i + (int64_t)row * k, out_s + (int64_t)row * k,
-                                  flags & LT_SORTED_OUTPUT, lds, rr.s);
+    if (chunks > 1) {
+      const int64_t cb = (int64_t)e * chunks * k;
+      split_fallback_select<C::NTHREADS>(srow, rr.s, len, per, chunks, c, kb, ke, k, cidx + cb, cscore + cb,
+                                         &qctl[kQctlDone + e], out_i + (int64_t)row * k, out_s + (int64_t)row * k,
+                                         flags & LT_SORTED_OUTPUT, lds, &last);
+    } else {
+      radix_select_row<C::NTHREADS>(srow + rr.s, len, k, out_i + (int64_t)row * k, out_s + (int64_t)row * k,
+                                    flags & LT_SORTED_OUTPUT, lds, rr.s);
+    }
     __syncthreads();
   }
 }
@@ -690,8 +713,8 @@ hipError_t launch_wide_fused(const ScoreArgs& a, const RowParam* params, int S, 
   return err;
 }
 
-hipError_t launch_wide_fallback(const ScoreArgs& a, int k, uint32_t flags, const uint32_t* qctl,
-                                const int32_t* queue, float* scratch, int grid, int32_t* out_i, float* out_s,
+hipError_t launch_wide_fallback(const ScoreArgs& a, int k, uint32_t flags, uint32_t* qctl, const int32_t* queue,
+                                int slots, float* scratch, int32_t* cidx, float* cscore, int32_t* out_i, float* out_s,
                                 hipStream_t st) {
   hipError_t err = hipErrorInvalidValue;
   with_wide(a.dtype, a.mode, a.h, a.d, [&]<class C>() {
@@ -699,8 +722,8 @@ hipError_t launch_wide_fallback(const ScoreArgs& a, int k, uint32_t flags, const
     const size_t rl = radix_lds_bytes(k);
     if (rl > lds) lds = rl;
     allow_lds(k_wide_fallback<C>, lds);
-    hipLaunchKernelGGL(k_wide_fallback<C>, dim3(grid), dim3(C::NTHREADS), lds, st, a, k, flags, qctl, queue,
-                       scratch, out_i, out_s);
+    hipLaunchKernelGGL(k_wide_fallback<C>, dim3(kFallbackGrid), dim3(C::NTHREADS), lds, st, a, k, flags, qctl,
+                       queue, slots, scratch, cidx, cscore, out_i, out_s);
     err = hipGetLastError();
   });
   return err;

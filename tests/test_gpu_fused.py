@@ -246,3 +246,38 @@ def test_dense_fallback_batches_rows_of_a_tile(lib, law):
     np.testing.assert_array_equal(gs.view(np.uint32), rs.cpu().numpy().view(np.uint32))
     rows = sorted(set(np.linspace(0, nq - 1, 24).round().astype(int).tolist()) | {b, b + 1})
     _check_tol(x, cfg.dtype, k, mode, gi, gs, rows=rows)
+
+
+@pytest.mark.parametrize("sorted_out", [True, False], ids=["sorted", "unsorted"])
+@pytest.mark.parametrize("law", [
+    # id, base config, nq, nk, k, mode
+    ("dsa_bf16_h64", "dsa_bf16_128k", 3, 262144, 2048, "dsa"),
+    ("dsa_fp8_h64", "dsa_fp8_1m", 2, 1048576, 2048, "dsa"),
+    ("ip_bf16_h1", "retrieval_bf16_4m", 5, 1000004, 100, "ip"),
+], ids=lambda l: l[0])
+def test_dense_fallback_splits_few_rows_over_blocks(lib, law, sorted_out):
+    """A few queued rows at a large Nk: the dense fallback cuts each row's
+    visible keys into chunks re-scored by different blocks, and the block that
+    scores a row's last chunk selects the row. Forced fallback on rows of
+    different lengths (the whole context, about half of it, none, fewer keys
+    than k, all but 77): every row equals radix selection over the dense
+    scores bit for bit (sorted output; unsorted: the same set and scores), and
+    the non-empty rows meet the oracle."""
+    name, base, nq, nk, k, mode = law
+    assert nk % 4 == 0, "the dense score rows must stay 16-byte aligned"
+    cfg = workloads.scaled(workloads.CONFIGS[base], nq=nq, nk=nk)
+    x = workloads.generate(cfg, seed=29)
+    offs = np.array([nk, nk // 2 + 3, 0, k - 5, nk - 77], dtype=np.int32)[:nq]
+    x["offsets"] = torch.from_numpy(offs)
+    gi, gs, st = _fused(x, k, mode, sorted_output=sorted_out, force_fallback=True)
+    np.testing.assert_array_equal(st[:, 2], 3)
+    d = to_dev(x)
+    dense = lt.indexer_scores(d["q"], d["w"], d["keys"], d["q_scale"], d["k_scale"], mode=mode)
+    ri, rs = lt.topk_radix(dense, k, causal_offsets=d["offsets"], sorted_output=True)
+    torch.cuda.synchronize()
+    ri, rs = ri.cpu().numpy(), rs.cpu().numpy()
+    e = visible(offs, nq, nk)
+    for t in range(nq):
+        check_row_exact(gi[t], gs[t], ri[t], rs[t], int(e[t]), k, sorted_out)
+    rows = [t for t in range(nq) if e[t] > 0][:2]
+    _check_tol(x, cfg.dtype, k, mode, gi, gs, rows=rows)

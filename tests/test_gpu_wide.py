@@ -236,3 +236,30 @@ def test_wide_full_size(lib, k):
     fi_h, fs_h = fi.cpu().numpy(), fs.cpu().numpy()
     for j, t in enumerate(rows):
         check_row_tol(fi_h[t], fs_h[t], oi[j], os_[j], full[j], nk, k, RTOL["bf16"])
+
+
+def test_wide_fallback_splits_few_rows_over_blocks(lib):
+    """Three queued rows over 300000 passages: the fallback cuts each row's
+    visible passages into chunks re-scored by different blocks, and the block
+    that scores a row's last chunk selects the row. Forced fallback, rows of
+    different lengths, sorted and unsorted output: every row equals radix
+    selection over the dense scores bit for bit (unsorted: the same set and
+    scores), and the shorter rows meet the oracle."""
+    nq, nk, k = 3, 300000, 1024
+    x = workloads.generate(workloads.scaled(E7, nq=nq, nk=nk), seed=31)
+    offs = np.array([nk, nk // 3 + 1, 700], dtype=np.int32)
+    x["offsets"] = torch.from_numpy(offs)
+    d = to_dev(x)
+    dense = lt.indexer_scores(d["q"], None, d["keys"], mode="ip")
+    ri, rs = lt.topk_radix(dense, k, causal_offsets=d["offsets"], sorted_output=True)
+    torch.cuda.synchronize()
+    ri, rs = ri.cpu().numpy(), rs.cpu().numpy()
+    e = visible(offs, nq, nk)
+    for sorted_out in (True, False):
+        gi, gs, st = _fused(x, k, sorted_output=sorted_out, force_fallback=True)
+        np.testing.assert_array_equal(st[:, 2], 3)
+        for t in range(nq):
+            check_row_exact(gi[t], gs[t], ri[t], rs[t], int(e[t]), k, sorted_out)
+    oi, os_, full = oracle_topk(x, "bf16", k, "ip", rows=[1, 2])
+    for j, t in enumerate([1, 2]):
+        check_row_tol(gi[t], gs[t], oi[j], os_[j], full[j], int(e[t]), k, RTOL["bf16"])
