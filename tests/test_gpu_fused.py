@@ -281,3 +281,23 @@ def test_dense_fallback_splits_few_rows_over_blocks(lib, law, sorted_out):
         check_row_exact(gi[t], gs[t], ri[t], rs[t], int(e[t]), k, sorted_out)
     rows = [t for t in range(nq) if e[t] > 0][:2]
     _check_tol(x, cfg.dtype, k, mode, gi, gs, rows=rows)
+
+
+@pytest.mark.parametrize("nq", [128, 129], ids=["split_128_rows", "whole_rows_129"])
+def test_dense_fallback_mode_boundary(lib, nq):
+    """The fallback splits rows over blocks for up to 128 queued rows (two
+    chunks each here) and takes whole rows from the shared cursor above that:
+    both sides of the switch, every row forced, causal rows of different
+    lengths, equal to radix selection over the dense scores bit for bit."""
+    nk, k = 16384, 300
+    cfg = workloads.scaled(workloads.CONFIGS["dsa_bf16_128k"], nq=nq, nk=nk)
+    x = workloads.generate(cfg, seed=37)
+    gi, gs, st = _fused(x, k, "dsa", sorted_output=True, force_fallback=True)
+    np.testing.assert_array_equal(st[:, 2], 3)
+    d = to_dev(x)
+    dense = lt.indexer_scores(d["q"], d["w"], d["keys"], mode="dsa")
+    ri, rs = lt.topk_radix(dense, k, causal_offsets=d["offsets"], sorted_output=True)
+    torch.cuda.synchronize()
+    np.testing.assert_array_equal(gi, ri.cpu().numpy())
+    np.testing.assert_array_equal(gs.view(np.uint32), rs.cpu().numpy().view(np.uint32))
+    _check_tol(x, "bf16", k, "dsa", gi, gs, rows=[0, nq // 2, nq - 1])
