@@ -106,3 +106,23 @@ def test_scores_in_select_with_starts(lib, opt):
     gi, gs = gi.cpu().numpy(), gs.cpu().numpy()
     for t in range(nq):
         check_row_exact(gi[t], gs[t], ri[t], rs[t], int(e0[t] - s0[t]), k, True)
+
+
+def test_packed_rows_split_over_fallback_blocks(lib):
+    """A few forced rows over 40000 keys take the fallback's split mode (each
+    row's visible keys in chunks over many blocks); with packed starts the
+    chunks cover [s_t, e_t) only: exact inputs, sorted output, bit-exact
+    against the oracle, including a row whose start is past its end and one
+    that sees fewer keys than k."""
+    nq, nk, k = 6, 40000, 256
+    x = workloads.exact_inputs(nq, nk, 64, 128, "bf16", seed=9, causal=False)
+    ends = np.array([nk, 31000, 25000, 40000, 9000, 20000], dtype=np.int32)
+    starts = np.array([0, 7003, 26000, 39900, 1, 12345], dtype=np.int32)
+    x["offsets"] = torch.from_numpy(ends)
+    x["starts"] = torch.from_numpy(starts)
+    d = to_dev(x)
+    ri, rs, _ = oracle_topk(x, "bf16", k, "dsa")
+    s0, e0 = orc.visible_ranges(ends, starts, nq, nk)
+    gi, gs = _fused(d, k, "dsa", visible_start=d["starts"], force_fallback=True)
+    for t in range(nq):
+        check_row_exact(gi[t], gs[t], ri[t], rs[t], int(e0[t] - s0[t]), k, True)
