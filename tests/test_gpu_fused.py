@@ -254,6 +254,7 @@ def test_dense_fallback_batches_rows_of_a_tile(lib, law):
     ("dsa_bf16_h64", "dsa_bf16_128k", 3, 262144, 2048, "dsa"),
     ("dsa_fp8_h64", "dsa_fp8_1m", 2, 1048576, 2048, "dsa"),
     ("ip_bf16_h1", "retrieval_bf16_4m", 5, 1000004, 100, "ip"),
+    ("dsa_bf16_kmax", "dsa_bf16_128k", 3, 200000, 8192, "dsa"),     # k = LT_K_MAX, chunks shorter than k
 ], ids=lambda l: l[0])
 def test_dense_fallback_splits_few_rows_over_blocks(lib, law, sorted_out):
     """A few queued rows at a large Nk: the dense fallback cuts each row's
