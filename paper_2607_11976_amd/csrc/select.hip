@@ -469,10 +469,9 @@ __device__ __forceinline__ void select_row(int row, RowParam* params, const uint
 #pragma unroll
       for (int j = 0; j < PER; ++j) {
         if (sorted) {
-          if (ab[j] || ti[j]) {
-            const uint32_t q = ra + rt;
-            if (q < (uint32_t)E) ent[q] = comp_key(__int_as_float(ce[j].y), gpos[j]);
-          }
+          // the keys above bin tau first (c_above of them), then those of bin tau
+          if (ab[j] && ra < c_above) ent[ra] = comp_key(__int_as_float(ce[j].y), gpos[j]);
+          if (ti[j] && c_above + rt < (uint32_t)E) ent[c_above + rt] = comp_key(__int_as_float(ce[j].y), gpos[j]);
         } else {
           if (ab[j] && ra < (uint32_t)k) {
             oi[ra] = ce[j].x;
@@ -495,13 +494,29 @@ __device__ __forceinline__ void select_row(int row, RowParam* params, const uint
     return;
   }
   const uint32_t need = (uint32_t)k - c_above;
-  const int P = next_pow2((int)nent < 1 ? 1 : (int)nent);
-  for (int i = tid; i < P; i += NTH)
-    if ((uint32_t)i >= nent) ent[i] = 0ull;
-  __syncthreads();
-  bitonic_sort_desc<NTH>(ent, P);
-  const uint32_t first = sorted ? 0u : c_above;
   const uint32_t take = sorted ? min(nent, (uint32_t)k) : min(need, nent);
+  // sorted: first the keys of bin tau alone (behind the c_above keys above
+  // it), so that only the k kept keys are sorted together, where the sort
+  // would otherwise take every key of the bin too
+  const int Pt = next_pow2(run_tie < 1 ? 1 : (int)run_tie);
+  if (sorted && run_tie > 0 && c_above + (uint32_t)Pt <= (uint32_t)E) {
+    for (int i = tid; i < Pt; i += NTH)
+      if ((uint32_t)i >= run_tie) ent[c_above + i] = 0ull;
+    __syncthreads();
+    bitonic_sort_desc<NTH>(ent + c_above, Pt);
+    const int P = next_pow2((int)take < 1 ? 1 : (int)take);
+    for (int i = tid; i < P; i += NTH)
+      if ((uint32_t)i >= take) ent[i] = 0ull;
+    __syncthreads();
+    bitonic_sort_desc<NTH>(ent, P);
+  } else {
+    const int P = next_pow2((int)nent < 1 ? 1 : (int)nent);
+    for (int i = tid; i < P; i += NTH)
+      if ((uint32_t)i >= nent) ent[i] = 0ull;
+    __syncthreads();
+    bitonic_sort_desc<NTH>(ent, P);
+  }
+  const uint32_t first = sorted ? 0u : c_above;
   for (uint32_t i = tid; i < take; i += NTH) {
     uint32_t gp = comp_pos(ent[i]);
     if (keyed) {
