@@ -302,8 +302,9 @@ __device__ __forceinline__ void select_row(int row, RowParam* params, const uint
   uint64_t* ent = reinterpret_cast<uint64_t*>(lds + select_ent_offset(NTH));  // [E]
   const int tid = threadIdx.x;
   // keyed: the lists are not in key order, so the tie-break position is the
-  // key itself, the output is rebuilt from the sort entries, and every row
-  // is sorted (the order of arrival would make it vary between calls)
+  // key itself, the sorted scores are rebuilt from the sort entries, and
+  // every row is sorted (the order of arrival would make it vary between
+  // calls)
   const bool keyed = flags & kSelKeyed;
   const bool ilv = flags & kSelIlv;
   const bool sorted = (flags & LT_SORTED_OUTPUT) || keyed;
@@ -370,9 +371,7 @@ __device__ __forceinline__ void select_row(int row, RowParam* params, const uint
     // pass gated at tau from its first key writes exactly the c_above +
     // c_tie keys of those bins; when they fit in one list (and the sort
     // buffer) the row is queued for that pass, else for the dense fallback.
-    const bool sorted_all = (flags & LT_SORTED_OUTPUT) || (flags & kSelKeyed);
-    const uint32_t nsort = sorted_all ? c_above + c_tie : c_tie;
-    if ((flags & kSelRefilter) && tau >= 0 && c_above + c_tie <= (uint32_t)cap && nsort <= (uint32_t)E) {
+    if ((flags & kSelRefilter) && tau >= 0 && c_above + c_tie <= (uint32_t)cap && c_tie <= (uint32_t)E) {
       if (tid == 0) {
         params[row].tau0 = tau;
         rflag[row] = 1;
@@ -468,17 +467,11 @@ __device__ __forceinline__ void select_row(int row, RowParam* params, const uint
       uint32_t ra = run_above + (ex2 >> 16), rt = run_tie + (ex2 & 0xFFFFu);
 #pragma unroll
       for (int j = 0; j < PER; ++j) {
-        if (sorted) {
-          // the keys above bin tau first (c_above of them), then those of bin tau
-          if (ab[j] && ra < c_above) ent[ra] = comp_key(__int_as_float(ce[j].y), gpos[j]);
-          if (ti[j] && c_above + rt < (uint32_t)E) ent[c_above + rt] = comp_key(__int_as_float(ce[j].y), gpos[j]);
-        } else {
-          if (ab[j] && ra < (uint32_t)k) {
-            oi[ra] = ce[j].x;
-            os[ra] = __int_as_float(ce[j].y);
-          }
-          if (ti[j] && rt < (uint32_t)E) ent[rt] = comp_key(__int_as_float(ce[j].y), gpos[j]);
+        if (ab[j] && ra < (uint32_t)k) {
+          oi[ra] = ce[j].x;
+          os[ra] = __int_as_float(ce[j].y);
         }
+        if (ti[j] && rt < (uint32_t)E) ent[rt] = comp_key(__int_as_float(ce[j].y), gpos[j]);
         ra += ab[j];
         rt += ti[j];
       }
@@ -487,51 +480,71 @@ __device__ __forceinline__ void select_row(int row, RowParam* params, const uint
     }
     __syncthreads();  // off[] is rewritten by the next group
   }
-  const uint32_t nent = sorted ? run_above + run_tie : run_tie;
+  const uint32_t nent = run_tie;
   tie_ovf = nent > (uint32_t)E;
   if (tie_ovf || run_above != c_above) {
     enqueue(tie_ovf ? 2 : 4, tau, run_tie);
     return;
   }
+  // the need = k - c_above best keys of bin tau, after the keys above it
   const uint32_t need = (uint32_t)k - c_above;
-  const uint32_t take = sorted ? min(nent, (uint32_t)k) : min(need, nent);
-  // sorted: first the keys of bin tau alone (behind the c_above keys above
-  // it), so that only the k kept keys are sorted together, where the sort
-  // would otherwise take every key of the bin too
-  const int Pt = next_pow2(run_tie < 1 ? 1 : (int)run_tie);
-  if (sorted && run_tie > 0 && c_above + (uint32_t)Pt <= (uint32_t)E) {
-    for (int i = tid; i < Pt; i += NTH)
-      if ((uint32_t)i >= run_tie) ent[c_above + i] = 0ull;
-    __syncthreads();
-    bitonic_sort_desc<NTH>(ent + c_above, Pt);
-    const int P = next_pow2((int)take < 1 ? 1 : (int)take);
-    for (int i = tid; i < P; i += NTH)
-      if ((uint32_t)i >= take) ent[i] = 0ull;
-    __syncthreads();
-    bitonic_sort_desc<NTH>(ent, P);
-  } else {
+  const uint32_t take = min(need, nent);
+  {
     const int P = next_pow2((int)nent < 1 ? 1 : (int)nent);
     for (int i = tid; i < P; i += NTH)
       if ((uint32_t)i >= nent) ent[i] = 0ull;
     __syncthreads();
     bitonic_sort_desc<NTH>(ent, P);
   }
-  const uint32_t first = sorted ? 0u : c_above;
   for (uint32_t i = tid; i < take; i += NTH) {
     uint32_t gp = comp_pos(ent[i]);
     if (keyed) {
-      oi[first + i] = (int32_t)gp;
-      os[first + i] = ord_inv((uint32_t)(ent[i] >> 32));
+      oi[c_above + i] = (int32_t)gp;
+      os[c_above + i] = ord_inv((uint32_t)(ent[i] >> 32));
       continue;
     }
     uint32_t s = gp / (uint32_t)cap, j = gp - s * (uint32_t)cap;
     int2 ce = cand[((int64_t)row * S + s) * cap + j];
-    oi[first + i] = ce.x;
-    os[first + i] = __int_as_float(ce.y);
+    oi[c_above + i] = ce.x;
+    os[c_above + i] = __int_as_float(ce.y);
   }
-  for (uint32_t i = first + take + tid; i < (uint32_t)k; i += NTH) {
+  for (uint32_t i = c_above + take + tid; i < (uint32_t)k; i += NTH) {
     oi[i] = -1;
     os[i] = -__builtin_inff();
+  }
+  if (sorted) {
+    // Sort the row's nout kept keys in place. Equal scores lie in one bin, and
+    // within a bin the row already holds them in key order (the list order,
+    // or the bin's sort), so (score, slot) is the total order; keyed rows,
+    // whose keys above bin tau came in arrival order, sort by (score, key)
+    // and take canonical scores from the sort entries. The slots' pairs wait
+    // in the upper half of the sort buffer (k <= E / 2).
+    const uint32_t nout = c_above + take;
+    int2* pair = reinterpret_cast<int2*>(ent + E / 2);
+    __threadfence_block();
+    __syncthreads();
+    for (uint32_t i = tid; i < nout; i += NTH) {
+      const int32_t x = oi[i];
+      const float y = os[i];
+      pair[i] = make_int2(x, __float_as_int(y));
+      ent[i] = comp_key(y, keyed ? (uint32_t)x : i);
+    }
+    const int P = next_pow2((int)nout < 1 ? 1 : (int)nout);
+    for (int i = tid; i < P; i += NTH)
+      if ((uint32_t)i >= nout) ent[i] = 0ull;
+    __syncthreads();
+    bitonic_sort_desc<NTH>(ent, P);
+    for (uint32_t i = tid; i < nout; i += NTH) {
+      const uint32_t g = comp_pos(ent[i]);
+      if (keyed) {
+        oi[i] = (int32_t)g;
+        os[i] = ord_inv((uint32_t)(ent[i] >> 32));
+      } else {
+        const int2 pr = pair[g];
+        oi[i] = pr.x;
+        os[i] = __int_as_float(pr.y);
+      }
+    }
   }
   if (stats && tid == 0) {
     int32_t* st = stats + (int64_t)row * LT_ROW_STATS;
