@@ -287,6 +287,10 @@ constexpr int kSelPerWide = 8;
 constexpr int kSelFewRows = 512;     // launches of at most this many rows use the wide blocks
 constexpr int kSecondSelectGrid = 512;  // blocks of the second select (persistent over its queue)
 
+// Threshold bins of at most this many keys are ranked by counting instead of
+// sorted.
+constexpr int kRankMax = 512;
+
 // LDS byte offset of the sort entries of k_select with NTH threads.
 constexpr size_t select_ent_offset(int nth) { return ((size_t)kMaxBins + 32 + nth + 16) * 4; }
 
@@ -489,24 +493,37 @@ __device__ __forceinline__ void select_row(int row, RowParam* params, const uint
   // the need = k - c_above best keys of bin tau, after the keys above it
   const uint32_t need = (uint32_t)k - c_above;
   const uint32_t take = min(need, nent);
-  {
-    const int P = next_pow2((int)nent < 1 ? 1 : (int)nent);
+  // the bin's i-th best key goes to slot c_above + i
+  auto emit = [&](uint32_t i, uint64_t e) {
+    const uint32_t gp = comp_pos(e);
+    if (keyed) {
+      oi[c_above + i] = (int32_t)gp;
+      os[c_above + i] = ord_inv((uint32_t)(e >> 32));
+      return;
+    }
+    const uint32_t s = gp / (uint32_t)cap, j = gp - s * (uint32_t)cap;
+    const int2 ce = cand[((int64_t)row * S + s) * cap + j];
+    oi[c_above + i] = ce.x;
+    os[c_above + i] = __int_as_float(ce.y);
+  };
+  if (nent <= (uint32_t)kRankMax) {
+    // a small bin: each key's rank is the number of keys above it (the sort
+    // entries are distinct), one pass over the bin per key and no barrier
+    // per sorting stage
+    __syncthreads();
+    for (uint32_t i = tid; i < nent; i += NTH) {
+      const uint64_t e = ent[i];
+      uint32_t r = 0;
+      for (uint32_t j = 0; j < nent; ++j) r += ent[j] > e;
+      if (r < take) emit(r, e);
+    }
+  } else {
+    const int P = next_pow2((int)nent);
     for (int i = tid; i < P; i += NTH)
       if ((uint32_t)i >= nent) ent[i] = 0ull;
     __syncthreads();
     bitonic_sort_desc<NTH>(ent, P);
-  }
-  for (uint32_t i = tid; i < take; i += NTH) {
-    uint32_t gp = comp_pos(ent[i]);
-    if (keyed) {
-      oi[c_above + i] = (int32_t)gp;
-      os[c_above + i] = ord_inv((uint32_t)(ent[i] >> 32));
-      continue;
-    }
-    uint32_t s = gp / (uint32_t)cap, j = gp - s * (uint32_t)cap;
-    int2 ce = cand[((int64_t)row * S + s) * cap + j];
-    oi[c_above + i] = ce.x;
-    os[c_above + i] = __int_as_float(ce.y);
+    for (uint32_t i = tid; i < take; i += NTH) emit(i, ent[i]);
   }
   for (uint32_t i = c_above + take + tid; i < (uint32_t)k; i += NTH) {
     oi[i] = -1;
