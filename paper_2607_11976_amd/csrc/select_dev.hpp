@@ -93,8 +93,10 @@ __device__ __forceinline__ void sort_output_row(int32_t* oi, float* os, int n, u
 // (k entries, padded with (-1, -inf)). Plain most-significant-digit radix
 // selection over the order keys: four 8-bit passes find the k-th key K*, then
 // one pass writes every key > K* and the lowest-index keys == K*. Each wave
-// streams a contiguous segment of the row (kRadixUnroll loads in flight per
-// lane) into its own histogram; after each pass the wave also counts its keys
+// streams a contiguous segment of the row (wave_stream) into its own
+// histogram; the passes after the first test a key's prefix as a float range
+// and the write pass compares floats with K*'s float (the order keys of the
+// keys that pass are computed only for them); after each pass the wave also counts its keys
 // above the pass's digit, so that after the last pass every wave knows how
 // many keys > K* and == K* lie in the segments before its own, and the write
 // pass places each hit without block barriers.
@@ -152,13 +154,16 @@ __device__ __forceinline__ void split_fallback_select(const float* srow, int rs,
     if (oi[i] >= 0) oi[i] = cidx[oi[i]];
 }
 
-// Loads in flight per lane, and the histogram passes (from the first) whose
-// lanes of the most common bins add their counts with one atomic per bin
-// (measured on MI355X, one row of 262144 / 1M / 4M keys per block: 32 loads
-// and one grouped bin in the first pass, 0.72 / 2.6 / 10.1 ms; 8 loads,
-// 0.76 / 2.8 / 12.4 ms; four grouped bins in two passes, slower).
+// Keys per lane of one streaming step, and the histogram passes (from the
+// first) whose lanes of the most common bins add their counts with one
+// atomic per bin. Measured on MI355X, one row of 262144 / 1M / 4M keys per
+// 256-thread block: 0.41 / 1.5 / 5.7 ms with 16 keys and the next step in
+// flight (0.72 / 2.6 / 10.1 ms before, with 32 plain loads per step and no
+// look-ahead; 24 or 32 keys per step, no faster); without the grouped first
+// pass the dense fallback of concentrated scores is 5% slower, four grouped
+// bins in two passes slower too.
 #ifndef LT_RADIX_UNROLL
-#define LT_RADIX_UNROLL 32
+#define LT_RADIX_UNROLL 16
 #endif
 #ifndef LT_RADIX_GROUP_PASSES
 #define LT_RADIX_GROUP_PASSES 1
@@ -168,6 +173,76 @@ __device__ __forceinline__ void split_fallback_select(const float* srow, int rs,
 #endif
 constexpr int kRadixUnroll = LT_RADIX_UNROLL;
 
+// One wave streams keys [s0, s1) of a row in steps of kWave * U keys (key
+// s0 + j * kWave * U + u * kWave + lane in x[u] of step j). The loads of the
+// next step are issued before the current step is processed, so that every
+// step but the first finds its keys loaded while the previous one ran. The
+// loads go through a buffer descriptor over the segment, whose range check
+// turns the keys past s1 into zeros without a branch; body(c0, x) handles
+// the step at key c0 (and tells the keys below s1 from those zeros itself,
+// without branches: a step whose body branches on that makes the compiler
+// wait for every load in flight). s0 and s1 are wave-uniform,
+// s1 - s0 < 2^30.
+template <int U, class Body>
+__device__ __forceinline__ void wave_stream(const float* row, int s0, int s1, Body&& body) {
+  constexpr int S = kWave * U;
+  // the descriptor lives in scalar registers: the address and length are
+  // made wave-uniform explicitly (a caller's arguments may sit in vector
+  // registers, and a descriptor there would need a loop per load)
+  const int len = __builtin_amdgcn_readfirstlane(s1 - s0);
+  if (len <= 0) return;
+  const uint64_t base = (uint64_t)(row + s0);
+  const float* ubase = (const float*)((uint64_t)(uint32_t)__builtin_amdgcn_readfirstlane((uint32_t)base) |
+                                      (uint64_t)(uint32_t)__builtin_amdgcn_readfirstlane((uint32_t)(base >> 32)) << 32);
+  // one descriptor per step (its base moves with the step, so every load
+  // takes the lane's fixed offset plus an immediate)
+  const int vo = lane_id() * 4;
+  auto load = [&](int off, float (&x)[U]) {
+    const int left = len - off;
+    const __amdgpu_buffer_rsrc_t rs =
+        __builtin_amdgcn_make_buffer_rsrc((void*)(ubase + off), 0, left > 0 ? (int)((uint32_t)left * 4u) : 0, kBufferRaw);
+#pragma unroll
+    for (int u = 0; u < U; ++u)
+      x[u] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rs, vo + u * kWave * 4, 0, 0));
+  };
+  // two steps per trip and one exit, at the bottom (an exit between the
+  // steps also makes the compiler wait for every load in flight): a step past
+  // s1 loads only zeros and its body finds no key below s1
+  float xa[U], xb[U];
+  load(0, xa);
+  for (int off = 0; off < len; off += 2 * S) {
+    load(off + S, xb);
+    body(s0 + off, xa);
+    load(off + 2 * S, xa);
+    body(s0 + off + S, xb);
+  }
+}
+
+// radix_select_row_at of a row of n <= k keys: every key is taken (a
+// function of its own: inside the selection its branch made the compiler
+// wait for every load in flight in the streaming loops).
+template <int NTH>
+__device__ __noinline__ void radix_copy_short_row(const float* row, int n, int k, int32_t* oi, float* os, bool sorted,
+                                                  uint8_t* lds, bool pad) {
+  uint64_t* ent = reinterpret_cast<uint64_t*>(lds + kRadixEnt);
+  const int tid = threadIdx.x;
+  auto fetch = [&](uint32_t idx) { return row[idx]; };
+  for (int i = tid; i < k; i += NTH) {
+    if (i < n) {
+      oi[i] = i;
+      os[i] = row[i];
+    } else if (pad) {
+      oi[i] = -1;
+      os[i] = -__builtin_inff();
+    }
+  }
+  if (sorted) {
+    __threadfence_block();
+    __syncthreads();
+    sort_output_row<NTH>(oi, os, n, ent, fetch);
+  }
+}
+
 // Not inlined: the callers inline it after a register-heavy scan, and a
 // separate allocation keeps its unrolled loads from spilling the scan.
 template <int NTH>
@@ -175,6 +250,14 @@ __device__ __noinline__ void radix_select_row_at(const float* row, int n, int k,
                                                  uint8_t* lds, bool pad) {
   constexpr int NW = NTH / kWave, U = kRadixUnroll;
   static_assert(NW <= kRadixWaves, "one histogram per wave");
+  static_assert(NW >= 4, "segments of fewer than 2^30 keys");
+  // the sizes and flags are the same in every lane (arguments arrive in
+  // vector registers): branches on them stay scalar, which keeps the loads
+  // of the streaming loops in flight across their steps
+  n = __builtin_amdgcn_readfirstlane(n);
+  k = __builtin_amdgcn_readfirstlane(k);
+  sorted = __builtin_amdgcn_readfirstlane((int)sorted) != 0;
+  pad = __builtin_amdgcn_readfirstlane((int)pad) != 0;
   uint32_t* hist = reinterpret_cast<uint32_t*>(lds);              // [NW][256]
   uint32_t* tot = reinterpret_cast<uint32_t*>(lds + kRadixTot);   // [256]
   uint32_t* tmp = reinterpret_cast<uint32_t*>(lds + kRadixTmp);   // [32]
@@ -184,33 +267,13 @@ __device__ __noinline__ void radix_select_row_at(const float* row, int n, int k,
   auto fetch = [&](uint32_t idx) { return row[idx]; };
 
   if (n <= k) {
-    for (int i = tid; i < k; i += NTH) {
-      if (i < n) {
-        oi[i] = i;
-        os[i] = row[i];
-      } else if (pad) {
-        oi[i] = -1;
-        os[i] = -__builtin_inff();
-      }
-    }
-    if (sorted) {
-      __threadfence_block();
-      __syncthreads();
-      sort_output_row<NTH>(oi, os, n, ent, fetch);
-    }
+    radix_copy_short_row<NTH>(row, n, k, oi, os, sorted, lds, pad);
     return;
   }
-
-  // this wave's segment [s0, s1) of the row, read kWave * U keys per step
+  // this wave's segment [s0, s1) of the row
   const int seg = ((n + NW - 1) / NW + kWave - 1) / kWave * kWave;
-  const int s0 = min(wave * seg, n), s1 = min(s0 + seg, n);
-  auto load = [&](int c0, float (&x)[U]) {
-#pragma unroll
-    for (int u = 0; u < U; ++u) {
-      const int i = c0 + u * kWave + l;
-      x[u] = i < s1 ? row[i] : 0.0f;
-    }
-  };
+  const int wv = __builtin_amdgcn_readfirstlane(wave);
+  const int s0 = min(wv * seg, n), s1 = min(s0 + seg, n);
 
   uint32_t prefix = 0, pmask = 0, remaining = (uint32_t)k;
   uint32_t gbefore = 0;  // this wave's keys above the digits chosen so far (wave-uniform)
@@ -219,32 +282,55 @@ __device__ __noinline__ void radix_select_row_at(const float* row, int n, int k,
     const int shift = 24 - 8 * pass;
     for (int b = tid; b < NW * 256; b += NTH) hist[b] = 0;
     __syncthreads();
-    for (int c0 = s0; c0 < s1; c0 += kWave * U) {
-      float x[U];
-      load(c0, x);
+    // GROUP (the first passes): concentrated scores share their leading
+    // bytes, so the lanes of the few most common bins add their counts with
+    // one atomic per bin
+    auto hist_pass = [&]<bool GROUP>() {
+      wave_stream<U>(row, s0, s1, [&](int c0, const float (&x)[U]) {
 #pragma unroll
-      for (int u = 0; u < U; ++u) {
-        if (c0 + u * kWave >= s1) break;  // wave-uniform
-        const bool v = c0 + u * kWave + l < s1;
-        const uint32_t key = ord_key(x[u]);
-        const uint32_t b = (key >> shift) & 255u;
-        bool in = v && (key & pmask) == prefix;
-        if (pass < LT_RADIX_GROUP_PASSES) {
-          // concentrated scores share their leading bytes: the lanes of the
-          // few most common bins add their counts with one atomic per bin
-          uint64_t left = __ballot(in);
+        for (int u = 0; u < U; ++u) {
+          // (bool & bool: a short-circuit && would branch)
+          const bool v = c0 + u * kWave + l < s1;
+          const uint32_t key = ord_key(x[u]);
+          const uint32_t b = (key >> shift) & 255u;
+          bool in = v & ((key & pmask) == prefix);
+          if constexpr (GROUP) {
+            uint64_t left = __ballot(in);
 #pragma unroll
-          for (int g = 0; g < LT_RADIX_GROUP_BINS; ++g) {
-            if (left == 0) break;
-            const uint32_t bg = __builtin_amdgcn_readlane(b, __builtin_ctzll(left));
-            const uint64_t mg = __ballot(in && b == bg);
-            if (l == (int)__builtin_ctzll(mg)) atomicAdd(&hw[bg], (uint32_t)__popcll(mg));
-            in = in && b != bg;
-            left &= ~mg;
+            for (int g = 0; g < LT_RADIX_GROUP_BINS; ++g) {
+              if (left == 0) break;
+              const uint32_t bg = __builtin_amdgcn_readlane(b, __builtin_ctzll(left));
+              const uint64_t mg = __ballot(in && b == bg);
+              if (l == (int)__builtin_ctzll(mg)) atomicAdd(&hw[bg], (uint32_t)__popcll(mg));
+              in = in && b != bg;
+              left &= ~mg;
+            }
           }
+          if (in) atomicAdd(&hw[b], 1u);
         }
-        if (in) atomicAdd(&hw[b], 1u);
-      }
+      });
+    };
+    if (pass < LT_RADIX_GROUP_PASSES) {
+      hist_pass.template operator()<true>();
+    } else if (prefix == 0u) {
+      hist_pass.template operator()<false>();
+    } else {
+      // a prefix other than 0 (the NaN key) spans the order keys of the
+      // floats in [lo, hi]: two compares find the keys of the prefix, and
+      // only their digits are computed (keys past +inf are NaN codes no
+      // score maps to; below +0 lies -0's unused key, so the top of a range
+      // that ends there is the largest negative float)
+      const uint32_t lk = prefix < 0x007FFFFFu ? 0x007FFFFFu : prefix;
+      uint32_t hk = prefix | ~pmask;
+      hk = hk > 0xFF800000u ? 0xFF800000u : hk == 0x7FFFFFFFu ? 0x7FFFFFFEu : hk;
+      const float lo = ord_inv(lk), hi = ord_inv(hk);
+      wave_stream<U>(row, s0, s1, [&](int c0, const float (&x)[U]) {
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+          const bool in = (c0 + u * kWave + l < s1) & (x[u] >= lo) & (x[u] <= hi);
+          if (in) atomicAdd(&hw[(ord_key(x[u]) >> shift) & 255u], 1u);
+        }
+      });
     }
     __syncthreads();
     for (int b = tid; b < 256; b += NTH) {
@@ -262,7 +348,10 @@ __device__ __noinline__ void radix_select_row_at(const float* row, int n, int k,
       }
     }
     __syncthreads();
-    const uint32_t d = tmp[16], above = tmp[17];
+    // (read into scalar registers: the digit chooses the next pass's loop,
+    // and a choice the compiler cannot see as wave-uniform becomes a masked
+    // branch around loops whose loads then all wait for each other)
+    const uint32_t d = __builtin_amdgcn_readfirstlane(tmp[16]), above = __builtin_amdgcn_readfirstlane(tmp[17]);
     // this wave's keys of the current prefix in bins above d (and == d)
     uint32_t mine = 0;
     for (int b = l; b < 256; b += kWave) mine += (uint32_t)b > d ? hw[b] : 0u;
@@ -291,16 +380,18 @@ __device__ __noinline__ void radix_select_row_at(const float* row, int n, int k,
   __syncthreads();
   // a key > K* goes after the keys > K* and the taken keys == K* of lower
   // index; a key == K* is taken while fewer than `need` of lower index were
-  if (cg != 0 || (ce != 0 && e < need)) {  // wave-uniform
-    for (int c0 = s0; c0 < s1; c0 += kWave * U) {
-      float x[U];
-      load(c0, x);
+  // for K* other than the NaN key, the float K with that key: key > K* and
+  // key == K* are the float compares x > K and x == K (NaN fails both; -0
+  // and +0 share a key and compare equal); for the NaN key, key > K* is
+  // "not NaN" and key == K* is "NaN"
+  const float kf = ord_inv(kstar);
+  auto write_pass = [&]<bool KNAN>() {
+    wave_stream<U>(row, s0, s1, [&](int c0, const float (&x)[U]) {
 #pragma unroll
       for (int u = 0; u < U; ++u) {
-        if (c0 + u * kWave >= s1) break;  // wave-uniform
         const int i = c0 + u * kWave + l;
-        const uint32_t key = i < s1 ? ord_key(x[u]) : 0u;
-        const bool gt = i < s1 && key > kstar, eq = i < s1 && key == kstar;
+        const bool v = i < s1;
+        const bool gt = v & (KNAN ? x[u] == x[u] : x[u] > kf), eq = v & (KNAN ? x[u] != x[u] : x[u] == kf);
         const uint64_t mg = __ballot(gt), me = __ballot(eq);
         if ((mg | me) == 0) continue;
         const uint32_t rg = g + mbcnt64(mg), re = e + mbcnt64(me);
@@ -316,7 +407,11 @@ __device__ __noinline__ void radix_select_row_at(const float* row, int n, int k,
         g += (uint32_t)__popcll(mg);
         e += (uint32_t)__popcll(me);
       }
-    }
+    });
+  };
+  if (cg != 0 || (ce != 0 && e < need)) {  // wave-uniform
+    if (kstar == 0u) write_pass.template operator()<true>();
+    else write_pass.template operator()<false>();
   }
   if (sorted) {
     __threadfence_block();

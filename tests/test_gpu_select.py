@@ -131,3 +131,66 @@ def test_select_c1_shaped_rows(lib):
     offs = workloads.causal_offsets(nq, nk)
     gi, gs, _ = _run(scores, nk, k, offs, "select", sorted_output=True)
     _check_all(scores, nk, k, offs, gi, gs, True)
+
+
+def _order_key_edge_rows(n, seed):
+    """Rows whose k-th score (k = 300) sits where the order-key digits of the
+    radix passes meet the float encoding: among negative denormals (just
+    below -0), at -inf, at NaN, at +inf, among positive denormals, at the
+    largest finite float, and in rows of arbitrary bit patterns (NaN codes of
+    either sign included)."""
+    rng = np.random.default_rng(seed)
+
+    def f32(b):
+        return np.asarray(b, dtype=np.uint32).view(np.float32)
+
+    rows = []
+    r = f32(rng.integers(0x80000001, 0x80800000, n, dtype=np.uint64))  # negative denormals
+    r[:60] = 1.0
+    r[60:110] = 0.0
+    r[110:160] = -0.0
+    rows.append(r)
+    r = np.full(n, -np.inf, np.float32)
+    r[:50] = np.nan
+    r[50:150] = np.inf
+    r[150:250] = rng.standard_normal(100)
+    rows.append(r)
+    r = np.full(n, np.nan, np.float32)
+    r[:100] = rng.standard_normal(100)
+    rows.append(r)
+    r = rng.standard_normal(n).astype(np.float32)
+    r[:500] = np.inf
+    rows.append(r)
+    r = f32(rng.integers(1, 0x00800000, n, dtype=np.uint64))  # positive denormals
+    r[:40] = 0.0
+    r[40:80] = -0.0
+    r[80:100] = -1.0
+    rows.append(r)
+    r = f32(rng.integers(0x7F7FF000, 0x7F800000, n, dtype=np.uint64))  # the largest finite floats
+    r[:30] = np.inf
+    r[30:60] = np.nan
+    rows.append(r)
+    for _ in range(2):
+        rows.append(f32(rng.integers(0, 1 << 32, n, dtype=np.uint64)))
+    for r in rows:
+        rng.shuffle(r)
+    # rows padded to a multiple of 4 floats with a large score the selection
+    # must not see
+    ld = (n + 3) // 4 * 4
+    out = np.full((len(rows), ld), np.float32(3e38), np.float32)
+    out[:, :n] = np.stack(rows)
+    return torch.from_numpy(out)
+
+
+@pytest.mark.parametrize("entry", ["radix", "select"])
+@pytest.mark.parametrize("sorted_out", [False, True])
+@pytest.mark.parametrize("n", [5000, 40001])
+def test_radix_order_key_edges(lib, entry, sorted_out, n):
+    """Exact selection where the k-th score is a special or boundary float
+    (the scores-in entry with every row sent to the fallback's radix
+    selection, and the plain radix entry)."""
+    k = 300
+    scores = _order_key_edge_rows(n, seed=n)
+    opt = dict(force_fallback=True) if entry == "select" else {}
+    gi, gs, _ = _run(scores, n, k, None, entry, sorted_output=sorted_out, **opt)
+    _check_all(scores, n, k, None, gi, gs, sorted_out)
