@@ -370,6 +370,12 @@ int lt_indexer_topk(const void* q, const float* q_scale, const float* w, const v
   if ((e = launch_fused_fallback(a, k, fb_flags, qctl, queue, rflag + nq, fs.batch, fs.grid * fs.batch, scratch,
                                  fbc_idx, fbc_score, out_idx, out_scores, st)) != hipSuccess)
     return hip_status(e);
+  // the dense fallback mode's selection (the wide scan's fallback has no
+  // dense mode)
+  if (!r.shared && (e = launch_fallback_rows(qctl, rflag + nq, scratch, nq, nk, offs, r.starts, k, fb_flags,
+                                             fs.grid * fs.batch, sh.queries_per_block, out_idx, out_scores, st)) !=
+                       hipSuccess)
+    return hip_status(e);
   record(r, LT_NUM_STAGE_EVENTS - 1, st);
   return LT_OK;
 }

@@ -102,7 +102,7 @@ hipError_t launch_fused_scan(const ScoreArgs& a, const RowParam* params, int S, 
                              const uint32_t* qctl, hipStream_t st);
 // Exact fallback for queued rows (queue, length qctl[0]): dense re-score
 // into scratch rows of nk floats (`slots` of them), then radix select. Both
-// fallback kernels run kFallbackGrid blocks in one of two modes, chosen on
+// fallback kernels run kFallbackGrid blocks in one of three modes, chosen on
 // the device from the queue length n:
 // * split (fallback_chunks(...) > 1: few rows, each with its own scratch
 //   row): the visible keys of every queued row are cut into that many chunks,
@@ -110,6 +110,11 @@ hipError_t launch_fused_scan(const ScoreArgs& a, const RowParam* params, int S, 
 //   the candidate arrays; the block that completes a row's last chunk
 //   (counter qctl[kQctlDone + entry]) selects the row from its chunks'
 //   candidates.
+// * dense (fallback_dense(...): every row of the call has a scratch row of
+//   its own, nq <= slots): the blocks take (query tile, key slice) items of
+//   the tiles holding queued rows, slice by slice, and write each queued row
+//   t's scores to scratch row t, every tile scored once; launch_fallback_rows
+//   then radix-selects each queued row, one block per row.
 // * whole rows: blocks below slots / batch take queue entries from the
 //   cursor qctl[kQctlCursor] and re-score whole rows into their own scratch
 //   rows [blockIdx][batch][nk]. fbflag (or NULL) [nq]: 1 for the queued rows;
@@ -136,10 +141,25 @@ __host__ __device__ inline int fallback_chunks(uint32_t n, int grid, int slots, 
   if (c > by_keys) c = by_keys;
   return c < 2 ? 1 : c;
 }
+// Dense mode (see above): any queue the split mode does not take, when every
+// row has a scratch row and the scan's query tiles hold at most 64 rows (the
+// tile's row slots are bytes). kDenseSlice keys per item.
+constexpr int kDenseSlice = 8192;
+__host__ __device__ inline bool fallback_dense(uint32_t n, int nq, int grid, int slots, int nk, int qt) {
+  return n > 0 && qt <= 64 && nq <= slots && fallback_chunks(n, grid, slots, nk) == 1;
+}
 // cidx / cscore [kFallbackGrid * k]: the split mode's chunk candidates.
 hipError_t launch_fused_fallback(const ScoreArgs& a, int k, uint32_t flags, uint32_t* qctl, const int32_t* queue,
                                  int32_t* fbflag, int batch, int slots, float* scratch, int32_t* cidx, float* cscore,
                                  int32_t* out_i, float* out_s, hipStream_t st);
+// The dense mode's selection: a block per row t < nq whose fallback flag
+// fbflag[t] is 1 radix-selects scratch row t over the row's visible keys
+// (offs / starts as in ScoreArgs) into out_i / out_s [nq][k]; every block
+// returns at once unless fallback_dense(qctl[0], nq, kFallbackGrid, slots,
+// nk, qt) holds. The host launches it only where that can hold.
+hipError_t launch_fallback_rows(const uint32_t* qctl, const int32_t* fbflag, const float* scratch, int nq, int nk,
+                                const int32_t* offs, const int32_t* starts, int k, uint32_t flags, int slots,
+                                int qt, int32_t* out_i, float* out_s, hipStream_t st);
 
 // ---- wide-vector scan (wide.hip): bf16, one head, long vectors ----
 // wide_shape(...).supported is 0 for shapes the wide scan does not build.

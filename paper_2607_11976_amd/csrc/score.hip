@@ -1433,6 +1433,42 @@ __global__ __launch_bounds__(C::NTHREADS) void k_fused_fallback(ScoreArgs a, int
   int* bn = brow + kMaxFallbackBatch;  // [0] rows of the pass, [1] select after the pass
   const uint32_t n = qctl[0];
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
+  if (fbflag && fallback_dense(n, a.nq, gridDim.x, slots, a.nk, C::QT)) {
+    // dense mode: items (tile x, slice y), consecutive items on the same
+    // slice; queued row t of tile x goes to scratch row t (slot t - q0)
+    const int tiles = (a.nq + C::QT - 1) / C::QT, nsl = (a.nk + kDenseSlice - 1) / kDenseSlice;
+    for (int item = blockIdx.x; item < tiles * nsl; item += gridDim.x) {
+      const int q0 = (item % tiles) * C::QT, y = item / tiles;
+      if (threadIdx.x == 0) {
+        brow[0] = INT_MAX;  // the union of the queued rows' visible ranges
+        brow[1] = 0;
+      }
+      __syncthreads();
+      if (threadIdx.x < C::QT) {
+        const int t = q0 + (int)threadIdx.x;
+        const bool on = t < a.nq && fbflag[t] == 1;
+        smap[threadIdx.x] = on ? (int8_t)threadIdx.x : (int8_t)-1;
+        if (on) {
+          const RowRange rr = row_range(a.offs, a.starts, t, a.nk);
+          if (rr.e > rr.s) {
+            atomicMin(&brow[0], rr.s);
+            atomicMax(&brow[1], rr.e);
+          }
+        }
+      }
+      __syncthreads();
+      const int kb = max(y * kDenseSlice, brow[0]), ke = min(y * kDenseSlice + kDenseSlice, brow[1]);
+      if (kb < ke) {  // block-uniform
+        const int qbase = q0 + wave * C::QW;
+        WaveQ<C> wq;
+        load_q<C>(wq, a, qbase);
+        RowSink<C> sink{scratch + (int64_t)q0 * a.nk, a.nk, smap, qbase, q0};
+        wg_scan<C>(a, SrcContig{}, kb, ke, lds, wq, sink);
+      }
+      __syncthreads();  // smap and the range are rewritten by the next item
+    }
+    return;
+  }
   const int chunks = fallback_chunks(n, gridDim.x, slots, a.nk);
   const bool split = chunks > 1;
   // split: block = (queue entry, chunk of that row's visible keys), one pass;

@@ -631,6 +631,21 @@ __global__ __launch_bounds__(kSelThreads) void k_radix(const float* scores, int6
                                 out_s + (int64_t)row * k, flags & LT_SORTED_OUTPUT, lds);
 }
 
+// The fused path's dense fallback mode, second half: queued row t (flag 1)
+// was re-scored into scratch row t; one block selects it.
+__global__ __launch_bounds__(kSelThreads) void k_fallback_rows(const uint32_t* qctl, const int32_t* fbflag,
+                                                               const float* scratch, int nq, int nk,
+                                                               const int32_t* offs, const int32_t* starts, int k,
+                                                               uint32_t flags, int slots, int qt, int32_t* out_i,
+                                                               float* out_s) {
+  extern __shared__ __align__(16) uint8_t lds[];
+  const int row = blockIdx.x;
+  if (!fallback_dense(qctl[0], nq, kFallbackGrid, slots, nk, qt) || fbflag[row] != 1) return;  // block-uniform
+  const RowRange rr = row_range(offs, starts, row, nk);
+  radix_select_row<kSelThreads>(scratch + (int64_t)row * nk + rr.s, rr.e - rr.s, k, out_i + (int64_t)row * k,
+                                out_s + (int64_t)row * k, flags & LT_SORTED_OUTPUT, lds, rr.s);
+}
+
 // ---------------------------------------------------------------------------
 // Host launchers
 // ---------------------------------------------------------------------------
@@ -719,6 +734,18 @@ hipError_t launch_fallback_scores(const float* scores, int64_t stride, int nk, c
                               (int)radix_lds_bytes(k));
   hipLaunchKernelGGL(k_fallback_scores, dim3(grid), dim3(kSelThreads), radix_lds_bytes(k), st, scores,
                      stride, nk, offs, starts, k, flags, qctl, queue, out_i, out_s);
+  return hipGetLastError();
+}
+
+hipError_t launch_fallback_rows(const uint32_t* qctl, const int32_t* fbflag, const float* scratch, int nq, int nk,
+                                const int32_t* offs, const int32_t* starts, int k, uint32_t flags, int slots,
+                                int qt, int32_t* out_i, float* out_s, hipStream_t st) {
+  if (nq <= 0 || nq > slots || qt > 64) return hipSuccess;  // the dense mode cannot hold
+  const size_t lds = radix_lds_bytes(k);
+  if (lds > 65536)
+    (void)hipFuncSetAttribute((const void*)k_fallback_rows, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+  hipLaunchKernelGGL(k_fallback_rows, dim3(nq), dim3(kSelThreads), lds, st, qctl, fbflag, scratch, nq, nk, offs,
+                     starts, k, flags, slots, qt, out_i, out_s);
   return hipGetLastError();
 }
 

@@ -284,13 +284,17 @@ def test_dense_fallback_splits_few_rows_over_blocks(lib, law, sorted_out):
     _check_tol(x, cfg.dtype, k, mode, gi, gs, rows=rows)
 
 
-@pytest.mark.parametrize("nq", [128, 129], ids=["split_128_rows", "whole_rows_129"])
-def test_dense_fallback_mode_boundary(lib, nq):
+@pytest.mark.parametrize("nq,nk", [(128, 16384), (129, 16384), (2304, 8192)],
+                         ids=["split_128_rows", "dense_129_rows", "whole_rows_2304"])
+def test_dense_fallback_mode_boundary(lib, nq, nk):
     """The fallback splits rows over blocks for up to 128 queued rows (two
-    chunks each here) and takes whole rows from the shared cursor above that:
-    both sides of the switch, every row forced, causal rows of different
-    lengths, equal to radix selection over the dense scores bit for bit."""
-    nk, k = 16384, 300
+    chunks each here); above that, while every row of the call has a scratch
+    row of its own (here up to 2048 rows), it re-scores the queued rows'
+    query tiles in (tile, key slice) items and selects each row in a block
+    of its own; beyond, blocks take whole rows from the shared cursor. Each
+    mode with every row forced, causal rows of different lengths, equal to
+    radix selection over the dense scores bit for bit."""
+    k = 300
     cfg = workloads.scaled(workloads.CONFIGS["dsa_bf16_128k"], nq=nq, nk=nk)
     x = workloads.generate(cfg, seed=37)
     gi, gs, st = _fused(x, k, "dsa", sorted_output=True, force_fallback=True)
