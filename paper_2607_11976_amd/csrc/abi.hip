@@ -20,7 +20,9 @@ namespace {
 
 constexpr int kDefaultBins = 256;
 constexpr size_t kFallbackScratchBudget = 2ull << 30;  // bytes of scratch the dense fallback may take
-constexpr int kFallbackGridScores = 256;
+// blocks of the scores-in fallback: one per row up to 2048 rows (several
+// resident per CU hide the radix select's load latency), at least 256
+constexpr int kFallbackGridScoresMin = 256, kFallbackGridScoresMax = 2048;
 constexpr int kTargetBlocks = 256;          // one block per CU before key splitting stops
 constexpr int kMinSplitKeys = 512;          // shortest key split the automatic choice makes
 constexpr int kMaxAutoSplits = 64;
@@ -464,7 +466,8 @@ int lt_topk_select(const float* scores, int64_t stride, int32_t nq, int32_t nk, 
     return hip_status(e);
   record(r, LT_STAGE_FALLBACK, st);
   if ((e = launch_fallback_scores(scores, stride, nk, offs, r.starts, k, r.flags, qctl, queue, out_idx, out_scores,
-                                  kFallbackGridScores, st)) != hipSuccess)
+                                  std::min(std::max(nq, kFallbackGridScoresMin), kFallbackGridScoresMax), st)) !=
+      hipSuccess)
     return hip_status(e);
   record(r, LT_NUM_STAGE_EVENTS - 1, st);
   return LT_OK;
