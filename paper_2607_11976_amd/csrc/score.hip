@@ -1420,7 +1420,9 @@ constexpr int fallback_meta_lds() { return ((C::QT + 15) & ~15) + kMaxFallbackBa
 // Exact fallback of the queued rows: dense re-score of each row's visible keys
 // into scratch, then radix select, in split mode (few rows: each row's keys
 // cut into chunks over many blocks, each selecting its chunk's top-k, the
-// last one merging them) or whole-row mode (see launch_fused_fallback).
+// last one merging them), dense mode (the queued rows' tiles scored once in
+// (tile, key slice) items; the selection is launch_fallback_rows') or
+// whole-row mode (see launch_fused_fallback).
 template <class C>
 __global__ __launch_bounds__(C::NTHREADS) void k_fused_fallback(ScoreArgs a, int k, uint32_t flags, uint32_t* qctl,
                                                                 const int32_t* queue, int32_t* fbflag, int batch,
