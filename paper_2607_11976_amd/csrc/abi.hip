@@ -94,9 +94,9 @@ Layout carve(int nq, int nk, const Resolved& r, bool fused) {
   L.gate = fused ? take((size_t)nq * 8) : 0;  // published bins: [nq] ints (wide), [nq][8] bytes
   const FallbackShape fs = fallback_shape(nq, nk);
   L.scratch = fused ? take((size_t)fs.grid * fs.batch * nk * 4) : 0;
-  // split fallback: the chunks' top-k candidates, (index, score) arrays of
-  // kFallbackGrid * k entries each
-  L.fbcand = fused ? take((size_t)kFallbackGrid * r.k * 8) : 0;
+  // split fallback (both entries): the chunks' top-k candidates, (index,
+  // score) arrays of kFallbackGrid * k entries each
+  L.fbcand = take((size_t)kFallbackGrid * r.k * 8);
   L.total = off;
   return L;
 }
@@ -447,6 +447,8 @@ int lt_topk_select(const float* scores, int64_t stride, int32_t nq, int32_t nk, 
   uint32_t* cnt = reinterpret_cast<uint32_t*>(ws + L.cnt);
   uint32_t* hist = reinterpret_cast<uint32_t*>(ws + L.hist);
   int2* cand = reinterpret_cast<int2*>(ws + L.cand);
+  int32_t* fbc_idx = reinterpret_cast<int32_t*>(ws + L.fbcand);
+  float* fbc_score = reinterpret_cast<float*>(ws + L.fbcand + (size_t)kFallbackGrid * k * 4);
 
   hipError_t e;
   record(r, LT_STAGE_SAMPLE, st);
@@ -465,7 +467,8 @@ int lt_topk_select(const float* scores, int64_t stride, int32_t nq, int32_t nk, 
                          queue, nullptr, nullptr, r.stats, st)) != hipSuccess)
     return hip_status(e);
   record(r, LT_STAGE_FALLBACK, st);
-  if ((e = launch_fallback_scores(scores, stride, nk, offs, r.starts, k, r.flags, qctl, queue, out_idx, out_scores,
+  if ((e = launch_fallback_scores(scores, stride, nk, offs, r.starts, k, r.flags, qctl, queue, fbc_idx, fbc_score,
+                                  out_idx, out_scores,
                                   std::min(std::max(nq, kFallbackGridScoresMin), kFallbackGridScoresMax), st)) !=
       hipSuccess)
     return hip_status(e);

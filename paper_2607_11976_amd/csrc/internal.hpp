@@ -40,9 +40,17 @@ hipError_t launch_select_second(RowParam* params, const uint32_t* cnt, const uin
                                 int nq, int S, int HS, int cap, int m, int k, int E, uint32_t flags, int32_t* out_i,
                                 float* out_s, uint32_t* qctl, int32_t* queue, int32_t* rqueue, int32_t* rflag,
                                 int32_t* stats, hipStream_t st);
+// Exact fallback of the scores-in entry for the queued rows (queue, length
+// qctl[0]), radix selection straight from the caller's score rows, `grid`
+// blocks: few rows (fallback_chunks over min(grid, kFallbackGrid) blocks)
+// have their visible keys cut into chunks, one block per (row, chunk), each
+// selecting its chunk's top-k into cidx / cscore [kFallbackGrid * k] and
+// counting the chunk on qctl[kQctlDone + entry], the last one selecting the
+// row from the chunks' candidates; otherwise one block per row.
 hipError_t launch_fallback_scores(const float* scores, int64_t stride, int nk, const int32_t* offs,
-                                  const int32_t* starts, int k, uint32_t flags, const uint32_t* qctl,
-                                  const int32_t* queue, int32_t* out_i, float* out_s, int grid, hipStream_t st);
+                                  const int32_t* starts, int k, uint32_t flags, uint32_t* qctl,
+                                  const int32_t* queue, int32_t* cidx, float* cscore, int32_t* out_i, float* out_s,
+                                  int grid, hipStream_t st);
 hipError_t launch_radix(const float* scores, int64_t stride, int nq, int nk, const int32_t* offs,
                         int k, uint32_t flags, int32_t* out_i, float* out_s, hipStream_t st);
 

@@ -606,9 +606,27 @@ __global__ __launch_bounds__(NTH) void k_select_second(
 // ---------------------------------------------------------------------------
 __global__ __launch_bounds__(kSelThreads) void k_fallback_scores(
     const float* scores, int64_t stride, int nk, const int32_t* offs, const int32_t* starts, int k,
-    uint32_t flags, const uint32_t* qctl, const int32_t* queue, int32_t* out_i, float* out_s) {
+    uint32_t flags, uint32_t* qctl, const int32_t* queue, int32_t* cidx, float* cscore, int32_t* out_i,
+    float* out_s) {
   extern __shared__ __align__(16) uint8_t lds[];
+  __shared__ int last;
   const uint32_t n = qctl[0];
+  // split mode (few rows: up to kFallbackGrid blocks over the rows' chunks,
+  // no scratch rows needed), else one block per queued row
+  const int chunks = fallback_chunks(n, min((int)gridDim.x, kFallbackGrid), INT_MAX, nk);
+  if (chunks > 1) {
+    if (blockIdx.x >= n * (uint32_t)chunks) return;  // block-uniform
+    const int e = blockIdx.x / chunks, c = blockIdx.x - e * chunks;
+    const int row = queue[e];
+    const RowRange rr = row_range(offs, starts, row, nk);
+    const int len = rr.e > rr.s ? rr.e - rr.s : 0, per = (len + chunks - 1) / chunks;
+    const int kb = min(rr.s + c * per, rr.s + len), ke = min(kb + per, rr.s + len);
+    const int64_t cb = (int64_t)e * chunks * k;
+    split_fallback_select<kSelThreads>(scores + (int64_t)row * stride, rr.s, len, per, chunks, c, kb, ke, k,
+                                       cidx + cb, cscore + cb, &qctl[kQctlDone + e], out_i + (int64_t)row * k,
+                                       out_s + (int64_t)row * k, flags & LT_SORTED_OUTPUT, lds, &last);
+    return;
+  }
   for (uint32_t r = blockIdx.x; r < n; r += gridDim.x) {
     const int row = queue[r];
     const RowRange rr = row_range(offs, starts, row, nk);
@@ -727,13 +745,14 @@ hipError_t launch_select_second(RowParam* params, const uint32_t* cnt, const uin
 }
 
 hipError_t launch_fallback_scores(const float* scores, int64_t stride, int nk, const int32_t* offs,
-                                  const int32_t* starts, int k, uint32_t flags, const uint32_t* qctl,
-                                  const int32_t* queue, int32_t* out_i, float* out_s, int grid, hipStream_t st) {
+                                  const int32_t* starts, int k, uint32_t flags, uint32_t* qctl,
+                                  const int32_t* queue, int32_t* cidx, float* cscore, int32_t* out_i, float* out_s,
+                                  int grid, hipStream_t st) {
   if (radix_lds_bytes(k) > 65536)
     (void)hipFuncSetAttribute((const void*)k_fallback_scores, hipFuncAttributeMaxDynamicSharedMemorySize,
                               (int)radix_lds_bytes(k));
   hipLaunchKernelGGL(k_fallback_scores, dim3(grid), dim3(kSelThreads), radix_lds_bytes(k), st, scores,
-                     stride, nk, offs, starts, k, flags, qctl, queue, out_i, out_s);
+                     stride, nk, offs, starts, k, flags, qctl, queue, cidx, cscore, out_i, out_s);
   return hipGetLastError();
 }
 

@@ -194,3 +194,27 @@ def test_radix_order_key_edges(lib, entry, sorted_out, n):
     opt = dict(force_fallback=True) if entry == "select" else {}
     gi, gs, _ = _run(scores, n, k, None, entry, sorted_output=sorted_out, **opt)
     _check_all(scores, n, k, None, gi, gs, sorted_out)
+
+
+@pytest.mark.parametrize("sorted_out", [False, True])
+def test_select_fallback_splits_few_long_rows(lib, sorted_out):
+    """A few forced rows of a million scores take the scores-in fallback's
+    split mode (each row's visible keys in chunks over many blocks, the last
+    chunk's block merging the chunks' top k): rows of different lengths and
+    starts, one shorter than k, one with special values, against the oracle."""
+    nq, nk, k = 5, 1_000_001, 2048
+    ld = (nk + 3) // 4 * 4
+    rows = workloads.score_rows(nq, nk, seed=21, kind="ties", ld=ld).numpy()
+    rows[4, : nk // 2] = workloads.score_rows(1, nk // 2, seed=22, kind="special").numpy()[0]
+    scores = torch.from_numpy(rows)
+    offs = np.array([nk, 700_001, 1000, nk, 999_999], dtype=np.int32)
+    starts = np.array([0, 3, 0, 400_000, 1], dtype=np.int32)
+    ri, rs = orc.topk_select(rows, nk, k, offs, visible_start=starts)
+    gi, gs = lt.topk_select(scores.cuda(), k, num_keys=nk, causal_offsets=torch.from_numpy(offs).cuda(),
+                            options=lt.make_options(sorted_output=sorted_out, force_fallback=True,
+                                                    visible_start=torch.from_numpy(starts).cuda()))
+    torch.cuda.synchronize()
+    s0, e0 = orc.visible_ranges(offs, starts, nq, nk)
+    gi, gs = gi.cpu().numpy(), gs.cpu().numpy()
+    for t in range(nq):
+        check_row_exact(gi[t], gs[t], ri[t], rs[t], int(e0[t] - s0[t]), k, sorted_out)
