@@ -284,9 +284,12 @@ def test_dense_fallback_splits_few_rows_over_blocks(lib, law, sorted_out):
     _check_tol(x, cfg.dtype, k, mode, gi, gs, rows=rows)
 
 
-@pytest.mark.parametrize("nq,nk", [(128, 16384), (129, 16384), (2304, 8192)],
-                         ids=["split_128_rows", "dense_129_rows", "whole_rows_2304"])
-def test_dense_fallback_mode_boundary(lib, nq, nk):
+@pytest.mark.parametrize("base,nq,nk", [("dsa_bf16_128k", 128, 16384), ("dsa_bf16_128k", 129, 16384),
+                                        ("dsa_bf16_128k", 2304, 8192), ("dsa_fp8_1m", 300, 20000),
+                                        ("tiny_fp32", 200, 9000)],
+                         ids=["split_128_rows", "dense_129_rows", "whole_rows_2304", "dense_fp8_300_rows",
+                              "dense_f32_h4_200_rows"])
+def test_dense_fallback_mode_boundary(lib, base, nq, nk):
     """The fallback splits rows over blocks for up to 128 queued rows (two
     chunks each here); above that, while every row of the call has a scratch
     row of its own (here up to 2048 rows), it re-scores the queued rows'
@@ -295,14 +298,14 @@ def test_dense_fallback_mode_boundary(lib, nq, nk):
     mode with every row forced, causal rows of different lengths, equal to
     radix selection over the dense scores bit for bit."""
     k = 300
-    cfg = workloads.scaled(workloads.CONFIGS["dsa_bf16_128k"], nq=nq, nk=nk)
+    cfg = workloads.scaled(workloads.CONFIGS[base], nq=nq, nk=nk)
     x = workloads.generate(cfg, seed=37)
     gi, gs, st = _fused(x, k, "dsa", sorted_output=True, force_fallback=True)
     np.testing.assert_array_equal(st[:, 2], 3)
     d = to_dev(x)
-    dense = lt.indexer_scores(d["q"], d["w"], d["keys"], mode="dsa")
+    dense = lt.indexer_scores(d["q"], d["w"], d["keys"], d["q_scale"], d["k_scale"], mode="dsa")
     ri, rs = lt.topk_radix(dense, k, causal_offsets=d["offsets"], sorted_output=True)
     torch.cuda.synchronize()
     np.testing.assert_array_equal(gi, ri.cpu().numpy())
     np.testing.assert_array_equal(gs.view(np.uint32), rs.cpu().numpy().view(np.uint32))
-    _check_tol(x, "bf16", k, "dsa", gi, gs, rows=[0, nq // 2, nq - 1])
+    _check_tol(x, cfg.dtype, k, "dsa", gi, gs, rows=[0, nq // 2, nq - 1])
