@@ -109,9 +109,10 @@ hipError_t launch_fused_scan(const ScoreArgs& a, const RowParam* params, int S, 
                              int k, int* pub, uint32_t* cnt, uint32_t* hist, int2* cand, const int32_t* rflag,
                              const uint32_t* qctl, hipStream_t st);
 // Exact fallback for queued rows (queue, length qctl[0]): dense re-score
-// into scratch rows of nk floats (`slots` of them), then radix select. Both
-// fallback kernels run kFallbackGrid blocks in one of three modes, chosen on
-// the device from the queue length n:
+// into scratch rows of nk floats (`slots` of them), then radix select. The
+// fallback kernel runs kFallbackGrid blocks in one of three modes (the wide
+// scan's, in the split or whole-row mode), chosen on the device from the
+// queue length n:
 // * split (fallback_chunks(...) > 1: few rows, each with its own scratch
 //   row): the visible keys of every queued row are cut into that many chunks,
 //   one block per (row, chunk), which also selects its chunk's top-k into
