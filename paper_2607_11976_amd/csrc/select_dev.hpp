@@ -67,8 +67,16 @@ constexpr size_t kRadixTot = (size_t)kRadixWaves * 256 * 4;
 constexpr size_t kRadixTmp = kRadixTot + 256 * 4;
 constexpr size_t kRadixEnt = kRadixTmp + 32 * 4;
 
+// Sort entries of radix_select_row: the output sort (k of them) and the keys
+// of a digit prefix gathered in LDS once at most this many remain.
+__host__ __device__ __forceinline__ int radix_collect_cap(int k) {
+  const int p = next_pow2(k);
+  return p < 4096 ? 4096 : p;
+}
 // LDS bytes radix_select_row needs for a given k.
-__host__ __device__ __forceinline__ size_t radix_lds_bytes(int k) { return kRadixEnt + (size_t)next_pow2(k) * 8; }
+__host__ __device__ __forceinline__ size_t radix_lds_bytes(int k) {
+  return kRadixEnt + (size_t)radix_collect_cap(k) * 8;
+}
 
 // Sort the first n (<= k) entries of an output row by the total order, in
 // place. The rows were written by this block; the caller has made them
@@ -92,7 +100,11 @@ __device__ __forceinline__ void sort_output_row(int32_t* oi, float* os, int n, u
 // Exact top-k of row[0, n) by (score desc, index asc), written to oi/os
 // (k entries, padded with (-1, -inf)). Plain most-significant-digit radix
 // selection over the order keys: four 8-bit passes find the k-th key K*, then
-// one pass writes every key > K* and the lowest-index keys == K*. Each wave
+// one pass writes every key > K* and the lowest-index keys == K*. Once at
+// most radix_collect_cap(k) keys share the digits chosen so far (before any
+// pass for rows that short), one last pass instead writes the keys above
+// those digits and gathers the keys with them in LDS, which are sorted there
+// by the total order; the best of them fill the remaining slots. Each wave
 // streams a contiguous segment of the row (wave_stream) into its own
 // histogram; the passes after the first test a key's prefix as a float range
 // and the write pass compares floats with K*'s float (the order keys of the
@@ -100,7 +112,9 @@ __device__ __forceinline__ void sort_output_row(int32_t* oi, float* os, int n, u
 // above the pass's digit, so that after the last pass every wave knows how
 // many keys > K* and == K* lie in the segments before its own, and the write
 // pass places each hit without block barriers.
-// Output order: ascending key index, or the total order when `sorted`.
+// Output order: ascending key index (after a gathering pass: the keys above
+// the gathered digits in ascending key index, then the gathered ones in the
+// total order), or the total order when `sorted`.
 // pad = false: a row of n < k keys writes its n entries and nothing after.
 template <int NTH>
 __device__ __noinline__ void radix_select_row_at(const float* row, int n, int k, int32_t* oi, float* os, bool sorted,
@@ -159,7 +173,8 @@ __device__ __forceinline__ void split_fallback_select(const float* srow, int rs,
 // atomic per bin. Measured on MI355X, one row of 262144 / 1M / 4M keys per
 // 256-thread block: 0.41 / 1.5 / 5.7 ms with 16 keys and the next step in
 // flight (0.72 / 2.6 / 10.1 ms before, with 32 plain loads per step and no
-// look-ahead; 24 or 32 keys per step, no faster); without the grouped first
+// look-ahead; 24 or 32 keys per step, no faster), 0.36 / 1.3 / 4.9 ms with
+// the gathering pass in place of the last passes; without the grouped first
 // pass the dense fallback of concentrated scores is 5% slower, four grouped
 // bins in two passes slower too.
 #ifndef LT_RADIX_UNROLL
@@ -278,7 +293,59 @@ __device__ __noinline__ void radix_select_row_at(const float* row, int n, int k,
   uint32_t prefix = 0, pmask = 0, remaining = (uint32_t)k;
   uint32_t gbefore = 0;  // this wave's keys above the digits chosen so far (wave-uniform)
   uint32_t eqw = 0;      // this wave's keys == K* (after the last pass)
+  uint32_t inbin = (uint32_t)n;  // keys with the digits chosen so far
+  const uint32_t cap = (uint32_t)radix_collect_cap(k);
+  bool collected = false;
   for (int pass = 0; pass < 4; ++pass) {
+    if (inbin <= cap) {  // wave-uniform
+      // Few keys left with the chosen digits: one last pass writes the keys
+      // above them to the output (after those of lower waves, counted by
+      // gbefore) and gathers them in LDS as (key, index) sort entries; the
+      // best `remaining` of those, by the total order, fill the last slots.
+      if (l == 0) tmp[wave] = gbefore;
+      if (tid == 0) tmp[18] = 0u;
+      __syncthreads();
+      uint32_t g = 0;
+      for (int w = 0; w < wv; ++w) g += tmp[w];
+      wave_stream<U>(row, s0, s1, [&](int c0, const float (&x)[U]) {
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+          const int i = c0 + u * kWave + l;
+          const bool v = i < s1;
+          const uint32_t kp = ord_key(x[u]) & pmask;
+          const bool ab = v & (kp > prefix), in = v & (kp == prefix);
+          const uint64_t ma = __ballot(ab), mi = __ballot(in);
+          if (ab) {
+            const uint32_t p = g + mbcnt64(ma);
+            oi[p] = i;
+            os[p] = x[u];
+          }
+          g += (uint32_t)__popcll(ma);
+          if (mi != 0) {  // wave-uniform: one slot reservation for the wave's keys
+            const int lead = (int)__builtin_ctzll(mi);
+            uint32_t base = 0u;
+            if (l == lead) base = atomicAdd(&tmp[18], (uint32_t)__popcll(mi));
+            base = (uint32_t)__builtin_amdgcn_readlane((int)base, lead);
+            const uint32_t sl = base + mbcnt64(mi);
+            if (in && sl < cap) ent[sl] = comp_key(x[u], (uint32_t)i);
+          }
+        }
+      });
+      __syncthreads();
+      const uint32_t cnt = min(tmp[18], cap);
+      const int P = next_pow2(cnt < 1u ? 1 : (int)cnt);
+      for (int j = (int)cnt + tid; j < P; j += NTH) ent[j] = 0ull;
+      __syncthreads();
+      bitonic_sort_desc<NTH>(ent, P);
+      const uint32_t first = (uint32_t)k - remaining;
+      for (uint32_t j = tid; j < remaining; j += NTH) {
+        const uint32_t idx = comp_pos(ent[j]);
+        oi[first + j] = (int32_t)idx;
+        os[first + j] = row[idx];
+      }
+      collected = true;
+      break;
+    }
     const int shift = 24 - 8 * pass;
     for (int b = tid; b < NW * 256; b += NTH) hist[b] = 0;
     __syncthreads();
@@ -352,6 +419,7 @@ __device__ __noinline__ void radix_select_row_at(const float* row, int n, int k,
     // and a choice the compiler cannot see as wave-uniform becomes a masked
     // branch around loops whose loads then all wait for each other)
     const uint32_t d = __builtin_amdgcn_readfirstlane(tmp[16]), above = __builtin_amdgcn_readfirstlane(tmp[17]);
+    const uint32_t nbin = __builtin_amdgcn_readfirstlane(tot[d]);
     // this wave's keys of the current prefix in bins above d (and == d)
     uint32_t mine = 0;
     for (int b = l; b < 256; b += kWave) mine += (uint32_t)b > d ? hw[b] : 0u;
@@ -361,6 +429,15 @@ __device__ __noinline__ void radix_select_row_at(const float* row, int n, int k,
     remaining -= above;
     prefix |= d << shift;
     pmask |= 0xFFu << shift;
+    inbin = nbin;
+  }
+  if (collected) {  // block-uniform
+    if (sorted) {
+      __threadfence_block();
+      __syncthreads();
+      sort_output_row<NTH>(oi, os, k, ent, fetch);
+    }
+    return;
   }
   const uint32_t kstar = prefix, need = remaining;
   if (l == 0) {
