@@ -75,9 +75,9 @@ COPY_FACTOR = (0.5000, 1.0000)
 # the query count they give the bytes written per query.
 WRITE_KIB = {
     "dsa_bf16_128k": {"fused": {"k_sample": 98304.0, "k_fused": 281894.6, "k_select": 65776.4},
-                      "unfused": {"k_dense": 2097152.0, "k_radix": 73729.5}},
+                      "unfused": {"k_dense": 2097152.0, "k_radix": 70735.7}},
     "dsa_fp8_1m": {"fused": {"k_sample": 49152.0, "k_fused": 209557.7, "k_select": 32879.8},
-                   "unfused": {"k_dense": 8388608.0, "k_radix": 97273.2}},
+                   "unfused": {"k_dense": 8388608.0, "k_radix": 86124.8}},
 }
 
 
