@@ -403,10 +403,88 @@ __device__ __forceinline__ void select_row(int row, RowParam* params, const uint
     return;
   }
 
-  // ---- 2./3. one ordered pass over the candidates ----
+  // ---- 2./3. one pass over the candidates ----
   uint32_t run_above = 0, run_tie = 0;
   bool tie_ovf = false;
-  for (int g0 = 0; g0 < S; g0 += NTH) {
+  if (keyed) {
+    // The final sort puts the keys above bin tau in order and bin tau's
+    // entries carry their keys, so no position needs the list order: each
+    // wave takes whole lists, four at a time when there are enough (16 lanes
+    // on 16 consecutive positions of each, one 128-byte chunk), with PER
+    // loads in flight per lane, and reserves output slots with one LDS
+    // atomic per kind and step. No block-wide step, no search for a
+    // position's list.
+    constexpr int NW = NTH / kWave;
+    const int wave = tid / kWave, l = lane_id();
+    const int lpw = S >= 4 * NW ? 4 : 1;  // lists a wave takes at once
+    const int ll = kWave / lpw, sub = l / ll, lo = l - sub * ll;
+    if (tid == 0) {
+      tmp[26] = 0u;
+      tmp[27] = 0u;
+    }
+    __syncthreads();
+    for (int s0 = wave * lpw; s0 < S; s0 += NW * lpw) {
+      const int s = s0 + sub;
+      const int64_t li = (int64_t)row * S + s;
+      const uint32_t c = s < S ? min(cnt[li], (uint32_t)cap) : 0u;
+      // the wave steps through the longest of its lists
+      uint32_t cmax = 0u;
+      for (int g = 0; g < lpw; ++g) cmax = max(cmax, (uint32_t)__builtin_amdgcn_readlane((int)c, g * ll));
+      for (uint32_t p0 = 0; p0 < cmax; p0 += (uint32_t)(PER * ll)) {
+        int2 ce[PER];
+#pragma unroll
+        for (int u = 0; u < PER; ++u) {
+          const uint32_t pos = p0 + (uint32_t)(u * ll + lo);
+          ce[u] = make_int2(0, 0);
+          if (pos < c) ce[u] = cand[ilv ? ilv_index(li, pos, (int64_t)nq * S) : li * cap + pos];
+        }
+        // bit u: entry u is above bin tau (ab) / in it (ti); the wave masks
+        // are taken again where they are used, to keep few of them live
+        uint32_t ab = 0u, ti = 0u, na = 0u, nt = 0u;
+#pragma unroll
+        for (int u = 0; u < PER; ++u) {
+          const bool v = p0 + (uint32_t)(u * ll + lo) < c;
+          const int b = bin_of(bin_x(__int_as_float(ce[u].y), p.delta, p.c), m);
+          const bool a1 = v & (b > tau), t1 = v & (b == tau);
+          ab |= (uint32_t)a1 << u;
+          ti |= (uint32_t)t1 << u;
+          na += (uint32_t)__popcll(__ballot(a1));
+          nt += (uint32_t)__popcll(__ballot(t1));
+        }
+        uint32_t ba = 0u, bt = 0u;
+        if (l == 0) {
+          if (na) ba = atomicAdd(&tmp[26], na);
+          if (nt) bt = atomicAdd(&tmp[27], nt);
+        }
+        ba = (uint32_t)__builtin_amdgcn_readfirstlane((int)ba);
+        bt = (uint32_t)__builtin_amdgcn_readfirstlane((int)bt);
+#pragma unroll
+        for (int u = 0; u < PER; ++u) {
+          const bool a1 = (ab >> u) & 1u, t1 = (ti >> u) & 1u;
+          const uint64_t ma = __ballot(a1), mt = __ballot(t1);
+          if (a1) {
+            const uint32_t r = ba + mbcnt64(ma);
+            if (r < (uint32_t)k) {
+              oi[r] = ce[u].x;
+              os[r] = __int_as_float(ce[u].y);
+            }
+          }
+          if (t1) {
+            const uint32_t r = bt + mbcnt64(mt);
+            if (r < (uint32_t)E) ent[r] = comp_key(__int_as_float(ce[u].y), (uint32_t)ce[u].x);
+          }
+          ba += (uint32_t)__popcll(ma);
+          bt += (uint32_t)__popcll(mt);
+        }
+      }
+    }
+    __syncthreads();
+    run_above = tmp[26];
+    run_tie = tmp[27];
+  }
+  // lists in key order: one block-wide pass in list order, so that a
+  // position in the concatenated lists orders equal scores by key
+  for (int g0 = 0; g0 < (keyed ? 0 : S); g0 += NTH) {
     // offsets of the group's lists in their concatenation
     const int sg = g0 + tid;
     const uint32_t cg = sg < S ? min(cnt[(int64_t)row * S + sg], (uint32_t)cap) : 0u;
@@ -457,8 +535,8 @@ __device__ __forceinline__ void select_row(int row, RowParam* params, const uint
         ab[j] = ti[j] = false;
         gpos[j] = 0;
         if (i < gtot) {
-          // increases with the key index (keyed: it is the key index)
-          gpos[j] = keyed ? (uint32_t)ce[j].x : (uint32_t)(g0 + lst[j]) * (uint32_t)cap + (i - off[lst[j]]);
+          // the list position, which increases with the key index
+          gpos[j] = (uint32_t)(g0 + lst[j]) * (uint32_t)cap + (i - off[lst[j]]);
           const int b = bin_of(bin_x(__int_as_float(ce[j].y), p.delta, p.c), m);
           ab[j] = b > tau;
           ti[j] = b == tau;
