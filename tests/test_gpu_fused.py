@@ -92,6 +92,21 @@ def test_fused_equals_select_over_dense_scores(lib, base):
     np.testing.assert_array_equal(fs.view(np.uint32), ss.cpu().numpy().view(np.uint32))
 
 
+@pytest.mark.parametrize("ns", [16384, 32768])
+def test_long_sample_same_results(lib, ns):
+    # samples of 16384 to 32768 keys (the range stage's wide blocks): results
+    # equal the default sample's
+    cfg = workloads.scaled(workloads.CONFIGS["dsa_bf16_128k"], nq=10, nk=40000)
+    k = 256
+    x = workloads.generate(cfg, seed=21)
+    ref = _fused(x, k, "dsa", sorted_output=True)
+    got = _fused(x, k, "dsa", sorted_output=True, sample_size=ns)
+    np.testing.assert_array_equal(got[0], ref[0])
+    np.testing.assert_array_equal(got[1].view(np.uint32), ref[1].view(np.uint32))
+    _check_tol(x, "bf16", k, "dsa", got[0], got[1])
+    assert np.all(got[2][:, 2] == 0)
+
+
 @pytest.mark.parametrize("opt", [
     dict(force_fallback=True),
     dict(capacity=64),

@@ -100,6 +100,16 @@ def test_select_forced_paths_are_still_exact(lib, opt):
         assert np.all(stats[:, 2] == 1)
 
 
+@pytest.mark.parametrize("ns", [16384, 32768])
+def test_select_long_sample(lib, ns):
+    # samples of 16384 to 32768 keys (the range stage's wide blocks)
+    nq, nk, k = 12, 40000, 300
+    scores = workloads.score_rows(nq, nk, seed=9, kind="ties")
+    offs = workloads.causal_offsets(nq, nk)
+    gi, gs, stats = _run(scores, nk, k, offs, "select", sorted_output=True, sample_size=ns)
+    _check_all(scores, nk, k, offs, gi, gs, True)
+
+
 def test_select_row_stats_invariants(lib):
     """Invariants of the filter (sec. 3.2): the final threshold bin leaves
     fewer than k candidates above it, survivors stay below capacity, and the
