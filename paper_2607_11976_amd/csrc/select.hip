@@ -600,7 +600,7 @@ __device__ __forceinline__ void select_row(int row, RowParam* params, const uint
     for (int i = tid; i < P; i += NTH)
       if ((uint32_t)i >= nent) ent[i] = 0ull;
     __syncthreads();
-    bitonic_sort_desc<NTH>(ent, P);
+    bitonic_sort_desc_fast<NTH>(ent, P);
     for (uint32_t i = tid; i < take; i += NTH) emit(i, ent[i]);
   }
   for (uint32_t i = c_above + take + tid; i < (uint32_t)k; i += NTH) {
@@ -628,7 +628,7 @@ __device__ __forceinline__ void select_row(int row, RowParam* params, const uint
     for (int i = tid; i < P; i += NTH)
       if ((uint32_t)i >= nout) ent[i] = 0ull;
     __syncthreads();
-    bitonic_sort_desc<NTH>(ent, P);
+    bitonic_sort_desc_fast<NTH>(ent, P);
     for (uint32_t i = tid; i < nout; i += NTH) {
       const uint32_t g = comp_pos(ent[i]);
       if (keyed) {
